@@ -1,0 +1,195 @@
+"""Benchmark: tree-shared decode attention on one MI355X, against the HBM roofline on unique KV bytes.
+
+    python bench.py [--steps K] [--warmup W] [--workload beam_decode] [--gpus 1] [--no-cpu]
+
+A step is one tkv_decode (or tkv_verify) call over the whole batch: the shared-segment and
+private-suffix contractions of every row and the log-sum-exp merge.  The block manager has built
+the tree, rows are coalesced and the plan is built and uploaded before timing (host times are
+reported beside the result).  Inputs are resident in HBM when the timed region starts; the
+K/V pool is rotated over several device copies so that no step finds it in the 256 MB
+Infinity Cache.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+MALL_BYTES = 256 << 20
+
+
+def _args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="beam_decode")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU baseline sample")
+    ap.add_argument("--traffic", default=None, help="JSON file with measured per-launch HBM bytes of the main kernel")
+    return ap.parse_args()
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus N with N > 1 is not supported "
+                                   "(the path shards by query tree with no exchange, see DESIGN.md)"}))
+        sys.exit(2)
+    import torch
+    import paper_2609_39334_amd as tkv
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU"}))
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    wl = W.CONFIGS[a.workload](a.seed)
+    s = wl.shape
+    launch = len(wl.launches) - 1            # the last launch is the measured one (mixed: after prune)
+
+    # ------------------------------------------------------------------ host side: tree, rows, plan
+    t0 = time.perf_counter()
+    bm = tkv.BlockManager(wl.num_blocks, s.block_size, wl.max_seqs)
+    cap = {}
+    W.drive(wl, bm, on_launch=lambda i, l, c: cap.__setitem__(i, (l, c)))
+    t_bm = time.perf_counter() - t0
+    L, cands = cap[launch]
+    seqs = [x for x, _ in cands]
+    qls = [q for _, q in cands]
+    t0 = time.perf_counter()
+    _, first, mult = bm.coalesce(seqs, qls)
+    t_coal = time.perf_counter() - t0
+    tables = [bm.table(seqs[c]) for c in first]
+    q_lens = [qls[c] for c in first]
+    bl = bm.block_len()
+    qi = np.concatenate([[0], np.cumsum(q_lens)]).astype(np.int32)
+    ki = np.concatenate([[0], np.cumsum([len(t) for t in tables])]).astype(np.int32)
+    kb = np.concatenate(tables).astype(np.int32)
+    n_qtok = int(qi[-1])
+    t0 = time.perf_counter()
+    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, bl, mult, device=dev)
+    torch.cuda.synchronize()
+    t_plan = time.perf_counter() - t0
+    st = plan.stats
+
+    # ------------------------------------------------------------------ device inputs
+    kbits, vbits = wl.kv_values()
+    qbits = wl.q_values(launch, n_qtok)
+
+    def to_dev(x):
+        return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    k0, v0 = to_dev(kbits), to_dev(vbits)
+    pool_bytes = 2 * k0.numel() * 2
+    n_copies = max(2, math.ceil(4 * MALL_BYTES / pool_bytes) + 1)
+    ks = [k0] + [k0.clone() for _ in range(n_copies - 1)]
+    vs = [v0] + [v0.clone() for _ in range(n_copies - 1)]
+    q = to_dev(qbits)
+    o = torch.empty((n_qtok, s.hq, s.d), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((n_qtok, s.hq), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    call = plan.decode if L.decode else plan.verify
+
+    for i in range(a.warmup):
+        call(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
+    torch.cuda.synchronize()
+    tkv.tkv_plan_profile(plan.h, a.steps)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(a.steps):
+        call(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    n_rec, ms_main, ms_merge = tkv.tkv_plan_profile_read(plan.h)
+    tkv.tkv_plan_profile(plan.h, 0)
+    ms_step = ms_total / a.steps
+    t_main = ms_main / max(1, n_rec) / 1e3
+    t_merge = ms_merge / max(1, n_rec) / 1e3
+
+    # ------------------------------------------------------------------ accounting
+    b_uniq = st["uniq_kv_tokens"] * s.hkv * s.d * 2 * 2            # K and V, bf16
+    flops = st["flops"]
+    cand_tok_s = n_qtok / (ms_step / 1e3)
+    achieved_gbs = b_uniq / t_main / 1e9
+    traffic = None
+    if a.traffic and os.path.exists(a.traffic):
+        with open(a.traffic) as f:
+            tr = json.load(f)
+        if tr.get("workload") == a.workload:
+            traffic = tr.get("bytes_per_launch")
+    roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": "attn_items", "algorithmic_bytes": b_uniq, "kernel_us": round(t_main * 1e6, 2)}
+
+    # ------------------------------------------------------------------ CPU baseline (oracle)
+    cpu = None
+    if not a.no_cpu:
+        import oracle
+        try:
+            from threadpoolctl import threadpool_info
+            blas_threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
+        except Exception:
+            blas_threads = None
+        kf, vf = W.bf16_bits_to_f32(kbits), W.bf16_bits_to_f32(vbits)
+        qf = W.bf16_bits_to_f32(qbits).astype(np.float64)
+        order = np.random.default_rng(0).permutation(len(tables))
+        done_rows, done_tok, t_cpu = [], 0, 0.0
+        for r in order:                                   # grow the sample until the time target
+            t0 = time.perf_counter()
+            oracle.attention(qf, kf, vf, tables, bl, q_lens, rows=[int(r)])
+            t_cpu += time.perf_counter() - t0
+            done_rows.append(int(r))
+            done_tok += q_lens[r]
+            if t_cpu >= a.cpu_seconds:
+                break
+        cpu = {"value": round(done_tok / t_cpu, 2), "unit": "candidate-tokens/s",
+               "cores": blas_threads or len(os.sched_getaffinity(0)), "kind": "oracle",
+               "host_cpus": len(os.sched_getaffinity(0)),
+               "sample": f"{len(done_rows)} of {len(tables)} rows ({done_tok} query tokens), fp64 NumPy gather "
+                         f"attention, {t_cpu:.1f} s"}
+
+    out = {
+        "metric": "candidate-tokens/s and % HBM roofline (unique KV bytes), tree decode + verify",
+        "value": round(cand_tok_s, 1),
+        "unit": "candidate-tokens/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded trees, N(0,1) bf16 values)",
+        "config": {"workload": a.workload, "hq": s.hq, "hkv": s.hkv, "head_dim": s.d, "block_size": s.block_size,
+                   "rows": st["n_rows"], "query_tokens": n_qtok, "logical_candidate_tokens": st["logical_qtok"],
+                   "decode": bool(L.decode), "unique_kv_bytes": b_uniq,
+                   "per_row_kv_bytes": st["path_kv_tokens"] * s.hkv * s.d * 4,
+                   "kv_pool_copies_rotated": n_copies},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "hbm_frac_whole_call": round(b_uniq / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+        "mfma_frac_whole_call": round(flops / (ms_step / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "logical_candidate_tokens_per_s": round(st["logical_qtok"] / (ms_step / 1e3), 1),
+        "kernel_us": {"attn_items": round(t_main * 1e6, 2), "merge_partials": round(t_merge * 1e6, 2)},
+        "plan": {"items": st["n_items"], "shared_items": st["n_items_shared"], "row_items": st["n_items_row"],
+                 "partial_slots": st["n_slots"], "merged_tokens": st["n_merge"], "segments": st["n_segments"],
+                 "shared_segments": st["n_shared_segments"]},
+        "host_ms": {"block_manager": round(t_bm * 1e3, 2), "coalesce": round(t_coal * 1e3, 3),
+                    "plan_and_upload": round(t_plan * 1e3, 2)},
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

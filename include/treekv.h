@@ -1,0 +1,207 @@
+/*
+ * treekv.h -- C ABI of libtreekv.so: tree-shared paged attention for speculative
+ * expand-verify-select search on AMD Instinct MI355X (gfx950).
+ *
+ * The problem (SpecScale, arXiv 2609.39334): a beam search with a process reward model keeps a
+ * tree of candidate reasoning paths (Sec. 2.2).  Speculation multiplies the live candidates and
+ * the decode work (Sec. 3.2.1) and fragments verification (Sec. 3.2.2); computation
+ * deduplication runs one forward pass per distinct prefix (Sec. 4.2); early pruning releases
+ * losers (Sec. 4.1).  All candidates read one paged KV cache with prefix sharing (Sec. 5.1).
+ * This library provides, for one attention layer:
+ *   - a prefix-tree KV block manager with refcounted, deduplicated step blocks (host, integer);
+ *   - row coalescing of identical candidates (host, integer);
+ *   - a planner that turns per-row block tables into shared segments and a device work list;
+ *   - decode (q_len 1) and verify (q_len >= 1, causal within the step) attention on the GPU.
+ *
+ * Conventions
+ *   - Every function returns TKV_OK (0) or a negative TKV_E* code; nothing throws or aborts across
+ *     the ABI.  tkv_last_error() returns a message for the last failure on the calling thread.
+ *   - Host arrays are read during the call only (copied where kept).  Device pointers are
+ *     caller-owned (e.g. PyTorch tensors); the library never frees caller memory.
+ *   - Device work is enqueued on the caller's hipStream_t (passed as void*, NULL = default
+ *     stream) and is asynchronous; the caller keeps buffers alive until the stream reaches it.
+ *   - bf16 is IEEE bfloat16 bit patterns (uint16); fp32 is IEEE binary32.
+ *   - Handles (tkv_bm, tkv_plan) are not thread-safe; use one thread per handle.
+ */
+#ifndef TREEKV_H
+#define TREEKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    TKV_OK = 0,
+    TKV_EINVAL = -1, /* bad argument, shape, id or state */
+    TKV_ENOMEM = -2, /* no free KV block or sequence slot (state unchanged), or host allocation failed */
+    TKV_ENOSEQ = -3, /* sequence id not live */
+    TKV_ECAP = -4,   /* caller output buffer too small; the n_*_out argument reports the size needed */
+    TKV_EHIP = -5    /* a HIP runtime call failed; message names the call */
+};
+
+/* Message of the most recent call on this thread ("" if it succeeded).  Valid until the next call. */
+const char* tkv_last_error(void);
+
+/* ======================================================================== block manager
+ * Prefix tree of reasoning-step blocks over one paged pool (paged attention and prefix sharing,
+ * Sec. 5.1; identical prefixes share KV and computation, Sec. 4.2).  Rules (exact, no hashing
+ * decides anything):
+ *   - Step-aligned blocks: each extension starts a fresh block; n tokens take ceil(n/block_size)
+ *     blocks, the last possibly partial.
+ *   - Dedup key of a chunk = (preceding block id in the path, or -1 at a root; exact tokens).  A chunk
+ *     of a sealed extension reuses the live sealed block with that key (hit); otherwise it takes
+ *     the lowest free block id (miss).  Unsealed chunks never hit and are never indexed.
+ *   - refcount(b) = number of live sequences whose table holds b; a block is freed and unindexed
+ *     when it reaches 0.  New sequence ids are the lowest free id.
+ * Host-only; no device memory is touched.
+ */
+typedef struct tkv_bm tkv_bm;
+
+/* num_blocks >= 1 pool blocks, block_size >= 1 tokens per block (the attention path needs 16),
+ * max_seqs >= 1 live sequences.  *out receives the handle.  EINVAL, ENOMEM. */
+int tkv_bm_create(int32_t num_blocks, int32_t block_size, int32_t max_seqs, tkv_bm** out);
+void tkv_bm_destroy(tkv_bm* bm);
+
+/* New sequence = parent's path + tokens[0..n).  parent = -1 starts a root (needs n >= 1).
+ * seal = 1: a completed step (chunks are deduplicated and indexed); seal = 0: an in-progress step
+ * (private chunks; the sequence cannot be extended).  Outputs: *child_out = new sequence id;
+ * blk_out[0..*n_blk_out) = the ids of the new step's blocks in order and hit_out[] = 1 where the
+ * block was reused (the caller writes K/V only where hit_out is 0).  cap = capacity of blk_out and
+ * hit_out.  Errors: EINVAL (n < 0, root without tokens, parent unsealed, seal not 0/1, NULL
+ * pointers), ENOSEQ (parent not live), ENOMEM (too few free blocks or no sequence slot), ECAP
+ * (cap < ceil(n/block_size); *n_blk_out = that size).  On error nothing changes. */
+int tkv_bm_extend(tkv_bm* bm, int32_t parent, const int32_t* tokens, int32_t n, int32_t seal,
+                  int32_t* child_out, int32_t* blk_out, uint8_t* hit_out, int32_t cap, int32_t* n_blk_out);
+
+/* Release a sequence (early pruning, Sec. 4.1): refcounts of its table drop by one in table order;
+ * blocks reaching 0 are freed and written to freed_out[0..*n_freed_out) in that order.  cap =
+ * capacity of freed_out; ECAP (nothing changes) if it could be too small, i.e. if cap is below the
+ * sequence's table length (*n_freed_out = that length).  ENOSEQ if seq is not live. */
+int tkv_prune(tkv_bm* bm, int32_t seq, int32_t* freed_out, int32_t cap, int32_t* n_freed_out);
+
+/* Block table of a live sequence: blk_out[0..*n_out), *kv_len_out = sum of block lengths.
+ * ENOSEQ, ECAP (*n_out = table length). */
+int tkv_bm_table(const tkv_bm* bm, int32_t seq, int32_t* blk_out, int32_t cap, int32_t* n_out,
+                 int32_t* kv_len_out);
+
+/* Reference count of one block (0 = free).  EINVAL if blk is out of range. */
+int tkv_bm_refcount(const tkv_bm* bm, int32_t blk, int32_t* rc_out);
+
+/* Token count of every block, len_out[0..num_blocks) (0 = free).  This is the block_len array
+ * that tkv_plan_create takes. */
+int tkv_bm_block_len(const tkv_bm* bm, int32_t* len_out);
+
+/* Whole state as int32 words, for bit-exact comparison in tests:
+ *   num_blocks, block_size, max_seqs, n_live,
+ *   refcount[num_blocks], block_len[num_blocks], indexed[num_blocks] (0/1),
+ *   then per live sequence in ascending id: seq, sealed, n, table[n].
+ * *used = bytes needed; ECAP if cap < *used (buf may be NULL to query the size). */
+int tkv_bm_snapshot(const tkv_bm* bm, void* buf, size_t cap, size_t* used);
+
+/* Computation deduplication at the attention boundary (Sec. 4.2: one forward pass per distinct
+ * prefix, with a potential size standing for identical candidates): candidates with identical
+ * block tables and equal q_len become one row.  Rows are numbered by first appearance.
+ * Outputs: row_of_cand_out[n_cand], first_cand_out[*n_rows_out] (first candidate of each row),
+ * mult_out[*n_rows_out] (multiplicity); the two row arrays need room for n_cand entries.
+ * ENOSEQ for a dead sequence, EINVAL for q_len < 1 or NULL pointers. */
+int tkv_bm_coalesce(const tkv_bm* bm, int32_t n_cand, const int32_t* seqs, const int32_t* q_len,
+                    int32_t* row_of_cand_out, int32_t* first_cand_out, int32_t* mult_out,
+                    int32_t* n_rows_out);
+
+/* ======================================================================== attention
+ * One attention layer over the paged cache for a batch of rows (Sec. 2.1 attention; decode of
+ * every live candidate, Sec. 3.2.1; prefill-only step verification, Sec. 3.2.2).  For row r with
+ * block table T, q_len L and kv_len N = sum of block_len over T, query token i (0 <= i < L) and
+ * query head h (kv head h / (hq/hkv)) attend keys 0 .. N-L+i of the path (bottom-right causal;
+ * decode is L = 1 and sees all N keys):
+ *   o[i,h] = softmax(q[i,h] . K^T / sqrt(d)) V,   lse[i,h] = natural log of the softmax denominator
+ * computed from bf16 inputs with fp32 accumulation; o is rounded to bf16 (nearest even).
+ *
+ * Device layouts (row-major, contiguous):
+ *   q, o   [n_qtok][hq][d] bf16, rows' query tokens concatenated in q_indptr order
+ *   k, v   [num_blocks][hkv][block_size][d] bf16 (the paged pool; slots past a block's length are
+ *          never read)
+ *   lse    [n_qtok][hq] fp32, nullable
+ * Supported: block_size 16, d in {64, 128}, hq % hkv == 0, hq / hkv <= 64.
+ */
+typedef struct {
+    int32_t hq, hkv, d, block_size, num_blocks;
+} tkv_shape;
+
+typedef struct tkv_plan tkv_plan;
+
+/* Build the work plan on the host (host arrays are copied):
+ *   n_rows >= 0 rows; q_indptr[n_rows+1] offsets of each row's query tokens (q_indptr[0] = 0);
+ *   kv_indptr[n_rows+1] offsets into kv_blocks; kv_blocks = the rows' block tables in path order;
+ *   block_len[num_blocks] = tokens per block (tkv_bm_block_len); multiplicity[n_rows] = logical
+ *   candidates per row (nullable: all 1; used for accounting only).
+ * The planner finds the blocks that several rows share (a trie over the tables) so that each
+ * shared K/V block is contracted against all query rows that reference it, splits long runs,
+ * and lays out descriptors for the device.  EINVAL: bad shape, q_len < 1, q_len > kv_len, a block
+ * id out of range or with block_len outside [1, block_size], multiplicity < 1. */
+int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
+                    const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
+                    const int32_t* multiplicity, tkv_plan** out);
+
+/* Device workspace the plan needs (descriptors + partial results), in bytes (>= 256). */
+size_t tkv_plan_workspace_bytes(const tkv_plan* plan);
+
+/* Copy the plan's descriptors into d_workspace (device memory of >= tkv_plan_workspace_bytes,
+ * 256-byte aligned, caller-owned) on hip_stream; the plan keeps using that workspace until the
+ * next upload.  The plan must outlive the copy.  EINVAL (size, alignment, NULL), EHIP. */
+int tkv_plan_upload(tkv_plan* plan, void* d_workspace, size_t bytes, void* hip_stream);
+
+void tkv_plan_destroy(tkv_plan* plan);
+
+/* Counts for accounting and tests. */
+typedef struct {
+    int32_t n_rows, n_qtok, n_items, n_items_shared, n_items_row, n_slots, n_merge;
+    int32_t n_segments, n_shared_segments;
+    int64_t logical_qtok;   /* sum of multiplicity * q_len */
+    int64_t uniq_kv_tokens; /* tokens in the union of the rows' blocks */
+    int64_t path_kv_tokens; /* sum over rows of kv_len (what per-row gathering would read) */
+    int64_t flops;          /* 4 * d * hq * sum over query tokens of visible keys */
+} tkv_plan_stats;
+int tkv_plan_get_stats(const tkv_plan* plan, tkv_plan_stats* out);
+
+/* Read-only view of the plan's host descriptor arrays (valid until tkv_plan_destroy), for tests
+ * and tools.  Formats (int32 words):
+ *   items[n_items][8]  {kv_head, tok_off, n_tok, blk_off, n_blk, pos0, kind (0 shared, 1 row), 0}
+ *   toks[n_toks][4]    {query token, largest visible key position, partial slot or -1, 0}
+ *   blks[n_blks][2]    {block id, block length}
+ *   merges[n_merge][4] {query token, offset into merge_slots, slot count, 0}
+ * An item contracts the G query heads of KV head kv_head of toks[tok_off .. +n_tok) against the
+ * keys of blks[blk_off .. +n_blk) (positions pos0, pos0+1, ... along the path).  A token with slot
+ * -1 gets its final output from that item; otherwise the merge entry of the token combines its
+ * partial slots (n_slots of them in the workspace). */
+typedef struct {
+    const int32_t *items, *toks, *blks, *merges, *merge_slots;
+    int32_t n_items, n_toks, n_blks, n_merge, n_merge_slots, n_slots;
+} tkv_plan_view;
+int tkv_plan_get_view(const tkv_plan* plan, tkv_plan_view* out);
+
+/* Attention for an uploaded plan.  tkv_decode requires every row's q_len == 1 (EINVAL
+ * otherwise); tkv_verify takes any q_len >= 1 (causal), including batches that mix decode and
+ * verify rows.  Enqueued on hip_stream; calls that share one plan's workspace must not overlap.
+ * EINVAL (not uploaded, NULL pointers), EHIP (launch failure). */
+int tkv_decode(const tkv_plan* plan, const void* q, const void* k, const void* v, void* o,
+               float* lse, void* hip_stream);
+int tkv_verify(const tkv_plan* plan, const void* q, const void* k, const void* v, void* o,
+               float* lse, void* hip_stream);
+
+/* Instrumentation.  tkv_plan_profile(plan, max_calls) makes the next max_calls attention calls on
+ * this plan record HIP events before the main attention kernel, after it, and after the merge
+ * kernel, on the call's stream (0 turns recording off and frees the events).
+ * tkv_plan_profile_read waits for the recorded events and returns the number of recorded calls
+ * and the summed milliseconds of the main kernel and of the merge kernel over those calls, then
+ * starts a new recording window.  EINVAL, EHIP. */
+int tkv_plan_profile(tkv_plan* plan, int32_t max_calls);
+int tkv_plan_profile_read(tkv_plan* plan, int32_t* n_calls, float* ms_main, float* ms_merge);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TREEKV_H */

@@ -1,0 +1,344 @@
+"""Python binding of libtreekv.so: tree-shared paged attention for speculative search on MI355X.
+
+Argument marshalling only -- every step of the path (block manager, coalescing, planning and the
+attention kernels) runs in the C/HIP library; PyTorch provides device memory and streams.  The
+functions carry the names of the C entry points in include/treekv.h; failures raise TkvError
+with the library's message.  The library must be built first (``python -m
+paper_2609_39334_amd.build``); any entry point raises if it is missing -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch  # imported before the library so that both share torch's HIP runtime
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtreekv.so")
+
+TKV_OK, TKV_EINVAL, TKV_ENOMEM, TKV_ENOSEQ, TKV_ECAP, TKV_EHIP = 0, -1, -2, -3, -4, -5
+
+
+class TkvError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class tkv_shape(ctypes.Structure):
+    _fields_ = [("hq", ctypes.c_int32), ("hkv", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int32)]
+
+
+class tkv_plan_stats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("n_rows", "n_qtok", "n_items", "n_items_shared", "n_items_row",
+                                              "n_slots", "n_merge", "n_segments", "n_shared_segments")] + \
+               [(n, ctypes.c_int64) for n in ("logical_qtok", "uniq_kv_tokens", "path_kv_tokens", "flops")]
+
+
+class tkv_plan_view(ctypes.Structure):
+    _fields_ = [(n, ctypes.POINTER(ctypes.c_int32)) for n in ("items", "toks", "blks", "merges", "merge_slots")] + \
+               [(n, ctypes.c_int32) for n in ("n_items", "n_toks", "n_blks", "n_merge", "n_merge_slots", "n_slots")]
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_PI32 = ctypes.POINTER(ctypes.c_int32)
+_PU8 = ctypes.POINTER(ctypes.c_uint8)
+_SIG = {
+    "tkv_last_error": (ctypes.c_char_p, []),
+    "tkv_bm_create": (ctypes.c_int, [_I32, _I32, _I32, ctypes.POINTER(_P)]),
+    "tkv_bm_destroy": (None, [_P]),
+    "tkv_bm_extend": (ctypes.c_int, [_P, _I32, _PI32, _I32, _I32, _PI32, _PI32, _PU8, _I32, _PI32]),
+    "tkv_prune": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32]),
+    "tkv_bm_table": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32, _PI32]),
+    "tkv_bm_refcount": (ctypes.c_int, [_P, _I32, _PI32]),
+    "tkv_bm_block_len": (ctypes.c_int, [_P, _PI32]),
+    "tkv_bm_snapshot": (ctypes.c_int, [_P, _P, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
+    "tkv_bm_coalesce": (ctypes.c_int, [_P, _I32, _PI32, _PI32, _PI32, _PI32, _PI32, _PI32]),
+    "tkv_plan_create": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _I32, _PI32, _PI32, _PI32, _PI32, _PI32,
+                                       ctypes.POINTER(_P)]),
+    "tkv_plan_workspace_bytes": (ctypes.c_size_t, [_P]),
+    "tkv_plan_upload": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P]),
+    "tkv_plan_destroy": (None, [_P]),
+    "tkv_plan_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_stats)]),
+    "tkv_plan_get_view": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_view)]),
+    "tkv_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
+    "tkv_verify": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
+    "tkv_plan_profile": (ctypes.c_int, [_P, _I32]),
+    "tkv_plan_profile_read": (ctypes.c_int, [_P, _PI32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
+}
+EXPORTED = tuple(_SIG)
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libtreekv.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2609_39334_amd.build` "
+                               "(or __graft_entry__.build()) first")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIG.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(rc: int) -> None:
+    if rc != TKV_OK:
+        raise TkvError(rc, lib().tkv_last_error().decode())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32).reshape(-1))
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(_PI32)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+# ------------------------------------------------------------------------- C entry points
+
+def tkv_last_error() -> str:
+    return lib().tkv_last_error().decode()
+
+
+def tkv_bm_create(num_blocks: int, block_size: int, max_seqs: int) -> int:
+    h = _P()
+    _check(lib().tkv_bm_create(num_blocks, block_size, max_seqs, ctypes.byref(h)))
+    return h.value
+
+
+def tkv_bm_destroy(bm: int) -> None:
+    lib().tkv_bm_destroy(bm)
+
+
+def tkv_bm_extend(bm: int, parent: int, tokens, seal: bool, block_size: int = 16):
+    """Returns (seq, block ids, hit flags) of the new sequence's step."""
+    t = _i32(tokens)
+    cap = max(1, -(-len(t) // block_size))
+    blk = np.zeros(cap, dtype=np.int32)
+    hit = np.zeros(cap, dtype=np.uint8)
+    child, n = _I32(), _I32()
+    _check(lib().tkv_bm_extend(bm, parent, _ptr(t), len(t), int(bool(seal)), ctypes.byref(child), _ptr(blk),
+                               hit.ctypes.data_as(_PU8), cap, ctypes.byref(n)))
+    return child.value, blk[:n.value].copy(), hit[:n.value].copy()
+
+
+def tkv_prune(bm: int, seq: int, cap: int = None) -> np.ndarray:
+    """Releases a sequence; returns the freed block ids in table order."""
+    if cap is None:
+        n, _ = _table_len(bm, seq)
+        cap = max(1, n)
+    out = np.zeros(cap, dtype=np.int32)
+    n = _I32()
+    _check(lib().tkv_prune(bm, seq, _ptr(out), cap, ctypes.byref(n)))
+    return out[:n.value].copy()
+
+
+def _table_len(bm: int, seq: int):
+    n, kv = _I32(), _I32()
+    rc = lib().tkv_bm_table(bm, seq, None, 0, ctypes.byref(n), ctypes.byref(kv))
+    if rc not in (TKV_OK, TKV_ECAP):
+        _check(rc)
+    return n.value, kv.value
+
+
+def tkv_bm_table(bm: int, seq: int):
+    """Returns (block table, kv_len)."""
+    n, _ = _table_len(bm, seq)
+    out = np.zeros(max(1, n), dtype=np.int32)
+    nn, kv = _I32(), _I32()
+    _check(lib().tkv_bm_table(bm, seq, _ptr(out), len(out), ctypes.byref(nn), ctypes.byref(kv)))
+    return out[:nn.value].copy(), kv.value
+
+
+def tkv_bm_refcount(bm: int, blk: int) -> int:
+    rc = _I32()
+    _check(lib().tkv_bm_refcount(bm, blk, ctypes.byref(rc)))
+    return rc.value
+
+
+def tkv_bm_block_len(bm: int, num_blocks: int) -> np.ndarray:
+    out = np.zeros(num_blocks, dtype=np.int32)
+    _check(lib().tkv_bm_block_len(bm, _ptr(out)))
+    return out
+
+
+def tkv_bm_snapshot(bm: int, seqs: bool = True) -> dict:
+    """Parsed state; seqs=False skips decoding the per-sequence tables."""
+    used = ctypes.c_size_t()
+    lib().tkv_bm_snapshot(bm, None, 0, ctypes.byref(used))
+    buf = np.zeros(used.value // 4, dtype=np.int32)
+    _check(lib().tkv_bm_snapshot(bm, buf.ctypes.data_as(_P), used.value, ctypes.byref(used)))
+    nb, bs, ms, nlive = (int(x) for x in buf[:4])
+    w = 4
+    snap = {"refcount": buf[w:w + nb].copy(), "block_len": buf[w + nb:w + 2 * nb].copy(),
+            "indexed": buf[w + 2 * nb:w + 3 * nb].copy(), "seqs": {}}
+    w += 3 * nb
+    for _ in range(nlive if seqs else 0):
+        s, sealed, n = (int(x) for x in buf[w:w + 3])
+        snap["seqs"][s] = (tuple(int(b) for b in buf[w + 3:w + 3 + n]), sealed)
+        w += 3 + n
+    return snap
+
+
+def tkv_bm_coalesce(bm: int, seqs: Sequence[int], q_lens: Sequence[int]):
+    """Returns (row of each candidate, first candidate of each row, multiplicity of each row)."""
+    s, q = _i32(seqs), _i32(q_lens)
+    n = len(s)
+    row_of = np.zeros(max(1, n), dtype=np.int32)
+    first = np.zeros(max(1, n), dtype=np.int32)
+    mult = np.zeros(max(1, n), dtype=np.int32)
+    nr = _I32()
+    _check(lib().tkv_bm_coalesce(bm, n, _ptr(s), _ptr(q), _ptr(row_of), _ptr(first), _ptr(mult), ctypes.byref(nr)))
+    return row_of[:n].copy(), first[:nr.value].copy(), mult[:nr.value].copy()
+
+
+def tkv_plan_create(shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity=None) -> int:
+    """shape = (hq, hkv, d, block_size, num_blocks)."""
+    sh = tkv_shape(*[int(x) for x in shape])
+    qi, ki, kb, bl = _i32(q_indptr), _i32(kv_indptr), _i32(kv_blocks), _i32(block_len)
+    mu = None if multiplicity is None else _i32(multiplicity)
+    h = _P()
+    _check(lib().tkv_plan_create(ctypes.byref(sh), len(qi) - 1, _ptr(qi), _ptr(ki), _ptr(kb) if len(kb) else None,
+                                 _ptr(bl), None if mu is None else _ptr(mu), ctypes.byref(h)))
+    return h.value
+
+
+def tkv_plan_workspace_bytes(plan: int) -> int:
+    return int(lib().tkv_plan_workspace_bytes(plan))
+
+
+def tkv_plan_upload(plan: int, workspace: torch.Tensor, stream=None) -> None:
+    _check(lib().tkv_plan_upload(plan, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                 _stream(stream)))
+
+
+def tkv_plan_destroy(plan: int) -> None:
+    lib().tkv_plan_destroy(plan)
+
+
+def tkv_plan_get_stats(plan: int) -> dict:
+    st = tkv_plan_stats()
+    _check(lib().tkv_plan_get_stats(plan, ctypes.byref(st)))
+    return {n: int(getattr(st, n)) for n, _ in tkv_plan_stats._fields_}
+
+
+def tkv_plan_get_view(plan: int) -> dict:
+    v = tkv_plan_view()
+    _check(lib().tkv_plan_get_view(plan, ctypes.byref(v)))
+
+    def arr(p, n, w):
+        if n == 0:
+            return np.zeros((0, w), dtype=np.int32)
+        return np.ctypeslib.as_array(p, shape=(n * w,)).reshape(n, w).copy()
+    return {"items": arr(v.items, v.n_items, 8), "toks": arr(v.toks, v.n_toks, 4), "blks": arr(v.blks, v.n_blks, 2),
+            "merges": arr(v.merges, v.n_merge, 4),
+            "merge_slots": arr(v.merge_slots, v.n_merge_slots, 1).reshape(-1), "n_slots": int(v.n_slots)}
+
+
+def _attn(fn, plan, q, k, v, o, lse, stream):
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if not (t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous()):
+            raise TkvError(TKV_EINVAL, f"{name} must be a contiguous bfloat16 device tensor")
+    if lse is not None and not (lse.is_cuda and lse.dtype == torch.float32 and lse.is_contiguous()):
+        raise TkvError(TKV_EINVAL, "lse must be a contiguous float32 device tensor")
+    _check(fn(plan, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+              None if lse is None else lse.data_ptr(), _stream(stream)))
+
+
+def tkv_decode(plan: int, q, k, v, o, lse=None, stream=None) -> None:
+    _attn(lib().tkv_decode, plan, q, k, v, o, lse, stream)
+
+
+def tkv_verify(plan: int, q, k, v, o, lse=None, stream=None) -> None:
+    _attn(lib().tkv_verify, plan, q, k, v, o, lse, stream)
+
+
+def tkv_plan_profile(plan: int, max_calls: int) -> None:
+    _check(lib().tkv_plan_profile(plan, max_calls))
+
+
+def tkv_plan_profile_read(plan: int):
+    """Returns (recorded calls, summed main-kernel ms, summed merge-kernel ms)."""
+    n, a, b = _I32(), ctypes.c_float(), ctypes.c_float()
+    _check(lib().tkv_plan_profile_read(plan, ctypes.byref(n), ctypes.byref(a), ctypes.byref(b)))
+    return n.value, a.value, b.value
+
+
+# ------------------------------------------------------------------------- owning wrappers
+
+class BlockManager:
+    """Owns a tkv_bm handle; methods forward to the C entry points."""
+
+    def __init__(self, num_blocks: int, block_size: int = 16, max_seqs: int = 1024):
+        self.num_blocks, self.block_size = num_blocks, block_size
+        self.h = tkv_bm_create(num_blocks, block_size, max_seqs)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            tkv_bm_destroy(self.h)
+            self.h = None
+
+    def extend(self, parent, tokens, seal):
+        return tkv_bm_extend(self.h, parent, tokens, seal, self.block_size)
+
+    def prune(self, seq):
+        return tkv_prune(self.h, seq)
+
+    def table(self, seq):
+        return tkv_bm_table(self.h, seq)[0]
+
+    def block_len(self):
+        return tkv_bm_block_len(self.h, self.num_blocks)
+
+    def snapshot(self, seqs=True):
+        return tkv_bm_snapshot(self.h, seqs)
+
+    def coalesce(self, seqs, q_lens):
+        return tkv_bm_coalesce(self.h, seqs, q_lens)
+
+
+class Plan:
+    """Owns a tkv_plan handle and the device workspace it was uploaded to."""
+
+    def __init__(self, shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity=None,
+                 device="cuda", stream=None, upload=True):
+        self.h = tkv_plan_create(shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity)
+        self.workspace = None
+        if upload:
+            nbytes = tkv_plan_workspace_bytes(self.h)
+            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+            tkv_plan_upload(self.h, self.workspace, stream)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            tkv_plan_destroy(self.h)
+            self.h = None
+
+    @property
+    def stats(self):
+        return tkv_plan_get_stats(self.h)
+
+    def view(self):
+        return tkv_plan_get_view(self.h)
+
+    def decode(self, q, k, v, o, lse=None, stream=None):
+        tkv_decode(self.h, q, k, v, o, lse, stream)
+
+    def verify(self, q, k, v, o, lse=None, stream=None):
+        tkv_verify(self.h, q, k, v, o, lse, stream)

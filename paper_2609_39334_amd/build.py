@@ -1,0 +1,70 @@
+"""Build libtreekv.so in-tree: host C++ (block manager, planner, C entry points) with g++, the HIP
+kernels with hipcc for gfx950, linked into one shared library next to this file.
+
+    python -m paper_2609_39334_amd.build      (or __graft_entry__.build())
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+OUT = os.path.join(HERE, "_build")
+LIB = os.path.join(HERE, "libtreekv.so")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+HIPCC = os.path.join(ROCM, "bin", "hipcc")
+
+HOST_SOURCES = ["capi.cpp", "bm.cpp", "plan.cpp"]
+HIP_SOURCES = ["attn.hip"]
+
+HOST_FLAGS = ["-std=c++17", "-O2", "-fPIC", "-fvisibility=hidden", "-Wall", "-Wextra", "-Wno-unused-parameter"]
+HIP_FLAGS = [
+    "--offload-arch=gfx950", "-std=c++17", "-O3", "-fPIC", "-fvisibility=hidden",
+    "-mcode-object-version=5",
+    # no packed-fp32 instructions in device code
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+]
+
+
+def _run_all(cmds, verbose):
+    procs = []
+    for c in cmds:
+        if verbose:
+            print(" ".join(c), flush=True)
+        procs.append((c, subprocess.Popen(c, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
+    errs = []
+    for c, p in procs:
+        out, _ = p.communicate()
+        out = "\n".join(l for l in out.splitlines() if "packed-fp32-ops" not in l)
+        if p.returncode != 0:
+            errs.append(f"$ {' '.join(c)}\n{out}")
+        elif verbose and out.strip():
+            print(out)
+    if errs:
+        raise RuntimeError("build failed:\n" + "\n".join(errs))
+
+
+def build(verbose: bool = False, extra_host_flags=()) -> str:
+    os.makedirs(OUT, exist_ok=True)
+    inc = ["-I", CSRC, "-I", os.path.join(ROOT, "include")]
+    objs, cmds = [], []
+    for s in HOST_SOURCES:
+        o = os.path.join(OUT, s + ".o")
+        cmds.append(["g++", *HOST_FLAGS, *extra_host_flags, *inc, "-c", os.path.join(CSRC, s), "-o", o])
+        objs.append(o)
+    for s in HIP_SOURCES:
+        o = os.path.join(OUT, s + ".o")
+        cmds.append([HIPCC, *HIP_FLAGS, *inc, "-c", os.path.join(CSRC, s), "-o", o])
+        objs.append(o)
+    _run_all(cmds, verbose)
+    tmp = LIB + ".tmp"
+    _run_all([[HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]], verbose)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

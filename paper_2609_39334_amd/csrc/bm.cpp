@@ -1,0 +1,326 @@
+// Prefix-tree KV block manager (host, integer) and row coalescing.
+//
+// Paged KV with prefix sharing is the substrate the paper builds on (Sec. 5.1); candidate paths
+// of one request share the blocks of their common prefix, identical candidates collapse into one
+// sequence (computation deduplication, Sec. 4.2), and pruning releases a path's blocks (Sec. 4.1).
+// Block-level rules (the paper states none): step-aligned blocks; a sealed chunk reuses the live
+// sealed block with the same (predecessor block, exact tokens) key; misses take the lowest free id;
+// refcount = live sequences holding the block; freed and unindexed at zero; lowest free sequence id.
+// A 64-bit FNV-1a hash only selects a bucket -- keys are compared exactly.
+#include <algorithm>
+#include <cstring>
+#include <functional>
+#include <queue>
+#include <unordered_map>
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+struct ChunkKey {
+    int32_t pred;
+    std::vector<int32_t> toks;
+    bool operator==(const ChunkKey& o) const { return pred == o.pred && toks == o.toks; }
+};
+
+struct ChunkKeyHash {
+    size_t operator()(const ChunkKey& k) const {
+        uint64_t h = 1469598103934665603ull;
+        auto mix = [&h](uint32_t w) {
+            for (int i = 0; i < 4; ++i) {
+                h ^= (w >> (8 * i)) & 0xffu;
+                h *= 1099511628211ull;
+            }
+        };
+        mix(static_cast<uint32_t>(k.pred));
+        for (int32_t t : k.toks) mix(static_cast<uint32_t>(t));
+        return static_cast<size_t>(h);
+    }
+};
+
+using MinHeap = std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>>;
+
+struct Seq {
+    bool live = false;
+    bool sealed = false;
+    std::vector<int32_t> table;
+};
+
+}  // namespace
+
+struct tkv_bm {
+    int32_t num_blocks = 0, block_size = 0, max_seqs = 0;
+    std::vector<int32_t> refcount, block_len;
+    std::vector<uint8_t> indexed;
+    std::vector<ChunkKey> key;  // valid where indexed
+    std::unordered_map<ChunkKey, int32_t, ChunkKeyHash> index;
+    MinHeap free_blocks, free_seqs;
+    std::vector<Seq> seqs;
+    int32_t n_live = 0;
+};
+
+using tkv::set_error;
+
+TKV_EXPORT int tkv_bm_create(int32_t num_blocks, int32_t block_size, int32_t max_seqs, tkv_bm** out) {
+    tkv::clear_error();
+    if (!out) return set_error(TKV_EINVAL, "tkv_bm_create: out is NULL");
+    *out = nullptr;
+    if (num_blocks < 1 || block_size < 1 || max_seqs < 1)
+        return set_error(TKV_EINVAL, "tkv_bm_create: sizes must be >= 1 (got %d, %d, %d)", num_blocks,
+                         block_size, max_seqs);
+    tkv_bm* bm = new (std::nothrow) tkv_bm();
+    if (!bm) return set_error(TKV_ENOMEM, "tkv_bm_create: host allocation failed");
+    try {
+        bm->num_blocks = num_blocks;
+        bm->block_size = block_size;
+        bm->max_seqs = max_seqs;
+        bm->refcount.assign(num_blocks, 0);
+        bm->block_len.assign(num_blocks, 0);
+        bm->indexed.assign(num_blocks, 0);
+        bm->key.resize(num_blocks);
+        bm->seqs.resize(max_seqs);
+        std::vector<int32_t> ids(num_blocks);
+        for (int32_t i = 0; i < num_blocks; ++i) ids[i] = i;
+        bm->free_blocks = MinHeap(std::greater<int32_t>(), std::move(ids));
+        std::vector<int32_t> sids(max_seqs);
+        for (int32_t i = 0; i < max_seqs; ++i) sids[i] = i;
+        bm->free_seqs = MinHeap(std::greater<int32_t>(), std::move(sids));
+    } catch (...) {
+        delete bm;
+        return set_error(TKV_ENOMEM, "tkv_bm_create: host allocation failed");
+    }
+    *out = bm;
+    return TKV_OK;
+}
+
+TKV_EXPORT void tkv_bm_destroy(tkv_bm* bm) { delete bm; }
+
+static bool seq_live(const tkv_bm* bm, int32_t s) { return s >= 0 && s < bm->max_seqs && bm->seqs[s].live; }
+
+TKV_EXPORT int tkv_bm_extend(tkv_bm* bm, int32_t parent, const int32_t* tokens, int32_t n, int32_t seal,
+                             int32_t* child_out, int32_t* blk_out, uint8_t* hit_out, int32_t cap,
+                             int32_t* n_blk_out) {
+    tkv::clear_error();
+    if (!bm || !child_out || !n_blk_out || (n > 0 && !tokens))
+        return set_error(TKV_EINVAL, "tkv_bm_extend: NULL argument");
+    if (n < 0) return set_error(TKV_EINVAL, "tkv_bm_extend: n = %d < 0", n);
+    if (seal != 0 && seal != 1) return set_error(TKV_EINVAL, "tkv_bm_extend: seal must be 0 or 1");
+    const int32_t bs = bm->block_size;
+    const int32_t n_chunks = (n + bs - 1) / bs;
+    if (parent == -1) {
+        if (n < 1) return set_error(TKV_EINVAL, "tkv_bm_extend: a root needs at least one token");
+    } else {
+        if (!seq_live(bm, parent)) return set_error(TKV_ENOSEQ, "tkv_bm_extend: parent %d is not live", parent);
+        if (!bm->seqs[parent].sealed)
+            return set_error(TKV_EINVAL, "tkv_bm_extend: parent %d is unsealed (in-progress step)", parent);
+    }
+    if (cap < n_chunks || (n_chunks > 0 && (!blk_out || !hit_out))) {
+        *n_blk_out = n_chunks;
+        return set_error(TKV_ECAP, "tkv_bm_extend: output capacity %d < %d blocks", cap, n_chunks);
+    }
+    if (bm->free_seqs.empty()) return set_error(TKV_ENOMEM, "tkv_bm_extend: no free sequence slot");
+
+    // Resolve the hit prefix before changing anything: once a chunk misses, every later chunk of
+    // this extension misses too (a fresh block is nobody's predecessor yet).
+    std::vector<int32_t> hits;
+    int32_t pred = parent == -1 ? -1
+                                : (bm->seqs[parent].table.empty() ? -1 : bm->seqs[parent].table.back());
+    ChunkKey probe;
+    if (seal) {
+        for (int32_t c = 0; c < n_chunks; ++c) {
+            const int32_t a = c * bs, e = std::min(n, a + bs);
+            probe.pred = pred;
+            probe.toks.assign(tokens + a, tokens + e);
+            auto it = bm->index.find(probe);
+            if (it == bm->index.end()) break;
+            hits.push_back(it->second);
+            pred = it->second;
+        }
+    }
+    const int32_t n_miss = n_chunks - static_cast<int32_t>(hits.size());
+    if (static_cast<size_t>(n_miss) > bm->free_blocks.size())
+        return set_error(TKV_ENOMEM, "tkv_bm_extend: pool exhausted (need %d blocks, %zu free)", n_miss,
+                         bm->free_blocks.size());
+
+    // Commit.
+    const int32_t s = bm->free_seqs.top();
+    bm->free_seqs.pop();
+    Seq& sq = bm->seqs[s];
+    sq.table.clear();
+    if (parent != -1) sq.table = bm->seqs[parent].table;
+    for (int32_t b : sq.table) bm->refcount[b] += 1;
+    pred = sq.table.empty() ? -1 : sq.table.back();
+    for (int32_t c = 0; c < n_chunks; ++c) {
+        const int32_t a = c * bs, e = std::min(n, a + bs);
+        int32_t b;
+        uint8_t h;
+        if (c < static_cast<int32_t>(hits.size())) {
+            b = hits[c];
+            h = 1;
+        } else {
+            b = bm->free_blocks.top();
+            bm->free_blocks.pop();
+            bm->block_len[b] = e - a;
+            if (seal) {
+                ChunkKey k{pred, std::vector<int32_t>(tokens + a, tokens + e)};
+                bm->index.emplace(k, b);
+                bm->key[b] = std::move(k);
+                bm->indexed[b] = 1;
+            }
+            h = 0;
+        }
+        bm->refcount[b] += 1;
+        sq.table.push_back(b);
+        blk_out[c] = b;
+        hit_out[c] = h;
+        pred = b;
+    }
+    sq.live = true;
+    sq.sealed = seal != 0;
+    bm->n_live += 1;
+    *child_out = s;
+    *n_blk_out = n_chunks;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_prune(tkv_bm* bm, int32_t seq, int32_t* freed_out, int32_t cap, int32_t* n_freed_out) {
+    tkv::clear_error();
+    if (!bm || !n_freed_out) return set_error(TKV_EINVAL, "tkv_prune: NULL argument");
+    if (!seq_live(bm, seq)) return set_error(TKV_ENOSEQ, "tkv_prune: sequence %d is not live", seq);
+    Seq& sq = bm->seqs[seq];
+    const int32_t len = static_cast<int32_t>(sq.table.size());
+    if (cap < len || (len > 0 && !freed_out)) {
+        *n_freed_out = len;
+        return set_error(TKV_ECAP, "tkv_prune: capacity %d < table length %d", cap, len);
+    }
+    int32_t nf = 0;
+    for (int32_t b : sq.table) {
+        if (--bm->refcount[b] == 0) {
+            if (bm->indexed[b]) {
+                bm->index.erase(bm->key[b]);
+                bm->key[b] = ChunkKey{};
+                bm->indexed[b] = 0;
+            }
+            bm->block_len[b] = 0;
+            bm->free_blocks.push(b);
+            freed_out[nf++] = b;
+        }
+    }
+    sq.table.clear();
+    sq.live = false;
+    sq.sealed = false;
+    bm->free_seqs.push(seq);
+    bm->n_live -= 1;
+    *n_freed_out = nf;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_bm_table(const tkv_bm* bm, int32_t seq, int32_t* blk_out, int32_t cap, int32_t* n_out,
+                            int32_t* kv_len_out) {
+    tkv::clear_error();
+    if (!bm || !n_out) return set_error(TKV_EINVAL, "tkv_bm_table: NULL argument");
+    if (!seq_live(bm, seq)) return set_error(TKV_ENOSEQ, "tkv_bm_table: sequence %d is not live", seq);
+    const auto& t = bm->seqs[seq].table;
+    const int32_t len = static_cast<int32_t>(t.size());
+    *n_out = len;
+    if (cap < len || (len > 0 && !blk_out))
+        return set_error(TKV_ECAP, "tkv_bm_table: capacity %d < table length %d", cap, len);
+    int32_t kv = 0;
+    for (int32_t i = 0; i < len; ++i) {
+        blk_out[i] = t[i];
+        kv += bm->block_len[t[i]];
+    }
+    if (kv_len_out) *kv_len_out = kv;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_bm_refcount(const tkv_bm* bm, int32_t blk, int32_t* rc_out) {
+    tkv::clear_error();
+    if (!bm || !rc_out) return set_error(TKV_EINVAL, "tkv_bm_refcount: NULL argument");
+    if (blk < 0 || blk >= bm->num_blocks) return set_error(TKV_EINVAL, "tkv_bm_refcount: block %d out of range", blk);
+    *rc_out = bm->refcount[blk];
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_bm_block_len(const tkv_bm* bm, int32_t* len_out) {
+    tkv::clear_error();
+    if (!bm || !len_out) return set_error(TKV_EINVAL, "tkv_bm_block_len: NULL argument");
+    std::memcpy(len_out, bm->block_len.data(), sizeof(int32_t) * bm->num_blocks);
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_bm_snapshot(const tkv_bm* bm, void* buf, size_t cap, size_t* used) {
+    tkv::clear_error();
+    if (!bm || !used) return set_error(TKV_EINVAL, "tkv_bm_snapshot: NULL argument");
+    size_t words = 4 + 3 * static_cast<size_t>(bm->num_blocks);
+    for (const Seq& s : bm->seqs)
+        if (s.live) words += 3 + s.table.size();
+    *used = words * sizeof(int32_t);
+    if (!buf || cap < *used) return set_error(TKV_ECAP, "tkv_bm_snapshot: capacity %zu < %zu bytes", cap, *used);
+    int32_t* w = static_cast<int32_t*>(buf);
+    *w++ = bm->num_blocks;
+    *w++ = bm->block_size;
+    *w++ = bm->max_seqs;
+    *w++ = bm->n_live;
+    for (int32_t b = 0; b < bm->num_blocks; ++b) *w++ = bm->refcount[b];
+    for (int32_t b = 0; b < bm->num_blocks; ++b) *w++ = bm->block_len[b];
+    for (int32_t b = 0; b < bm->num_blocks; ++b) *w++ = bm->indexed[b];
+    for (int32_t s = 0; s < bm->max_seqs; ++s) {
+        const Seq& q = bm->seqs[s];
+        if (!q.live) continue;
+        *w++ = s;
+        *w++ = q.sealed ? 1 : 0;
+        *w++ = static_cast<int32_t>(q.table.size());
+        for (int32_t b : q.table) *w++ = b;
+    }
+    return TKV_OK;
+}
+
+namespace {
+struct RowKeyHash {
+    size_t operator()(const std::vector<int32_t>& v) const {
+        uint64_t h = 1469598103934665603ull;
+        for (int32_t x : v) {
+            h ^= static_cast<uint32_t>(x);
+            h *= 1099511628211ull;
+        }
+        return static_cast<size_t>(h);
+    }
+};
+}  // namespace
+
+TKV_EXPORT int tkv_bm_coalesce(const tkv_bm* bm, int32_t n_cand, const int32_t* seqs, const int32_t* q_len,
+                               int32_t* row_of_cand_out, int32_t* first_cand_out, int32_t* mult_out,
+                               int32_t* n_rows_out) {
+    tkv::clear_error();
+    if (!bm || !n_rows_out || n_cand < 0 ||
+        (n_cand > 0 && (!seqs || !q_len || !row_of_cand_out || !first_cand_out || !mult_out)))
+        return set_error(TKV_EINVAL, "tkv_bm_coalesce: bad argument");
+    for (int32_t c = 0; c < n_cand; ++c) {
+        if (!seq_live(bm, seqs[c])) return set_error(TKV_ENOSEQ, "tkv_bm_coalesce: sequence %d is not live", seqs[c]);
+        if (q_len[c] < 1) return set_error(TKV_EINVAL, "tkv_bm_coalesce: q_len[%d] = %d < 1", c, q_len[c]);
+    }
+    std::unordered_map<std::vector<int32_t>, int32_t, RowKeyHash> first;
+    int32_t n_rows = 0;
+    std::vector<int32_t> key;
+    for (int32_t c = 0; c < n_cand; ++c) {
+        const auto& t = bm->seqs[seqs[c]].table;
+        key.assign(1, q_len[c]);
+        key.insert(key.end(), t.begin(), t.end());
+        auto it = first.find(key);
+        int32_t r;
+        if (it == first.end()) {
+            r = n_rows++;
+            first.emplace(key, r);
+            first_cand_out[r] = c;
+            mult_out[r] = 0;
+        } else {
+            r = it->second;
+        }
+        mult_out[r] += 1;
+        row_of_cand_out[c] = r;
+    }
+    *n_rows_out = n_rows;
+    return TKV_OK;
+}

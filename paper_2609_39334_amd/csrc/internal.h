@@ -1,0 +1,90 @@
+// Internal declarations shared by the host library (block manager, planner, C entry points) and
+// the HIP kernels.  Not part of the public ABI (include/treekv.h is).
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "treekv.h"
+
+#define TKV_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace tkv {
+
+// Records the message for tkv_last_error() and returns `code`.
+int set_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+// ------------------------------------------------------------------ device descriptors
+// One work item = one workgroup: a tile of query tokens (each with all G query heads of one KV
+// head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the
+// keys at positions <= its `limit`; keys are numbered along the path starting at `pos0`.
+struct ItemDesc {
+    int32_t kvh;      // KV head
+    int32_t tok_off;  // first TokDesc of the tile
+    int32_t n_tok;    // query tokens in the tile (n_tok * G <= kTileRows)
+    int32_t blk_off;  // first BlkDesc of the key list
+    int32_t n_blk;    // blocks in the key list
+    int32_t pos0;     // path position of the first key
+    int32_t kind;     // kItemShared (partials of shared/private segments) or kItemRow (whole path)
+    int32_t pad;
+};
+
+struct TokDesc {
+    int32_t qtok;   // query token index (row of q / o)
+    int32_t limit;  // largest visible key position
+    int32_t slot;   // partial slot (>= 0) or -1: this item covers the token's whole path -> o, lse
+    int32_t pad;
+};
+
+struct BlkDesc {
+    int32_t blk;  // pool block id
+    int32_t len;  // tokens in the block (1..16)
+};
+
+struct MergeDesc {
+    int32_t qtok;
+    int32_t slot_off;  // first entry in the merge slot list
+    int32_t n_slots;
+    int32_t pad;
+};
+
+constexpr int kBlock = 16;     // tokens per KV block
+constexpr int kTileRows = 64;  // query rows (token x head) per work item
+constexpr int kItemShared = 0;
+constexpr int kItemRow = 1;
+
+}  // namespace tkv
+
+// ------------------------------------------------------------------ plan (host)
+struct tkv_plan {
+    tkv_shape shape{};
+    int32_t group = 1;
+    bool all_decode = true;
+    std::vector<tkv::ItemDesc> items;
+    std::vector<tkv::TokDesc> toks;
+    std::vector<tkv::BlkDesc> blks;
+    std::vector<tkv::MergeDesc> merges;
+    std::vector<int32_t> merge_slots;
+    int32_t n_slots = 0;
+    // workspace layout (byte offsets)
+    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0;
+    size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;
+    std::vector<uint8_t> image;  // host copy of the descriptor region
+    void* d_ws = nullptr;        // uploaded workspace (caller-owned)
+    tkv_plan_stats stats{};
+    // instrumentation: 3 HIP events per recorded call (see tkv_plan_profile)
+    mutable int32_t prof_max = 0;
+    mutable int32_t prof_n = 0;
+    mutable std::vector<void*> prof_events;
+    ~tkv_plan();
+};
+
+namespace tkv {
+// Launchers (attn.hip).
+int launch_attention(const tkv_plan* p, const void* q, const void* k, const void* v, void* o,
+                     float* lse, void* stream);
+int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream);
+}  // namespace tkv

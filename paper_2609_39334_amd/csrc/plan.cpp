@@ -1,0 +1,350 @@
+// Planner: per-row block tables -> shared segments -> device work list.
+//
+// The paper's lever (computation deduplication, Sec. 4.2, over prefix-shared paged KV, Sec. 5.1)
+// is that many candidates reference the same prompt and step blocks.  The planner finds those
+// blocks with a trie over the rows' tables and emits two kinds of work items:
+//
+//  * shared items, for rows whose query tile is small (q_len * G < kTileRows: decode rows and
+//    short verify rows).  A segment is a maximal run of trie nodes passed by the same set of rows;
+//    each segment (split into chunks of <= kChunkBlocks blocks) becomes items whose tile holds the
+//    query tokens of *every* row that references it, so each shared K/V block is staged once per
+//    tile and contracted against all of them.  Each (token, chunk) result is a partial (o, lse)
+//    that a log-sum-exp merge combines -- unless the chunk is the token's only one, in which case
+//    the item writes the final output.
+//  * row items, for rows whose own query tokens fill a tile (verify rows with q_len * G >=
+//    kTileRows).  A tile of one row's tokens walks the row's whole path (truncated at the tile's
+//    causal limit) and writes the final output; shared context blocks are then re-read from L2 by
+//    the tiles of other rows instead of being merged through HBM partials.
+//
+// Positions: key j of a row is the j-th token along its path; token i of a row with q_len L and
+// kv_len N sees positions <= N - L + i (bottom-right causal, the prefill-only verification pass of
+// Sec. 3.2.2; decode is L = 1).  A shared segment sits at the same positions in every row through
+// it, so one per-token limit suffices.
+#include <algorithm>
+#include <cstring>
+#include <numeric>
+#include <unordered_map>
+#include <vector>
+
+#include "internal.h"
+
+using tkv::BlkDesc;
+using tkv::ItemDesc;
+using tkv::MergeDesc;
+using tkv::set_error;
+using tkv::TokDesc;
+
+namespace {
+
+constexpr int kChunkBlocks = 16;  // longest key run of one shared item (256 tokens)
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+struct Node {
+    int32_t parent, blk, len, pos0, count, seg;
+};
+
+struct Segment {
+    std::vector<int32_t> nodes;
+    std::vector<int32_t> rows;
+};
+
+struct Chunk {
+    int32_t blk_off, n_blk, pos0;
+    std::vector<TokDesc> toks;  // slot filled in later
+};
+
+// Split n things into near-equal tiles of at most `cap`.
+template <class F>
+void tile_evenly(int32_t n, int32_t cap, F f) {
+    if (n <= 0) return;
+    const int32_t tiles = (n + cap - 1) / cap;
+    const int32_t per = (n + tiles - 1) / tiles;
+    for (int32_t a = 0; a < n; a += per) f(a, std::min(n, a + per));
+}
+
+}  // namespace
+
+TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
+                               const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
+                               const int32_t* multiplicity, tkv_plan** out) {
+    tkv::clear_error();
+    if (!out) return set_error(TKV_EINVAL, "tkv_plan_create: out is NULL");
+    *out = nullptr;
+    if (!shape) return set_error(TKV_EINVAL, "tkv_plan_create: shape is NULL");
+    const tkv_shape s = *shape;
+    if (s.block_size != tkv::kBlock) return set_error(TKV_EINVAL, "tkv_plan_create: block_size must be 16 (got %d)", s.block_size);
+    if (s.d != 64 && s.d != 128) return set_error(TKV_EINVAL, "tkv_plan_create: head_dim must be 64 or 128 (got %d)", s.d);
+    if (s.hq < 1 || s.hkv < 1 || s.hq % s.hkv)
+        return set_error(TKV_EINVAL, "tkv_plan_create: hq (%d) must be a positive multiple of hkv (%d)", s.hq, s.hkv);
+    const int32_t G = s.hq / s.hkv;
+    if (G > tkv::kTileRows) return set_error(TKV_EINVAL, "tkv_plan_create: hq/hkv = %d exceeds %d", G, tkv::kTileRows);
+    if (s.num_blocks < 1) return set_error(TKV_EINVAL, "tkv_plan_create: num_blocks must be >= 1");
+    if (n_rows < 0) return set_error(TKV_EINVAL, "tkv_plan_create: n_rows < 0");
+    if (n_rows > 0 && (!q_indptr || !kv_indptr || !block_len))
+        return set_error(TKV_EINVAL, "tkv_plan_create: NULL array");
+    if (n_rows > 0 && (q_indptr[0] != 0 || kv_indptr[0] != 0))
+        return set_error(TKV_EINVAL, "tkv_plan_create: q_indptr[0] and kv_indptr[0] must be 0");
+    if (n_rows > 0 && kv_indptr[n_rows] > 0 && !kv_blocks) return set_error(TKV_EINVAL, "tkv_plan_create: kv_blocks is NULL");
+
+    // ---------------------------------------------------------------- validate rows
+    std::vector<int32_t> L(n_rows), N(n_rows);
+    for (int32_t r = 0; r < n_rows; ++r) {
+        L[r] = q_indptr[r + 1] - q_indptr[r];
+        const int32_t nb = kv_indptr[r + 1] - kv_indptr[r];
+        if (L[r] < 1) return set_error(TKV_EINVAL, "tkv_plan_create: row %d has q_len %d < 1", r, L[r]);
+        if (nb < 0) return set_error(TKV_EINVAL, "tkv_plan_create: kv_indptr decreases at row %d", r);
+        int64_t n = 0;
+        for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1]; ++j) {
+            const int32_t b = kv_blocks[j];
+            if (b < 0 || b >= s.num_blocks) return set_error(TKV_EINVAL, "tkv_plan_create: row %d block id %d out of range", r, b);
+            if (block_len[b] < 1 || block_len[b] > s.block_size)
+                return set_error(TKV_EINVAL, "tkv_plan_create: block %d has length %d (free or invalid)", b, block_len[b]);
+            n += block_len[b];
+        }
+        if (n > (1 << 30)) return set_error(TKV_EINVAL, "tkv_plan_create: row %d kv_len too large", r);
+        N[r] = static_cast<int32_t>(n);
+        if (L[r] > N[r]) return set_error(TKV_EINVAL, "tkv_plan_create: row %d q_len %d > kv_len %d", r, L[r], N[r]);
+        if (multiplicity && multiplicity[r] < 1) return set_error(TKV_EINVAL, "tkv_plan_create: multiplicity[%d] < 1", r);
+    }
+
+    tkv_plan* p = new (std::nothrow) tkv_plan();
+    if (!p) return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
+    try {
+        p->shape = s;
+        p->group = G;
+        tkv_plan_stats& st = p->stats;
+        st.n_rows = n_rows;
+        st.n_qtok = n_rows ? q_indptr[n_rows] : 0;
+        const int32_t tpt = tkv::kTileRows / G;  // query tokens per tile
+
+        // ------------------------------------------------------------ accounting
+        {
+            std::vector<uint8_t> seen(s.num_blocks, 0);
+            for (int32_t r = 0; r < n_rows; ++r) {
+                p->all_decode = p->all_decode && L[r] == 1;
+                st.logical_qtok += static_cast<int64_t>(multiplicity ? multiplicity[r] : 1) * L[r];
+                st.path_kv_tokens += N[r];
+                for (int32_t i = 0; i < L[r]; ++i) st.flops += 4ll * s.d * s.hq * (N[r] - L[r] + i + 1);
+                for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1]; ++j) {
+                    const int32_t b = kv_blocks[j];
+                    if (!seen[b]) {
+                        seen[b] = 1;
+                        st.uniq_kv_tokens += block_len[b];
+                    }
+                }
+            }
+        }
+
+        // ------------------------------------------------------------ shared items (small rows)
+        std::vector<Node> nodes;
+        std::unordered_map<uint64_t, int32_t> child;
+        std::vector<std::vector<int32_t>> path(n_rows);
+        for (int32_t r = 0; r < n_rows; ++r) {
+            if (static_cast<int64_t>(L[r]) * G >= tkv::kTileRows) continue;
+            int32_t cur = -1;
+            for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1]; ++j) {
+                const int32_t b = kv_blocks[j];
+                const uint64_t key = (static_cast<uint64_t>(static_cast<uint32_t>(cur + 1)) << 32) | static_cast<uint32_t>(b);
+                auto it = child.find(key);
+                int32_t nd;
+                if (it == child.end()) {
+                    nd = static_cast<int32_t>(nodes.size());
+                    const int32_t pos0 = cur < 0 ? 0 : nodes[cur].pos0 + nodes[cur].len;
+                    nodes.push_back(Node{cur, b, block_len[b], pos0, 0, -1});
+                    child.emplace(key, nd);
+                } else {
+                    nd = it->second;
+                }
+                nodes[nd].count += 1;
+                path[r].push_back(nd);
+                cur = nd;
+            }
+        }
+        std::vector<Segment> segs;
+        for (int32_t nd = 0; nd < static_cast<int32_t>(nodes.size()); ++nd) {
+            Node& n = nodes[nd];
+            if (n.parent >= 0 && nodes[n.parent].count == n.count) {
+                n.seg = nodes[n.parent].seg;
+            } else {
+                n.seg = static_cast<int32_t>(segs.size());
+                segs.emplace_back();
+            }
+            segs[n.seg].nodes.push_back(nd);
+        }
+        for (int32_t r = 0; r < n_rows; ++r) {
+            int32_t last = -1;
+            for (int32_t nd : path[r]) {
+                if (nodes[nd].seg != last) {
+                    last = nodes[nd].seg;
+                    segs[last].rows.push_back(r);
+                }
+            }
+        }
+        st.n_segments = static_cast<int32_t>(segs.size());
+
+        std::vector<Chunk> chunks;
+        std::vector<int32_t> cover(st.n_qtok, 0);
+        for (const Segment& sg : segs) {
+            if (sg.rows.size() > 1) st.n_shared_segments += 1;
+            const int32_t nb = static_cast<int32_t>(sg.nodes.size());
+            const int32_t seg_blk_off = static_cast<int32_t>(p->blks.size());
+            for (int32_t nd : sg.nodes) p->blks.push_back(BlkDesc{nodes[nd].blk, nodes[nd].len});
+            tile_evenly(nb, kChunkBlocks, [&](int32_t a, int32_t e) {
+                Chunk c;
+                c.blk_off = seg_blk_off + a;
+                c.n_blk = e - a;
+                c.pos0 = nodes[sg.nodes[a]].pos0;
+                for (int32_t r : sg.rows) {
+                    for (int32_t i = 0; i < L[r]; ++i) {
+                        const int32_t lim = N[r] - L[r] + i;
+                        if (lim < c.pos0) continue;  // the whole chunk is in this token's future
+                        c.toks.push_back(TokDesc{q_indptr[r] + i, lim, -1, 0});
+                        cover[q_indptr[r] + i] += 1;
+                    }
+                }
+                if (!c.toks.empty()) chunks.push_back(std::move(c));
+            });
+        }
+        // partial slots for tokens covered by more than one chunk
+        std::vector<std::vector<int32_t>> slots_of(st.n_qtok);
+        for (Chunk& c : chunks)
+            for (TokDesc& t : c.toks)
+                if (cover[t.qtok] > 1) {
+                    t.slot = p->n_slots++;
+                    slots_of[t.qtok].push_back(t.slot);
+                }
+        for (int32_t q = 0; q < st.n_qtok; ++q) {
+            if (slots_of[q].empty()) continue;
+            p->merges.push_back(MergeDesc{q, static_cast<int32_t>(p->merge_slots.size()),
+                                          static_cast<int32_t>(slots_of[q].size()), 0});
+            p->merge_slots.insert(p->merge_slots.end(), slots_of[q].begin(), slots_of[q].end());
+        }
+        for (const Chunk& c : chunks) {
+            tile_evenly(static_cast<int32_t>(c.toks.size()), tpt, [&](int32_t a, int32_t e) {
+                const int32_t tok_off = static_cast<int32_t>(p->toks.size());
+                p->toks.insert(p->toks.end(), c.toks.begin() + a, c.toks.begin() + e);
+                for (int32_t h = 0; h < s.hkv; ++h)
+                    p->items.push_back(ItemDesc{h, tok_off, e - a, c.blk_off, c.n_blk, c.pos0, tkv::kItemShared, 0});
+            });
+        }
+        st.n_items_shared = static_cast<int32_t>(p->items.size());
+
+        // ------------------------------------------------------------ row items (large rows)
+        for (int32_t r = 0; r < n_rows; ++r) {
+            if (static_cast<int64_t>(L[r]) * G < tkv::kTileRows) continue;
+            const int32_t row_blk_off = static_cast<int32_t>(p->blks.size());
+            std::vector<int32_t> end_pos;  // end position of each block along the path
+            int32_t pos = 0;
+            for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1]; ++j) {
+                p->blks.push_back(BlkDesc{kv_blocks[j], block_len[kv_blocks[j]]});
+                pos += block_len[kv_blocks[j]];
+                end_pos.push_back(pos);
+            }
+            tile_evenly(L[r], tpt, [&](int32_t a, int32_t e) {
+                const int32_t max_lim = N[r] - L[r] + e - 1;
+                // blocks whose first position is <= max_lim
+                const int32_t nb = static_cast<int32_t>(std::upper_bound(end_pos.begin(), end_pos.end(), max_lim) - end_pos.begin()) + 1;
+                const int32_t nbk = std::min<int32_t>(nb, static_cast<int32_t>(end_pos.size()));
+                const int32_t tok_off = static_cast<int32_t>(p->toks.size());
+                for (int32_t i = a; i < e; ++i) p->toks.push_back(TokDesc{q_indptr[r] + i, N[r] - L[r] + i, -1, 0});
+                for (int32_t h = 0; h < s.hkv; ++h)
+                    p->items.push_back(ItemDesc{h, tok_off, e - a, row_blk_off, nbk, 0, tkv::kItemRow, 0});
+            });
+        }
+        st.n_items = static_cast<int32_t>(p->items.size());
+        st.n_items_row = st.n_items - st.n_items_shared;
+        st.n_slots = p->n_slots;
+        st.n_merge = static_cast<int32_t>(p->merges.size());
+
+        // Longest items first, so the tail of the launch is made of short ones.
+        std::stable_sort(p->items.begin(), p->items.end(),
+                         [](const ItemDesc& a, const ItemDesc& b) { return a.n_blk > b.n_blk; });
+
+        // ------------------------------------------------------------ workspace layout
+        auto bytes = [](size_t n, size_t e) { return n * e; };
+        size_t off = 0;
+        p->off_items = off;
+        off = align256(off + bytes(p->items.size(), sizeof(ItemDesc)));
+        p->off_toks = off;
+        off = align256(off + bytes(p->toks.size(), sizeof(TokDesc)));
+        p->off_blks = off;
+        off = align256(off + bytes(p->blks.size(), sizeof(BlkDesc)));
+        p->off_merges = off;
+        off = align256(off + bytes(p->merges.size(), sizeof(MergeDesc)));
+        p->off_mslots = off;
+        off = align256(off + bytes(p->merge_slots.size(), sizeof(int32_t)));
+        p->desc_bytes = off;
+        p->off_po = off;
+        off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq * s.d, sizeof(float)));
+        p->off_plse = off;
+        off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq, sizeof(float)));
+        p->total_bytes = std::max<size_t>(off, 256);
+        p->image.assign(p->desc_bytes, 0);
+        auto put = [&](size_t o, const void* src, size_t n) {
+            if (n) std::memcpy(p->image.data() + o, src, n);
+        };
+        put(p->off_items, p->items.data(), bytes(p->items.size(), sizeof(ItemDesc)));
+        put(p->off_toks, p->toks.data(), bytes(p->toks.size(), sizeof(TokDesc)));
+        put(p->off_blks, p->blks.data(), bytes(p->blks.size(), sizeof(BlkDesc)));
+        put(p->off_merges, p->merges.data(), bytes(p->merges.size(), sizeof(MergeDesc)));
+        put(p->off_mslots, p->merge_slots.data(), bytes(p->merge_slots.size(), sizeof(int32_t)));
+    } catch (...) {
+        delete p;
+        return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
+    }
+    *out = p;
+    return TKV_OK;
+}
+
+TKV_EXPORT size_t tkv_plan_workspace_bytes(const tkv_plan* p) { return p ? p->total_bytes : 0; }
+
+TKV_EXPORT void tkv_plan_destroy(tkv_plan* p) { delete p; }
+
+TKV_EXPORT int tkv_plan_get_stats(const tkv_plan* p, tkv_plan_stats* out) {
+    tkv::clear_error();
+    if (!p || !out) return set_error(TKV_EINVAL, "tkv_plan_get_stats: NULL argument");
+    *out = p->stats;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_plan_get_view(const tkv_plan* p, tkv_plan_view* out) {
+    tkv::clear_error();
+    if (!p || !out) return set_error(TKV_EINVAL, "tkv_plan_get_view: NULL argument");
+    out->items = reinterpret_cast<const int32_t*>(p->items.data());
+    out->toks = reinterpret_cast<const int32_t*>(p->toks.data());
+    out->blks = reinterpret_cast<const int32_t*>(p->blks.data());
+    out->merges = reinterpret_cast<const int32_t*>(p->merges.data());
+    out->merge_slots = p->merge_slots.data();
+    out->n_items = static_cast<int32_t>(p->items.size());
+    out->n_toks = static_cast<int32_t>(p->toks.size());
+    out->n_blks = static_cast<int32_t>(p->blks.size());
+    out->n_merge = static_cast<int32_t>(p->merges.size());
+    out->n_merge_slots = static_cast<int32_t>(p->merge_slots.size());
+    out->n_slots = p->n_slots;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_plan_upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream) {
+    tkv::clear_error();
+    if (!p || !d_ws) return set_error(TKV_EINVAL, "tkv_plan_upload: NULL argument");
+    if (bytes < p->total_bytes)
+        return set_error(TKV_EINVAL, "tkv_plan_upload: workspace of %zu bytes < %zu needed", bytes, p->total_bytes);
+    if (reinterpret_cast<uintptr_t>(d_ws) & 255) return set_error(TKV_EINVAL, "tkv_plan_upload: workspace not 256-byte aligned");
+    return tkv::upload(p, d_ws, bytes, stream);
+}
+
+TKV_EXPORT int tkv_decode(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
+                          void* stream) {
+    tkv::clear_error();
+    if (!p) return set_error(TKV_EINVAL, "tkv_decode: plan is NULL");
+    if (!p->all_decode) return set_error(TKV_EINVAL, "tkv_decode: every row must have q_len 1 (use tkv_verify)");
+    return tkv::launch_attention(p, q, k, v, o, lse, stream);
+}
+
+TKV_EXPORT int tkv_verify(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
+                          void* stream) {
+    tkv::clear_error();
+    if (!p) return set_error(TKV_EINVAL, "tkv_verify: plan is NULL");
+    return tkv::launch_attention(p, q, k, v, o, lse, stream);
+}

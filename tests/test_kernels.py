@@ -1,0 +1,139 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Tolerance (bf16 inputs, fp32 accumulation, bf16 output): max |o - o_ref| <= 1e-2 and
+mean |o - o_ref| <= 1e-3; lse within 2e-3.  Block tables and coalescing are compared exactly.
+Padding slots of partial blocks and every free block hold bf16 NaN, so any read of padding shows.
+Small workloads are compared in full; the full-size workloads are run in the launch
+configuration the benchmark times and compared on a seeded sample of rows.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from _harness import realize_native, realize_oracle
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS, LSE_ABS = 1e-2, 1e-3, 2e-3
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _dev(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _f64(bits):
+    return W.bf16_bits_to_f32(bits).astype(np.float64)
+
+
+def run_gpu(wl, launch, poison=True, kv=None, repeat=1):
+    """Realise the workload on the C block manager and run one launch on the GPU.
+    Returns (batch, o float32 [n_qtok, hq, d], lse [n_qtok, hq], k bits, v bits, plan stats)."""
+    import paper_2609_39334_amd as tkv
+    b = realize_native(wl)[launch]
+    s = wl.shape
+    k, v = kv if kv is not None else wl.kv_values()
+    if poison:
+        k, v = k.copy(), v.copy()
+        W.poison_padding(k, v, b.block_len)
+    q = wl.q_values(launch, b.n_qtok)
+    qi, ki, kb = b.arrays()
+    _log(f"  gpu: {wl.name} launch {launch}: rows {len(b.q_lens)} qtok {b.n_qtok} (hq {s.hq} hkv {s.hkv} d {s.d})")
+    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, b.block_len, b.mult)
+    qd, kd, vd = _dev(q), _dev(k), _dev(v)
+    outs = []
+    for _ in range(repeat):
+        o = torch.full((b.n_qtok, s.hq, s.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((b.n_qtok, s.hq), float("nan"), dtype=torch.float32, device="cuda")
+        if b.decode:
+            plan.decode(qd, kd, vd, o, lse)
+        else:
+            plan.verify(qd, kd, vd, o, lse)
+        torch.cuda.synchronize()
+        outs.append((o.float().cpu().numpy(), lse.cpu().numpy()))
+    return b, outs, k, v, q, plan.stats
+
+
+def compare(wl, launch, rows=None, poison=True, repeat=1):
+    b, outs, k, v, q, st = run_gpu(wl, launch, poison=poison, repeat=repeat)
+    ob = realize_oracle(wl)[launch]
+    assert ob.tables == b.tables and ob.q_lens == b.q_lens and ob.mult == b.mult
+    o_ref, l_ref = oracle.attention(_f64(q), W.bf16_bits_to_f32(k), W.bf16_bits_to_f32(v), ob.tables,
+                                    ob.block_len, ob.q_lens, rows=rows)
+    o, l = outs[0]
+    sel = np.ones(b.n_qtok, dtype=bool) if rows is None else np.zeros(b.n_qtok, dtype=bool)
+    if rows is not None:
+        qoff = np.concatenate([[0], np.cumsum(b.q_lens)])
+        for r in rows:
+            sel[qoff[r]:qoff[r + 1]] = True
+    err = np.abs(o[sel] - o_ref[sel])
+    lerr = np.abs(l[sel] - l_ref[sel])
+    _log(f"    max {err.max():.2e} mean {err.mean():.2e} lse max {lerr.max():.2e} over {sel.sum()} tokens")
+    assert np.isfinite(o[sel]).all() and np.isfinite(l[sel]).all()
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
+    assert lerr.max() <= LSE_ABS
+    for o2, l2 in outs[1:]:        # run-to-run determinism (no atomics in the reductions)
+        assert np.array_equal(o2, o) and np.array_equal(l2, l)
+    return b, st
+
+
+def test_tiny_decode_full():
+    compare(W.tiny_decode(0), 0, repeat=2)
+
+
+@pytest.mark.parametrize("seed,hq,hkv,d", [(0, 8, 2, 64), (1, 12, 2, 128), (2, 28, 4, 128), (3, 32, 8, 128),
+                                           (4, 4, 4, 64), (5, 14, 2, 64), (6, 64, 1, 128), (7, 16, 1, 64)])
+def test_random_trees_full(seed, hq, hkv, d):
+    wl = W.random_tree(seed, W.Shape(hq, hkv, d), n_roots=3, depth=3, max_branch=3, max_step=70)
+    compare(wl, 0)
+
+
+def test_verify_long_steps_and_single_token_rows():
+    # long verify steps (row items), q_len == kv_len rows (a root verified whole), kv_len 1 rows
+    wl = W.Workload("edge", W.Shape(12, 2, 128), 11)
+    rt = np.random.default_rng(5)
+    root = wl.extend(-1, rt.integers(0, 100, 300), True)
+    a = wl.extend(root, rt.integers(0, 100, 256), True)
+    b = wl.extend(root, rt.integers(0, 100, 17), True)
+    one = wl.extend(-1, [7], True)
+    lone = wl.extend(-1, rt.integers(0, 100, 40), True)
+    c = wl.extend(one, [], True)            # fork with no new tokens
+    wl.launch("mixed", [(a, 256), (b, 17), (one, 1), (lone, 40), (c, 1), (root, 300)])
+    wl.finalize()
+    compare(wl, 0)
+
+
+@pytest.mark.parametrize("name", ["beam_decode", "step_verify"])
+def test_full_size_small_configs(name):
+    wl = W.CONFIGS[name](0)
+    rows = None
+    if name == "step_verify":
+        rows = list(range(0, 128, 9))
+    compare(wl, 0, rows=rows, poison=False, repeat=2)
+
+
+def test_spec_explosion_sampled():
+    wl = W.spec_explosion(0)
+    rng = np.random.default_rng(1)
+    rows = sorted(rng.choice(1627, 60, replace=False).tolist() + [0, 1626])
+    b, st = compare(wl, 0, rows=rows, poison=False)
+    assert st["n_rows"] < 2048          # identical leaves coalesced
+
+
+def test_mixed_serving_both_launches_sampled():
+    wl = W.mixed_serving(0)
+    kv = wl.kv_values()
+    for launch in (0, 1):
+        b = realize_native(wl)[launch]
+        rng = np.random.default_rng(2 + launch)
+        rows = sorted(rng.choice(len(b.q_lens), 40, replace=False).tolist())
+        compare(wl, launch, rows=rows, poison=False)
