@@ -125,7 +125,7 @@ int tkv_bm_coalesce(const tkv_bm* bm, int32_t n_cand, const int32_t* seqs, const
  *   k, v   [num_blocks][hkv][block_size][d] bf16 (the paged pool; slots past a block's length are
  *          never read)
  *   lse    [n_qtok][hq] fp32, nullable
- * Supported: block_size 16, d in {64, 128}, hq % hkv == 0, hq / hkv <= 64.
+ * Supported: block_size 16, d in {64, 128}, hq % hkv == 0, hq / hkv <= 64, hq <= 256.
  */
 typedef struct {
     int32_t hq, hkv, d, block_size, num_blocks;

@@ -1,6 +1,6 @@
 // Tree-shared paged attention kernels for gfx950 (MI355X).
 //
-// attn_items: one workgroup per work item (see plan.cpp).  An item is a tile of up to 64 query
+// attn_persist: persistent workgroups, each walking its list of work items (see plan.cpp).  An item is a tile of up to 64 query
 // rows -- query tokens x the G query heads of one KV head -- and an ordered list of KV blocks.
 // K/V blocks are staged through LDS four at a time (64 keys) and every wave contracts them
 // against its 16 query rows on bf16 MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulation):
@@ -24,6 +24,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
 
@@ -31,187 +32,337 @@ __device__ __forceinline__ f32x4_t mfma_16x16x32(bf16x8_t a, bf16x8_t b, f32x4_t
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// fp32 -> bf16, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) { return bf16_rne(lo) | (bf16_rne(hi) << 16); }
+// Two fp32 -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
 
 constexpr int kThreads = 256;
 constexpr int kKeysPerStage = 64;  // four 16-token blocks
 
+// One stage as the kernel sees it after decoding its descriptor (scalar registers).
+struct StageInfo {
+    int len[4], pos[4];
+    int kvh, n_tok, flags;
+};
+
+// Lane l loads 16-byte word min(l & 7, 4) of the stage descriptor's header: lanes 0..3 hold
+// blocks[0..3] = {blk, len, pos, -} and lane 4 holds {kvh, n_tok, flags, -}, so a block's fields
+// come out with v_readlane at a (uniform) lane index -- no select chains, no branches.
+__device__ __forceinline__ int4 load_hdr(const tkv::StageDesc* __restrict__ stages, int gs, int lane) {
+    return reinterpret_cast<const int4*>(stages + gs)[min(lane & 7, 4)];
+}
+__device__ __forceinline__ int4 load_tok(const tkv::StageDesc* __restrict__ stages, int gs, int t) {
+    return reinterpret_cast<const int4*>(stages[gs].toks)[t];
+}
+
+__device__ __forceinline__ StageInfo decode_hdr(const int4& h) {
+    StageInfo si;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        si.len[j] = __builtin_amdgcn_readlane(h.y, j);
+        si.pos[j] = __builtin_amdgcn_readlane(h.z, j);
+    }
+    si.kvh = __builtin_amdgcn_readlane(h.x, 4);
+    si.n_tok = __builtin_amdgcn_readlane(h.y, 4);
+    si.flags = __builtin_amdgcn_readlane(h.z, 4);
+    return si;
+}
+
+// Registers of one stage owned by this thread: K in row layout, V as KPV consecutive keys x 8
+// dims (transposed into key-contiguous words on the way to LDS).
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_items(
-    const tkv::ItemDesc* __restrict__ items, const tkv::TokDesc* __restrict__ toks,
-    const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
-    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse,
-    float* __restrict__ po, float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
-    constexpr int KSTR = D + 8;                // K row stride in LDS (elements): 16-B reads spread over banks
-    constexpr int VSTR = kKeysPerStage + 4;    // V^T row stride (elements)
-    constexpr int NKS = D / 32;                // k-steps of the QK^T contraction
-    constexpr int NCT = D / 16;                // 16-column tiles of the output
-    constexpr int DCH = D / 8;                 // 16-byte chunks per K/V row
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeysPerStage * KSTR];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VSTR];
+struct StageRegs {
+    static constexpr int DCH = D / 8;                          // 16-byte chunks per row
+    static constexpr int KPT = kKeysPerStage * DCH / kThreads;  // K chunks per thread
+    static constexpr int KPV = D == 128 ? 4 : 2;                // V keys per thread
+    u32x4_t k[KPT];
+    u32x4_t v[KPV];
+};
 
-    const tkv::ItemDesc it = items[blockIdx.x];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int col = lane & 15, kg = lane >> 4;
-    const int mrow = wave * 16 + col;  // this lane's query row in the tile (token-major, head-minor)
-    const int t = mrow / G, g = mrow - t * G;
-    const bool row_ok = t < it.n_tok;
-    const bool wave_active = wave * 16 < it.n_tok * G;
-    int qtok = 0, limit = -1, slot = -1;
-    if (row_ok) {
-        const tkv::TokDesc td = toks[it.tok_off + t];
-        qtok = td.qtok;
-        limit = td.limit;
-        slot = td.slot;
+// All loads are straight-line (so the compiler's wait counts stay exact and nothing drains the
+// prefetch early).  A thread's block is uniform across its wave, read from the header with
+// v_readlane; a slot past the block's length reads the block's last row (masked in the softmax,
+// so it contributes exactly 0); an absent block reads the stage's first block.  valid = false
+// turns every length to 0 (the fetch past the end of the stream reads one row per block).
+template <int D>
+__device__ __forceinline__ void stage_load(StageRegs<D>& r, const int4& h, bool valid, int kvh,
+                                           const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
+                                           int hkv, int tid, int wave_u) {
+    constexpr int DCH = StageRegs<D>::DCH;
+#pragma unroll
+    for (int i = 0; i < StageRegs<D>::KPT; ++i) {
+        const int c = tid + kThreads * i;
+        const int dc = c % DCH, sl = (c / DCH) & 15;
+        const int j = D == 128 ? i : 2 * i + (wave_u >> 1);   // c / (16 * DCH), uniform per wave
+        const int id = __builtin_amdgcn_readlane(h.x, j);
+        const int len = valid ? __builtin_amdgcn_readlane(h.y, j) : 0;
+        const int se = min(sl, max(len - 1, 0));
+        const uint16_t* base = kpool + (static_cast<size_t>(id) * hkv + kvh) * (16 * D);
+        r.k[i] = *reinterpret_cast<const u32x4_t*>(base + se * D + dc * 8);
     }
-    const int h = it.kvh * G + g;
-
-    bf16x8_t qf[NKS];
+    constexpr int KPV = StageRegs<D>::KPV;
+    const int id = __builtin_amdgcn_readlane(h.x, wave_u);   // this wave's V keys lie in block `wave`
+    const int len = valid ? __builtin_amdgcn_readlane(h.y, wave_u) : 0;
+    const uint16_t* base = vpool + (static_cast<size_t>(id) * hkv + kvh) * (16 * D);
+    const int kq = tid / DCH, dc = tid % DCH;   // keys KPV*kq .. +KPV-1 of the stage, dims 8dc..8dc+7
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-        uint4 u = make_uint4(0, 0, 0, 0);
-        if (row_ok) u = *reinterpret_cast<const uint4*>(q + (static_cast<size_t>(qtok) * hq + h) * D + ks * 32 + kg * 8);
-        qf[ks] = as_bf16x8(u);
+    for (int i = 0; i < KPV; ++i) {
+        const int sl = (KPV * kq + i) & 15;
+        const int se = min(sl, max(len - 1, 0));
+        r.v[i] = *reinterpret_cast<const u32x4_t*>(base + se * D + dc * 8);
     }
-    f32x4_t acc[NCT];
-#pragma unroll
-    for (int c = 0; c < NCT; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;
-    int pos = it.pos0;
+}
 
-    for (int b0 = 0; b0 < it.n_blk; b0 += 4) {
-        const int nb = min(4, it.n_blk - b0);
-        int blen[4], bpos[4], bid[4];
+template <int D, int KSTR, int VSTR>
+__device__ __forceinline__ void stage_store(const StageRegs<D>& r, uint16_t* Ks, uint16_t* Vt, int tid) {
+    constexpr int DCH = StageRegs<D>::DCH;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            int len = 0, id = 0;
-            if (j < nb) {
-                const tkv::BlkDesc bd = blks[it.blk_off + b0 + j];
-                len = bd.len;
-                id = bd.blk;
-            }
-            blen[j] = len;
-            bid[j] = id;
-            bpos[j] = pos;
-            pos += len;
-        }
-        __syncthreads();  // the previous stage's LDS reads are done
-        for (int c = tid; c < 4 * 16 * DCH; c += kThreads) {
-            const int dc = c % DCH, sl = (c / DCH) & 15, j = c / (16 * DCH);
-            // select rather than index, so the small arrays stay in registers
-            const int len_j = j == 0 ? blen[0] : j == 1 ? blen[1] : j == 2 ? blen[2] : blen[3];
-            const int id_j = j == 0 ? bid[0] : j == 1 ? bid[1] : j == 2 ? bid[2] : bid[3];
-            uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-            if (sl < len_j) {
-                const size_t base = ((static_cast<size_t>(id_j) * hkv + it.kvh) * 16 + sl) * D + dc * 8;
-                kv = *reinterpret_cast<const uint4*>(kpool + base);
-                vv = *reinterpret_cast<const uint4*>(vpool + base);
-            }
-            *reinterpret_cast<uint4*>(&Ks[(j * 16 + sl) * KSTR + dc * 8]) = kv;
-            const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+    for (int i = 0; i < StageRegs<D>::KPT; ++i) {
+        const int c = tid + kThreads * i;
+        const int dc = c % DCH, key = c / DCH;
+        *reinterpret_cast<u32x4_t*>(&Ks[key * KSTR + dc * 8]) = r.k[i];
+    }
+    const int kq = tid / DCH, dc = tid % DCH;
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                Vt[(dc * 8 + e) * VSTR + j * 16 + sl] = static_cast<uint16_t>(vw[e >> 1] >> (16 * (e & 1)));
+    for (int e = 0; e < 8; ++e) {
+        // dim 8dc+e of consecutive keys -> bf16 pairs (key 2m in the low half)
+        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+        if constexpr (D == 128) {
+            uint2 out;
+            out.x = __builtin_amdgcn_perm(r.v[1][e >> 1], r.v[0][e >> 1], sel);
+            out.y = __builtin_amdgcn_perm(r.v[3][e >> 1], r.v[2][e >> 1], sel);
+            *reinterpret_cast<uint2*>(&Vt[(dc * 8 + e) * VSTR + 4 * kq]) = out;
+        } else {
+            *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + e) * VSTR + 2 * kq]) =
+                __builtin_amdgcn_perm(r.v[1][e >> 1], r.v[0][e >> 1], sel);
         }
-        __syncthreads();
-        if (!wave_active) continue;
+    }
+}
 
-        f32x4_t s[4];
+// Per-lane view of the current item's query row: lane (wave w, column c) owns tile row 16w + c,
+// i.e. query token t = row / G of the tile and head g = row % G of the item's KV head.
+template <int D>
+struct RowState {
+    int qtok, limit, slot, h;
+    bool row_ok, wave_active;
+    bf16x8_t qf[D / 32];  // this row's query, k-step ks holding dims 32ks + 8kg .. +7
+};
+
+// Rows of a stage's item from its decoded header and this lane's token entry (loaded a step
+// earlier, so the query loads below depend on nothing in flight).  A row past the tile reads
+// token 0's entry of the descriptor (zero-filled) and is never written.
+template <int D>
+__device__ __forceinline__ void make_rows(RowState<D>& rs, const StageInfo& si, const int4& tk,
+                                          const uint16_t* __restrict__ q, int hq, int G, int wave, int t, int g,
+                                          int kg) {
+    rs.row_ok = t < si.n_tok;
+    rs.wave_active = wave * 16 < si.n_tok * G;
+    rs.qtok = tk.x;
+    rs.limit = tk.y;
+    rs.slot = tk.z;
+    rs.h = si.kvh * G + g;
+    const uint16_t* qrow = q + (static_cast<size_t>(rs.qtok) * hq + rs.h) * D + kg * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) rs.qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
+}
+
+// Workgroup barrier that orders LDS only.  __syncthreads() also waits for every outstanding global
+// load (its release fence), which would drain the K/V prefetch at each stage.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Compute-side state of the current item.
+template <int D>
+struct Acc {
+    f32x4_t acc[D / 16];
+    float m_run, l_run;
+    __device__ __forceinline__ void reset() {
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        m_run = -INFINITY;
+        l_run = 0.f;
+    }
+};
+
+template <int D, int KSTR, int VSTR>
+__device__ __forceinline__ void contract_stage(Acc<D>& A, const RowState<D>& rs, const StageInfo& sb,
+                                               const uint16_t* Ks, const uint16_t* Vt, int col, int kg, float sl2) {
+    constexpr int NKS = D / 32, NCT = D / 16;
+    f32x4_t s[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+        s[st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const uint4 a = *reinterpret_cast<const uint4*>(&Ks[(st * 16 + col) * KSTR + ks * 32 + kg * 8]);
+            s[st] = mfma_16x16x32(as_bf16x8(a), rs.qf[ks], s[st]);
+        }
+    }
+    // lane holds keys st*16 + 4*kg + r (r = 0..3) of its query row.  Masking is needed only when a
+    // block is partial or some row of the wave has a causal limit inside the stage (wave-uniform).
+    const bool row_full = sb.len[0] + sb.len[1] + sb.len[2] + sb.len[3] == 64 && rs.limit >= sb.pos[0] + 63;
+    if (__builtin_amdgcn_ballot_w64(!row_full) != 0) {
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
-            s[st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            const int vlen = min(sb.len[st], rs.limit - sb.pos[st] + 1);  // visible slots of this block
 #pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
-                const uint4 a = *reinterpret_cast<const uint4*>(&Ks[(st * 16 + col) * KSTR + ks * 32 + kg * 8]);
-                s[st] = mfma_16x16x32(as_bf16x8(a), qf[ks], s[st]);
-            }
-        }
-        // lane holds keys st*16 + 4*kg + r (r = 0..3) of its query row
-        float mx = -INFINITY;
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int sl = 4 * kg + r;
-                const bool ok = sl < blen[st] && bpos[st] + sl <= limit;
-                const float v = ok ? s[st][r] : -INFINITY;
-                s[st][r] = v;
-                mx = fmaxf(mx, v);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        float alpha = 1.f, msc = 0.f;
-        if (m_new != -INFINITY) {
-            alpha = exp2f((m_run - m_new) * sl2);
-            msc = m_new * sl2;
-        }
-        float psum = 0.f;
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float v = s[st][r];
-                const float p = v == -INFINITY ? 0.f : exp2f(fmaf(v, sl2, -msc));
-                s[st][r] = p;
-                psum += p;
-            }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-#pragma unroll
-        for (int c = 0; c < NCT; ++c) acc[c] *= alpha;
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            // k index e of this lane: keys 32kk + 4kg + e (e < 4) and 32kk + 16 + 4kg + (e - 4)
-            uint4 pu;
-            pu.x = pack_bf16x2(s[2 * kk][0], s[2 * kk][1]);
-            pu.y = pack_bf16x2(s[2 * kk][2], s[2 * kk][3]);
-            pu.z = pack_bf16x2(s[2 * kk + 1][0], s[2 * kk + 1][1]);
-            pu.w = pack_bf16x2(s[2 * kk + 1][2], s[2 * kk + 1][3]);
-            const bf16x8_t pf = as_bf16x8(pu);
-#pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) {
-                const uint16_t* vrow = &Vt[(ct * 16 + col) * VSTR + kk * 32 + kg * 4];
-                const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-                const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
-                acc[ct] = mfma_16x16x32(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pf, acc[ct]);
-            }
+            for (int r = 0; r < 4; ++r)
+                if (4 * kg + r >= vlen) s[st][r] = -INFINITY;
         }
     }
+    float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                     fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+    mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[2][0], s[2][1]), fmaxf(s[2][2], s[2][3])),
+                         fmaxf(fmaxf(s[3][0], s[3][1]), fmaxf(s[3][2], s[3][3]))));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(A.m_run, mx);
+    // exp2(-inf) = 0, so masked keys need no select; a row with no visible key yet keeps msc = 0
+    const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            s[st][r] = __builtin_amdgcn_exp2f(fmaf(s[st][r], sl2, -msc));
+            psum += s[st][r];
+        }
+    const float alpha = m_new == A.m_run ? 1.f : __builtin_amdgcn_exp2f(A.m_run * sl2 - msc);
+    A.l_run = fmaf(A.l_run, alpha, psum);
+    A.m_run = m_new;
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {  // rescale only when some row's max grew
+#pragma unroll
+        for (int c = 0; c < NCT; ++c) A.acc[c] *= alpha;
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+        // k index e of this lane: keys 32kk + 4kg + e (e < 4) and 32kk + 16 + 4kg + (e - 4)
+        uint4 pu;
+        pu.x = pack_bf16x2(s[2 * kk][0], s[2 * kk][1]);
+        pu.y = pack_bf16x2(s[2 * kk][2], s[2 * kk][3]);
+        pu.z = pack_bf16x2(s[2 * kk + 1][0], s[2 * kk + 1][1]);
+        pu.w = pack_bf16x2(s[2 * kk + 1][2], s[2 * kk + 1][3]);
+        const bf16x8_t pf = as_bf16x8(pu);
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+            const uint16_t* vrow = &Vt[(ct * 16 + col) * VSTR + kk * 32 + kg * 4];
+            const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+            const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+            A.acc[ct] = mfma_16x16x32(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pf, A.acc[ct]);
+        }
+    }
+}
 
-    float l_tot = l_run + __shfl_xor(l_run, 16);
+template <int D>
+__device__ __forceinline__ void write_item(const Acc<D>& A, const RowState<D>& rs, int kg, uint16_t* __restrict__ o,
+                                           float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse,
+                                           int hq, float sl2) {
+    constexpr int NCT = D / 16;
+    float l_tot = A.l_run + __shfl_xor(A.l_run, 16);
     l_tot += __shfl_xor(l_tot, 32);
-    if (!row_ok) return;
+    if (!rs.row_ok) return;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float lse_v = l_tot > 0.f ? (m_run * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
+    const float lse_v = l_tot > 0.f ? (A.m_run * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
     // lane holds output columns ct*16 + 4*kg + r of its row
-    if (slot < 0) {
-        uint16_t* orow = o + (static_cast<size_t>(qtok) * hq + h) * D;
+    if (rs.slot < 0) {
+        uint16_t* orow = o + (static_cast<size_t>(rs.qtok) * hq + rs.h) * D;
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
             uint2 w;
-            w.x = pack_bf16x2(acc[ct][0] * inv, acc[ct][1] * inv);
-            w.y = pack_bf16x2(acc[ct][2] * inv, acc[ct][3] * inv);
+            w.x = pack_bf16x2(A.acc[ct][0] * inv, A.acc[ct][1] * inv);
+            w.y = pack_bf16x2(A.acc[ct][2] * inv, A.acc[ct][3] * inv);
             *reinterpret_cast<uint2*>(orow + ct * 16 + kg * 4) = w;
         }
-        if (lse && kg == 0) lse[static_cast<size_t>(qtok) * hq + h] = lse_v;
+        if (lse && kg == 0) lse[static_cast<size_t>(rs.qtok) * hq + rs.h] = lse_v;
     } else {
-        float* prow = po + (static_cast<size_t>(slot) * hq + h) * D;
+        float* prow = po + (static_cast<size_t>(rs.slot) * hq + rs.h) * D;
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct)
             *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) =
-                make_float4(acc[ct][0] * inv, acc[ct][1] * inv, acc[ct][2] * inv, acc[ct][3] * inv);
-        if (kg == 0) plse[static_cast<size_t>(slot) * hq + h] = lse_v;
+                make_float4(A.acc[ct][0] * inv, A.acc[ct][1] * inv, A.acc[ct][2] * inv, A.acc[ct][3] * inv);
+        if (kg == 0) plse[static_cast<size_t>(rs.slot) * hq + rs.h] = lse_v;
     }
 }
+
+// One workgroup per resident slot (persistent): it walks the planner's stream of 64-key stages
+// for this slot (items split into stages, items back to back).  While stage k is contracted from
+// LDS, stage k+1's K/V and its item's query rows are in flight into registers, and stage k+2's
+// descriptor is in flight too -- every load of the loop body is straight-line and depends on
+// nothing issued in the same step.  At an item boundary the rows are swapped in by selects.
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 3))) void attn_persist(
+    const tkv::StageDesc* __restrict__ stages, const int32_t* __restrict__ wg_off, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
+    float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
+    constexpr int KSTR = D + 8;                // K row stride in LDS (elements): 16-B reads spread over banks
+    constexpr int VSTR = kKeysPerStage + 4;    // V^T row stride (elements): 8-B reads of 16 rows spread over banks
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeysPerStage * KSTR];
+    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VSTR];
+
+    const int s0 = wg_off[blockIdx.x], s1 = wg_off[blockIdx.x + 1];
+    if (s0 >= s1) return;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int col = lane & 15, kg = lane >> 4;
+    const int mrow = wave * 16 + col;  // this lane's row of the tile (token-major, head-minor)
+    const int t = mrow / G, g = mrow - t * G;
+    const int trow = min(t, tkv::kTileRows - 1);
+
+    int4 h = load_hdr(stages, s0, lane);
+    int4 tk = load_tok(stages, s0, trow);
+    StageInfo si = decode_hdr(h);
+    StageRegs<D> r;
+    stage_load<D>(r, h, true, si.kvh, kpool, vpool, hkv, tid, wave_u);
+    RowState<D> rs, rs_n;
+    make_rows<D>(rs, si, tk, q, hq, G, wave, t, g, kg);
+    int gnext = s0 + 1;  // next stage to fetch
+    h = load_hdr(stages, min(gnext, s1 - 1), lane);
+    tk = load_tok(stages, min(gnext, s1 - 1), trow);
+    Acc<D> A;
+    A.reset();
+
+    for (;;) {
+        const StageInfo cur = si;
+        lds_barrier();  // the previous stage's LDS reads are done
+        stage_store<D, KSTR, VSTR>(r, Ks, Vt, tid);
+        lds_barrier();
+        const bool has_next = gnext < s1;
+        si = decode_hdr(h);
+        make_rows<D>(rs_n, si, tk, q, hq, G, wave, t, g, kg);
+        stage_load<D>(r, h, has_next, si.kvh, kpool, vpool, hkv, tid, wave_u);
+        ++gnext;
+        h = load_hdr(stages, min(gnext, s1 - 1), lane);
+        tk = load_tok(stages, min(gnext, s1 - 1), trow);
+        if (__builtin_amdgcn_readfirstlane(rs.wave_active))
+            contract_stage<D, KSTR, VSTR>(A, rs, cur, Ks, Vt, col, kg, sl2);
+        const bool last = cur.flags & tkv::kStageLast;
+        if (last) {
+            write_item<D>(A, rs, kg, o, lse, po, plse, hq, sl2);
+            if (!has_next) break;
+            A.reset();
+        }
+        rs.qtok = last ? rs_n.qtok : rs.qtok;
+        rs.limit = last ? rs_n.limit : rs.limit;
+        rs.slot = last ? rs_n.slot : rs.slot;
+        rs.h = last ? rs_n.h : rs.h;
+        rs.row_ok = last ? rs_n.row_ok : rs.row_ok;
+        rs.wave_active = last ? rs_n.wave_active : rs.wave_active;
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) rs.qf[ks] = last ? rs_n.qf[ks] : rs.qf[ks];
+    }
+}
+
+// Log-sum-exp merge of one query token's partials (one workgroup per token).  Slot ids, then all
+// partial lse values, then all partial outputs are each fetched in one parallel round, so the
+// token costs three memory latencies however many partials it has (up to kMergeChunk at a time).
+constexpr int kMergeChunk = 32;
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void merge_partials(const tkv::MergeDesc* __restrict__ md,
@@ -219,22 +370,103 @@ __global__ __launch_bounds__(kThreads) void merge_partials(const tkv::MergeDesc*
                                                            const float* __restrict__ po,
                                                            const float* __restrict__ plse,
                                                            uint16_t* __restrict__ o, float* __restrict__ lse, int hq) {
+    extern __shared__ float sm[];              // w[kMergeChunk][hq], mx[hq], sum[hq]
+    __shared__ int sid[kMergeChunk];
+    float* w = sm;
+    float* mxs = sm + kMergeChunk * hq;
+    float* sums = mxs + hq;
     const tkv::MergeDesc m = md[blockIdx.x];
-    for (int idx = threadIdx.x; idx < hq * D; idx += kThreads) {
-        const int h = idx / D, c = idx - h * D;
-        float mx = -INFINITY;
-        for (int j = 0; j < m.n_slots; ++j) mx = fmaxf(mx, plse[static_cast<size_t>(mslots[m.slot_off + j]) * hq + h]);
-        float ws = 0.f, acc = 0.f;
-        if (mx != -INFINITY) {
-            for (int j = 0; j < m.n_slots; ++j) {
-                const size_t sl = static_cast<size_t>(mslots[m.slot_off + j]);
-                const float w = expf(plse[sl * hq + h] - mx);
-                ws += w;
-                acc += w * po[(sl * hq + h) * D + c];
+    const int tid = threadIdx.x;
+    constexpr int C4 = D / 4;
+    // pass 1: running max and sum over all partials, chunk by chunk
+    for (int h = tid; h < hq; h += kThreads) {
+        mxs[h] = -INFINITY;
+        sums[h] = 0.f;
+    }
+    for (int c0 = 0; c0 < m.n_slots; c0 += kMergeChunk) {
+        const int n = min(kMergeChunk, m.n_slots - c0);
+        __syncthreads();
+        if (tid < n) sid[tid] = mslots[m.slot_off + c0 + tid];
+        __syncthreads();
+        for (int i = tid; i < n * hq; i += kThreads) {
+            const int j = i / hq, h = i - j * hq;
+            w[i] = plse[static_cast<size_t>(sid[j]) * hq + h];
+        }
+        __syncthreads();
+        for (int h = tid; h < hq; h += kThreads) {
+            float mx = mxs[h];
+            for (int j = 0; j < n; ++j) mx = fmaxf(mx, w[j * hq + h]);
+            float sum = mx == -INFINITY ? 0.f : sums[h] * __expf(mxs[h] - mx);
+            if (mx != -INFINITY)
+                for (int j = 0; j < n; ++j) sum += __expf(w[j * hq + h] - mx);
+            mxs[h] = mx;
+            sums[h] = sum;
+        }
+    }
+    __syncthreads();
+    for (int h = tid; h < hq; h += kThreads)
+        if (lse) lse[static_cast<size_t>(m.qtok) * hq + h] = sums[h] > 0.f ? mxs[h] + __logf(sums[h]) : -INFINITY;
+    // pass 2: weighted sum of the partial outputs
+    constexpr int kPer = (64 * C4 + kThreads - 1) / kThreads;   // float4 chunks per thread for hq <= 64
+    float4 acc[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int h0 = 0; h0 < hq; h0 += 64) {
+        const int hn = min(64, hq - h0);
+        for (int c0 = 0; c0 < m.n_slots; c0 += kMergeChunk) {
+            const int n = min(kMergeChunk, m.n_slots - c0);
+            __syncthreads();
+            if (tid < n) sid[tid] = mslots[m.slot_off + c0 + tid];
+            __syncthreads();
+            for (int i = tid; i < n * hn; i += kThreads) {
+                const int j = i / hn, h = h0 + i - j * hn;
+                const float s = sums[h];
+                w[j * hq + h] = s > 0.f ? __expf(plse[static_cast<size_t>(sid[j]) * hq + h] - mxs[h]) / s : 0.f;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int u = 0; u < kPer; ++u) {
+                const int idx = tid + u * kThreads;
+                if (idx >= hn * C4) continue;
+                const int h = h0 + idx / C4, c = (idx % C4) * 4;
+                float4 a = acc[u];
+                int j = 0;
+                for (; j + 4 <= n; j += 4) {   // four independent loads in flight
+                    float4 x[4];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        x[v] = *reinterpret_cast<const float4*>(po + (static_cast<size_t>(sid[j + v]) * hq + h) * D + c);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const float ww = w[(j + v) * hq + h];
+                        a.x += ww * x[v].x;
+                        a.y += ww * x[v].y;
+                        a.z += ww * x[v].z;
+                        a.w += ww * x[v].w;
+                    }
+                }
+                for (; j < n; ++j) {
+                    const float4 x = *reinterpret_cast<const float4*>(po + (static_cast<size_t>(sid[j]) * hq + h) * D + c);
+                    const float ww = w[j * hq + h];
+                    a.x += ww * x.x;
+                    a.y += ww * x.y;
+                    a.z += ww * x.z;
+                    a.w += ww * x.w;
+                }
+                acc[u] = a;
             }
         }
-        o[(static_cast<size_t>(m.qtok) * hq + h) * D + c] = static_cast<uint16_t>(bf16_rne(ws > 0.f ? acc / ws : 0.f));
-        if (lse && c == 0) lse[static_cast<size_t>(m.qtok) * hq + h] = ws > 0.f ? mx + logf(ws) : -INFINITY;
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int idx = tid + u * kThreads;
+            if (idx >= hn * C4) continue;
+            const int h = h0 + idx / C4, c = (idx % C4) * 4;
+            uint2 out;
+            out.x = pack_bf16x2(acc[u].x, acc[u].y);
+            out.y = pack_bf16x2(acc[u].z, acc[u].w);
+            *reinterpret_cast<uint2*>(o + (static_cast<size_t>(m.qtok) * hq + h) * D + c) = out;
+            acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
 }
 
@@ -257,11 +489,10 @@ template <int D>
 static int launch_d(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
                     hipStream_t st) {
     uint8_t* ws = static_cast<uint8_t*>(p->d_ws);
-    const auto* items = reinterpret_cast<const ItemDesc*>(ws + p->off_items);
-    const auto* toks = reinterpret_cast<const TokDesc*>(ws + p->off_toks);
-    const auto* blks = reinterpret_cast<const BlkDesc*>(ws + p->off_blks);
     const auto* merges = reinterpret_cast<const MergeDesc*>(ws + p->off_merges);
     const auto* mslots = reinterpret_cast<const int32_t*>(ws + p->off_mslots);
+    const auto* wg_off = reinterpret_cast<const int32_t*>(ws + p->off_wg);
+    const auto* stages = reinterpret_cast<const StageDesc*>(ws + p->off_stages);
     float* po = reinterpret_cast<float*>(ws + p->off_po);
     float* plse = reinterpret_cast<float*>(ws + p->off_plse);
     const float sl2 = 1.4426950408889634f / std::sqrt(static_cast<float>(D));
@@ -269,22 +500,23 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     hipEvent_t* ev = nullptr;
     if (p->prof_n < p->prof_max) {
         ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 3 * p->prof_n++;
-        hipEventRecord(ev[0], st);
+        (void)hipEventRecord(ev[0], st);
     }
-    hipLaunchKernelGGL(attn_items<D>, dim3(static_cast<unsigned>(p->items.size())), dim3(kThreads), 0, st, items,
-                       toks, blks, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+    hipLaunchKernelGGL(attn_persist<D>, dim3(static_cast<unsigned>(p->wg_off.size() - 1)), dim3(kThreads), 0, st,
+                       stages, wg_off, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                        static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
                        p->group, sl2);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
-    if (ev) hipEventRecord(ev[1], st);
+    if (ev) (void)hipEventRecord(ev[1], st);
     if (!p->merges.empty()) {
-        hipLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(kThreads), 0, st,
+        hipLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(kThreads),
+                           (kMergeChunk + 2) * hq * sizeof(float), st,
                            merges, mslots, po, plse, static_cast<uint16_t*>(o), lse, hq);
         e = hipGetLastError();
         if (e != hipSuccess) return set_error(TKV_EHIP, "merge launch: %s", hipGetErrorString(e));
     }
-    if (ev) hipEventRecord(ev[2], st);
+    if (ev) (void)hipEventRecord(ev[2], st);
     return TKV_OK;
 }
 
@@ -300,7 +532,7 @@ int launch_attention(const tkv_plan* p, const void* q, const void* k, const void
 }  // namespace tkv
 
 static void free_events(const tkv_plan* p) {
-    for (void* e : p->prof_events) hipEventDestroy(static_cast<hipEvent_t>(e));
+    for (void* e : p->prof_events) (void)hipEventDestroy(static_cast<hipEvent_t>(e));
     p->prof_events.clear();
     p->prof_max = p->prof_n = 0;
 }

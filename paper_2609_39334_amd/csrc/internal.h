@@ -18,6 +18,12 @@ int set_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3
 void clear_error();
 
 // ------------------------------------------------------------------ device descriptors
+constexpr int kBlock = 16;     // tokens per KV block
+constexpr int kTileRows = 64;  // query rows (token x head) per work item
+constexpr int kPersistentWGs = 768;  // resident workgroups of the attention kernel (3 per CU on 256 CUs)
+constexpr int kItemShared = 0;
+constexpr int kItemRow = 1;
+
 // One work item = one workgroup: a tile of query tokens (each with all G query heads of one KV
 // head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the
 // keys at positions <= its `limit`; keys are numbered along the path starting at `pos0`.
@@ -44,17 +50,31 @@ struct BlkDesc {
     int32_t len;  // tokens in the block (1..16)
 };
 
+// One 64-key stage of a persistent workgroup's stream.  The planner lays out each workgroup's
+// stages contiguously; the kernel loads a stage's descriptor one step before it fetches the
+// stage's K/V, so every address it needs (blocks and the query rows of the tile) is at hand
+// without a dependent load.  Lane l of a wave reads 16 bytes: blocks[l] (l < 4) or the item
+// fields (l == 4) into the header registers, and toks[row token] into its row registers.
+struct StageBlock {
+    int32_t blk;  // pool block id (block 0 of the stage where the stage has fewer blocks)
+    int32_t len;  // tokens in the block (0 = absent)
+    int32_t pos;  // path position of the block's first key
+    int32_t pad;
+};
+struct StageDesc {
+    StageBlock blocks[4];
+    int32_t kvh, n_tok, flags, pad;  // the item's KV head, tile size, kStageFirst | kStageLast
+    TokDesc toks[kTileRows];         // the item's tile tokens (n_tok used)
+};
+constexpr int kStageFirst = 1;
+constexpr int kStageLast = 2;
+
 struct MergeDesc {
     int32_t qtok;
     int32_t slot_off;  // first entry in the merge slot list
     int32_t n_slots;
     int32_t pad;
 };
-
-constexpr int kBlock = 16;     // tokens per KV block
-constexpr int kTileRows = 64;  // query rows (token x head) per work item
-constexpr int kItemShared = 0;
-constexpr int kItemRow = 1;
 
 }  // namespace tkv
 
@@ -68,9 +88,11 @@ struct tkv_plan {
     std::vector<tkv::BlkDesc> blks;
     std::vector<tkv::MergeDesc> merges;
     std::vector<int32_t> merge_slots;
+    std::vector<int32_t> wg_off;              // [n_wg + 1] each persistent workgroup's range in stages
+    std::vector<tkv::StageDesc> stages;       // per workgroup, in processing order
     int32_t n_slots = 0;
     // workspace layout (byte offsets)
-    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0;
+    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wg = 0, off_stages = 0, off_zero = 0;
     size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;
     std::vector<uint8_t> image;  // host copy of the descriptor region
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)

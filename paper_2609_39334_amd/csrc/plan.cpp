@@ -21,8 +21,10 @@
 // Sec. 3.2.2; decode is L = 1).  A shared segment sits at the same positions in every row through
 // it, so one per-token limit suffices.
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <numeric>
+#include <queue>
 #include <unordered_map>
 #include <vector>
 
@@ -79,6 +81,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         return set_error(TKV_EINVAL, "tkv_plan_create: hq (%d) must be a positive multiple of hkv (%d)", s.hq, s.hkv);
     const int32_t G = s.hq / s.hkv;
     if (G > tkv::kTileRows) return set_error(TKV_EINVAL, "tkv_plan_create: hq/hkv = %d exceeds %d", G, tkv::kTileRows);
+    if (s.hq > 256) return set_error(TKV_EINVAL, "tkv_plan_create: hq = %d exceeds 256", s.hq);
     if (s.num_blocks < 1) return set_error(TKV_EINVAL, "tkv_plan_create: num_blocks must be >= 1");
     if (n_rows < 0) return set_error(TKV_EINVAL, "tkv_plan_create: n_rows < 0");
     if (n_rows > 0 && (!q_indptr || !kv_indptr || !block_len))
@@ -257,9 +260,56 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         st.n_slots = p->n_slots;
         st.n_merge = static_cast<int32_t>(p->merges.size());
 
-        // Longest items first, so the tail of the launch is made of short ones.
+        // Longest items first, then longest-processing-time assignment to the persistent
+        // workgroups: each item goes to the least-loaded workgroup (cost = key blocks + a fixed
+        // per-item overhead), so every workgroup streams about the same number of bytes.
         std::stable_sort(p->items.begin(), p->items.end(),
                          [](const ItemDesc& a, const ItemDesc& b) { return a.n_blk > b.n_blk; });
+        {
+            const int32_t n_items = static_cast<int32_t>(p->items.size());
+            int32_t target = tkv::kPersistentWGs;
+            if (const char* env = std::getenv("TKV_PERSISTENT_WGS")) target = std::max(1, std::atoi(env));
+            const int32_t n_wg = std::min<int32_t>(target, n_items);
+            std::vector<std::vector<int32_t>> lists(n_wg);
+            using Load = std::pair<int64_t, int32_t>;
+            std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
+            for (int32_t w = 0; w < n_wg; ++w) heap.push({0, w});
+            for (int32_t i = 0; i < n_items; ++i) {
+                Load l = heap.top();
+                heap.pop();
+                lists[l.second].push_back(i);
+                l.first += p->items[i].n_blk + 2;
+                heap.push(l);
+            }
+            p->wg_off.assign(1, 0);
+            for (int32_t w = 0; w < n_wg; ++w) {
+                for (int32_t i : lists[w]) {
+                    const ItemDesc& it = p->items[i];
+                    int32_t pos = it.pos0;
+                    for (int32_t b0 = 0; b0 < it.n_blk; b0 += 4) {
+                        tkv::StageDesc sd{};
+                        for (int32_t j = 0; j < 4; ++j) {
+                            sd.blocks[j].pos = pos;
+                            if (b0 + j < it.n_blk) {
+                                const BlkDesc& bd = p->blks[it.blk_off + b0 + j];
+                                sd.blocks[j].blk = bd.blk;
+                                sd.blocks[j].len = bd.len;
+                                pos += bd.len;
+                            } else {
+                                sd.blocks[j].blk = sd.blocks[0].blk;  // read in place of the missing block, then masked
+                                sd.blocks[j].len = 0;
+                            }
+                        }
+                        sd.kvh = it.kvh;
+                        sd.n_tok = it.n_tok;
+                        sd.flags = (b0 == 0 ? tkv::kStageFirst : 0) | (b0 + 4 >= it.n_blk ? tkv::kStageLast : 0);
+                        for (int32_t t = 0; t < it.n_tok; ++t) sd.toks[t] = p->toks[it.tok_off + t];
+                        p->stages.push_back(sd);
+                    }
+                }
+                p->wg_off.push_back(static_cast<int32_t>(p->stages.size()));
+            }
+        }
 
         // ------------------------------------------------------------ workspace layout
         auto bytes = [](size_t n, size_t e) { return n * e; };
@@ -274,6 +324,12 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         off = align256(off + bytes(p->merges.size(), sizeof(MergeDesc)));
         p->off_mslots = off;
         off = align256(off + bytes(p->merge_slots.size(), sizeof(int32_t)));
+        p->off_wg = off;
+        off = align256(off + bytes(p->wg_off.size(), sizeof(int32_t)));
+        p->off_stages = off;
+        off = align256(off + bytes(p->stages.size(), sizeof(tkv::StageDesc)));
+        p->off_zero = off;  // one row of zero bf16 values, read in place of missing keys
+        off = align256(off + 512);
         p->desc_bytes = off;
         p->off_po = off;
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq * s.d, sizeof(float)));
@@ -289,6 +345,8 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         put(p->off_blks, p->blks.data(), bytes(p->blks.size(), sizeof(BlkDesc)));
         put(p->off_merges, p->merges.data(), bytes(p->merges.size(), sizeof(MergeDesc)));
         put(p->off_mslots, p->merge_slots.data(), bytes(p->merge_slots.size(), sizeof(int32_t)));
+        put(p->off_wg, p->wg_off.data(), bytes(p->wg_off.size(), sizeof(int32_t)));
+        put(p->off_stages, p->stages.data(), bytes(p->stages.size(), sizeof(tkv::StageDesc)));
     } catch (...) {
         delete p;
         return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
