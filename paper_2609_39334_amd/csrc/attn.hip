@@ -359,6 +359,252 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 3))
     }
 }
 
+// ============================================================================ wave-private kernel
+// For tiles of at most 16 query rows (decode rows: the G heads of a few tokens) every wave is an
+// independent worker with its own item: no LDS sharing, no barriers; latency is covered by the
+// dozen independent waves resident per CU.  Per 16-key block:
+//   S^T = K Q^T   on v_mfma_f32_16x16x32_bf16: K comes from HBM straight into the A operand
+//                 (lane = key, 16 contiguous bytes of its row per k-step), Q^T held in registers;
+//   online softmax on the four scores per lane (row max over the 4 lanes of a row by
+//                 v_permlane16/32_swap);
+//   O^T += V^T P^T on v_mfma_f32_16x16x16_bf16: P^T is the S^T result as it sits in the lanes;
+//                 V is written row-major to the wave's LDS and read back transposed with
+//                 ds_read_b64_tr_b16 (lane j of a 16-lane group addresses row 4kg + j/4, column
+//                 16ct + 4(j%4); lane i receives V[4kg + e][16ct + i], e = 0..3).
+// The next two blocks' K/V loads are in flight while a block is contracted.
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float rowmax4(float x) {  // max over lanes l, l^16, l^32, l^48
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(x, fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1])));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(x, fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1])));
+}
+
+template <int D>
+struct BlockRegs {
+    u32x4_t k[D / 32];  // K[key = lane%16][32ks + 8kg .. +7]
+    u32x4_t v[D / 32];  // V chunks c = lane + 64i: key c / (D/8), dims 8(c % (D/8)) .. +7
+};
+
+// len = 0 (a block past the item's end) reads row 0 of the block: the fetch is harmless.
+template <int D>
+__device__ __forceinline__ void load_k(BlockRegs<D>& r, const uint16_t* __restrict__ kpool, size_t boff, int len,
+                                       int lane) {
+    const int kse = min(lane & 15, max(len - 1, 0));
+    const uint16_t* krow = kpool + boff + kse * D + (lane >> 4) * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) r.k[ks] = *reinterpret_cast<const u32x4_t*>(krow + ks * 32);
+}
+template <int D>
+__device__ __forceinline__ void load_v(BlockRegs<D>& r, const uint16_t* __restrict__ vpool, size_t boff, int len,
+                                       int lane) {
+    const int last = max(len - 1, 0);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+        const int c = lane + 64 * i;
+        r.v[i] = *reinterpret_cast<const u32x4_t*>(vpool + boff + min(c / (D / 8), last) * D + (c % (D / 8)) * 8);
+    }
+}
+
+// Item-level fields of a wave descriptor (see tkv::WaveDesc): uniform values by v_readlane, the
+// lane's own tile token by ds_bpermute from the token lanes.
+struct WaveItem {
+    int kvh, n_tok, nb;
+    int qtok, limit, slot, h;
+    bool row_ok;
+};
+
+__device__ __forceinline__ WaveItem wave_item(int2 d, int t, int g, int G) {
+    WaveItem w;
+    w.kvh = __builtin_amdgcn_readlane(d.x, 48);
+    w.n_tok = __builtin_amdgcn_readlane(d.y, 48);
+    w.nb = __builtin_amdgcn_readlane(d.x, 49);
+    w.qtok = __builtin_amdgcn_ds_bpermute((16 + t) * 4, d.x);
+    w.limit = __builtin_amdgcn_ds_bpermute((16 + t) * 4, d.y);
+    w.slot = __builtin_amdgcn_ds_bpermute((32 + t) * 4, d.x);
+    w.row_ok = t < w.n_tok;
+    w.h = w.kvh * G + g;
+    return w;
+}
+
+template <int D>
+__device__ __forceinline__ void load_q(bf16x8_t (&qf)[D / 32], const uint16_t* __restrict__ q, const WaveItem& w,
+                                       int hq, int kg) {
+    const uint16_t* qrow = q + (static_cast<size_t>(w.qtok) * hq + w.h) * D + kg * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
+}
+
+// Running softmax state and output accumulator of a wave's 16 query rows (O^T: lane holds
+// columns 16ct + 4kg + r of row lane%16).
+template <int D>
+struct WaveAcc {
+    f32x4_t acc[D / 16];
+    float m, l;
+    __device__ __forceinline__ void reset() {
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        m = -INFINITY;
+        l = 0.f;
+    }
+};
+
+// One 16-key block against the wave's 16 query rows; the block's registers are refilled with the
+// block two ahead in the wave's stream as soon as each half (K, then V) has been consumed.
+template <int D, int VROW>
+__device__ __forceinline__ void wave_block(WaveAcc<D>& A, BlockRegs<D>& r, const bf16x8_t (&qf)[D / 32], int len,
+                                           int pos, int limit, const uint16_t* __restrict__ kpool,
+                                           const uint16_t* __restrict__ vpool, size_t boff_n, int len_n,
+                                           uint8_t* vs, const uint8_t* vrd, int lane, int kg, float sl2) {
+    // S^T = K Q^T, then the K registers take the next loads
+    f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) s = mfma_16x16x32(__builtin_bit_cast(bf16x8_t, r.k[ks]), qf[ks], s);
+    load_k<D>(r, kpool, boff_n, len_n, lane);
+    // lane holds keys 4kg + e of row lane%16; mask only partial blocks and rows with a causal limit inside
+    if (__builtin_amdgcn_ballot_w64(!(len == 16 && limit >= pos + 15)) != 0) {
+        const int vlen = min(len, limit - pos + 1);
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+            if (4 * kg + x >= vlen) s[x] = -INFINITY;
+    }
+    const float mx = rowmax4(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
+    const float m_new = fmaxf(A.m, mx);
+    const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
+    float psum = 0.f;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        s[x] = __builtin_amdgcn_exp2f(fmaf(s[x], sl2, -msc));
+        psum += s[x];
+    }
+    const float alpha = m_new == A.m ? 1.f : __builtin_amdgcn_exp2f(A.m * sl2 - msc);
+    A.l = fmaf(A.l, alpha, psum);
+    A.m = m_new;
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c) A.acc[c] *= alpha;
+    }
+    // V rows into this wave's LDS region, then the V registers take the next loads
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+        const int c = lane + 64 * i;
+        *reinterpret_cast<u32x4_t*>(vs + (c / (D / 8)) * VROW + (c % (D / 8)) * 16) = r.v[i];
+    }
+    load_v<D>(r, vpool, boff_n, len_n, lane);
+    // O^T += V^T P^T: P^T as the S^T result sits in the lanes, V^T by transposing LDS reads
+    const s16x4_t pb = __builtin_bit_cast(s16x4_t, uint2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])});
+#pragma unroll
+    for (int ct = 0; ct < D / 16; ++ct) {
+        const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vrd + ct * 32)));
+        A.acc[ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb, A.acc[ct], 0, 0, 0);
+    }
+}
+
+// Each wave walks its own list of items (a contiguous range of the descriptor stream) with no
+// barrier.  Key blocks go in pairs through two register sets, so the two blocks after the one
+// being contracted are always in flight, across item boundaries too (every item has an even
+// number of blocks); the descriptor two items ahead and the query rows of the next item are
+// fetched at the start of an item.
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_wave(
+    const int2* __restrict__ wdesc, const int32_t* __restrict__ woff, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
+    float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
+    constexpr int VROW = 2 * D + 32;  // LDS bytes per V row: the padding spreads 4 rows over 32 banks
+    __shared__ __attribute__((aligned(16))) uint8_t Vs[4][16 * VROW];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int w = blockIdx.x * 4 + wave;
+    const int e0 = woff[w], e1 = woff[w + 1];
+    if (e0 >= e1) return;  // waves are independent: no barrier follows
+    const int col = lane & 15, kg = lane >> 4;
+    const int t = col / G, g = col - t * G;
+    const size_t blk_stride = static_cast<size_t>(hkv) * (16 * D);
+    uint8_t* vs = Vs[wave];
+    const int j = lane & 15;
+    const uint8_t* vrd = vs + (4 * kg + (j >> 2)) * VROW + (4 * (j & 3)) * 2;
+
+    int2 dc = wdesc[static_cast<size_t>(e0) * 64 + lane];
+    int2 dn = wdesc[static_cast<size_t>(min(e0 + 1, e1 - 1)) * 64 + lane];
+    WaveItem ic = wave_item(dc, t, g, G);
+    bf16x8_t qf[D / 32];
+    load_q<D>(qf, q, ic, hq, kg);
+    BlockRegs<D> ra, rb;  // blocks 2i and 2i+1 of the stream
+    {
+        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
+        const int len0 = __builtin_amdgcn_readlane(dc.y, 0), len1 = __builtin_amdgcn_readlane(dc.y, 1);
+        const size_t b0 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 0)) * blk_stride + kvh_off;
+        const size_t b1 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 1)) * blk_stride + kvh_off;
+        load_k<D>(ra, kpool, b0, len0, lane);
+        load_v<D>(ra, vpool, b0, len0, lane);
+        load_k<D>(rb, kpool, b1, len1, lane);
+        load_v<D>(rb, vpool, b1, len1, lane);
+    }
+    WaveAcc<D> A;
+    for (int e = e0;; ++e) {
+        const bool more = e + 1 < e1;
+        // next item's query rows, and the descriptor of the item after it
+        const WaveItem in = wave_item(dn, t, g, G);
+        bf16x8_t qn[D / 32];
+        load_q<D>(qn, q, in, hq, kg);
+        const int2 dnn = wdesc[static_cast<size_t>(min(e + 2, e1 - 1)) * 64 + lane];
+        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
+        const size_t kvh_off_n = static_cast<size_t>(in.kvh) * (16 * D);
+        A.reset();
+        const int nb = ic.nb;  // even
+        for (int b = 0; b < nb; b += 2) {
+            // blocks b + 2 and b + 3 of this item, or blocks 0 and 1 of the next
+            // (a lane-wise select of the descriptor, then v_readlane: no branches)
+            const bool cross = b + 2 >= nb;
+            const int bn = cross ? 0 : b + 2;
+            const int src_x = cross ? dn.x : dc.x;
+            const int src_y = cross ? (more ? dn.y : 0) : dc.y;
+            const int blk_a = __builtin_amdgcn_readlane(src_x, bn), blk_b = __builtin_amdgcn_readlane(src_x, bn + 1);
+            const int len_a = __builtin_amdgcn_readlane(src_y, bn), len_b = __builtin_amdgcn_readlane(src_y, bn + 1);
+            const size_t off_n = cross ? kvh_off_n : kvh_off;
+            wave_block<D, VROW>(A, ra, qf, __builtin_amdgcn_readlane(dc.y, b), __builtin_amdgcn_readlane(dc.y, 32 + b),
+                                ic.limit, kpool, vpool, static_cast<size_t>(blk_a) * blk_stride + off_n, len_a, vs,
+                                vrd, lane, kg, sl2);
+            wave_block<D, VROW>(A, rb, qf, __builtin_amdgcn_readlane(dc.y, b + 1),
+                                __builtin_amdgcn_readlane(dc.y, 33 + b), ic.limit, kpool, vpool,
+                                static_cast<size_t>(blk_b) * blk_stride + off_n, len_b, vs, vrd, lane, kg, sl2);
+        }
+        // normalise and write the final output or the partial
+        float l_tot = A.l + __shfl_xor(A.l, 16);
+        l_tot += __shfl_xor(l_tot, 32);
+        if (ic.row_ok) {
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            const float lse_v = l_tot > 0.f ? (A.m * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
+            if (ic.slot < 0) {
+                uint16_t* orow = o + (static_cast<size_t>(ic.qtok) * hq + ic.h) * D;
+#pragma unroll
+                for (int ct = 0; ct < D / 16; ++ct) {
+                    uint2 wv;
+                    wv.x = pack_bf16x2(A.acc[ct][0] * inv, A.acc[ct][1] * inv);
+                    wv.y = pack_bf16x2(A.acc[ct][2] * inv, A.acc[ct][3] * inv);
+                    *reinterpret_cast<uint2*>(orow + ct * 16 + kg * 4) = wv;
+                }
+                if (lse && kg == 0) lse[static_cast<size_t>(ic.qtok) * hq + ic.h] = lse_v;
+            } else {
+                float* prow = po + (static_cast<size_t>(ic.slot) * hq + ic.h) * D;
+#pragma unroll
+                for (int ct = 0; ct < D / 16; ++ct)
+                    *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) = make_float4(
+                        A.acc[ct][0] * inv, A.acc[ct][1] * inv, A.acc[ct][2] * inv, A.acc[ct][3] * inv);
+                if (kg == 0) plse[static_cast<size_t>(ic.slot) * hq + ic.h] = lse_v;
+            }
+        }
+        if (!more) break;
+        ic = in;
+        dc = dn;
+        dn = dnn;
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) qf[ks] = qn[ks];
+    }
+}
+
 // Log-sum-exp merge of one query token's partials (one workgroup per token).  Slot ids, then all
 // partial lse values, then all partial outputs are each fetched in one parallel round, so the
 // token costs three memory latencies however many partials it has (up to kMergeChunk at a time).
@@ -493,6 +739,10 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     const auto* mslots = reinterpret_cast<const int32_t*>(ws + p->off_mslots);
     const auto* wg_off = reinterpret_cast<const int32_t*>(ws + p->off_wg);
     const auto* stages = reinterpret_cast<const StageDesc*>(ws + p->off_stages);
+    const auto* wdesc = reinterpret_cast<const int2*>(ws + p->off_wdesc);
+    const auto* woff = reinterpret_cast<const int32_t*>(ws + p->off_woff);
+    const auto* toks = reinterpret_cast<const TokDesc*>(ws + p->off_toks);
+    const auto* blks = reinterpret_cast<const BlkDesc*>(ws + p->off_blks);
     float* po = reinterpret_cast<float*>(ws + p->off_po);
     float* plse = reinterpret_cast<float*>(ws + p->off_plse);
     const float sl2 = 1.4426950408889634f / std::sqrt(static_cast<float>(D));
@@ -502,11 +752,21 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
         ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 3 * p->prof_n++;
         (void)hipEventRecord(ev[0], st);
     }
-    hipLaunchKernelGGL(attn_persist<D>, dim3(static_cast<unsigned>(p->wg_off.size() - 1)), dim3(kThreads), 0, st,
-                       stages, wg_off, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                       static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
-                       p->group, sl2);
+    const int n_wg = static_cast<int>(p->wg_off.size()) - 1;
+    if (n_wg > 0)
+        hipLaunchKernelGGL(attn_persist<D>, dim3(static_cast<unsigned>(n_wg)), dim3(kThreads), 0, st, stages, wg_off,
+                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                           static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
+                           p->group, sl2);
     hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
+    const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of 4
+    if (n_wave > 0)
+        hipLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / 4)), dim3(kThreads), 0, st,
+                           wdesc, woff, static_cast<const uint16_t*>(q),
+                           static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                           static_cast<uint16_t*>(o), lse, po, plse, hq, hkv, p->group, sl2);
+    e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
     if (ev) (void)hipEventRecord(ev[1], st);
     if (!p->merges.empty()) {
@@ -523,7 +783,7 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
 int launch_attention(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
                      void* stream) {
     if (!p->d_ws) return set_error(TKV_EINVAL, "attention: plan has not been uploaded");
-    if (p->items.empty()) return TKV_OK;
+    if (p->items.empty() && p->wave_items.empty()) return TKV_OK;
     if (!q || !k || !v || !o) return set_error(TKV_EINVAL, "attention: NULL tensor pointer");
     const hipStream_t st = static_cast<hipStream_t>(stream);
     return p->shape.d == 128 ? launch_d<128>(p, q, k, v, o, lse, st) : launch_d<64>(p, q, k, v, o, lse, st);

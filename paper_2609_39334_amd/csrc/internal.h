@@ -21,8 +21,12 @@ void clear_error();
 constexpr int kBlock = 16;     // tokens per KV block
 constexpr int kTileRows = 64;  // query rows (token x head) per work item
 constexpr int kPersistentWGs = 768;  // resident workgroups of the attention kernel (3 per CU on 256 CUs)
-constexpr int kItemShared = 0;
-constexpr int kItemRow = 1;
+constexpr int kItemShared = 0;  // tile of several rows' tokens over one segment chunk (workgroup kernel)
+constexpr int kItemRow = 1;     // tile of one row's tokens over its whole path (workgroup kernel)
+constexpr int kItemWave = 2;    // tile of <= kWaveRows rows over one segment chunk (wave kernel)
+constexpr int kWaveRows = 16;   // query rows of a wave-kernel tile
+constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
+constexpr int kWaveWorkers = 2048;  // waves of the wave kernel (each streams a list of items)
 
 // One work item = one workgroup: a tile of query tokens (each with all G query heads of one KV
 // head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the
@@ -69,6 +73,16 @@ struct StageDesc {
 constexpr int kStageFirst = 1;
 constexpr int kStageLast = 2;
 
+// A wave-kernel item as one 512-byte record that a wave loads with one 8-byte load per lane
+// (lane l gets e[l]); block fields come out with v_readlane, token fields with ds_bpermute.
+//   e[j]      (j < 16): {pool block id, length} of key block j (block 0's id, length 0 past n_blk)
+//   e[16 + t] (t < 16): {query token, causal limit} of tile token t (token 0's past n_tok)
+//   e[32 + j]:          {partial slot of tile token j (-1: final output), path position of block j}
+//   e[48]:              {KV head, tile tokens}     e[49]: {key blocks rounded up to even, 0}
+struct WaveDesc {
+    int32_t e[128];
+};
+
 struct MergeDesc {
     int32_t qtok;
     int32_t slot_off;  // first entry in the merge slot list
@@ -83,16 +97,20 @@ struct tkv_plan {
     tkv_shape shape{};
     int32_t group = 1;
     bool all_decode = true;
-    std::vector<tkv::ItemDesc> items;
+    std::vector<tkv::ItemDesc> items;       // workgroup-kernel items
+    std::vector<tkv::ItemDesc> wave_items;  // wave-kernel items, longest first
+    std::vector<tkv::ItemDesc> view_items;  // items then wave_items (tkv_plan_get_view)
     std::vector<tkv::TokDesc> toks;
     std::vector<tkv::BlkDesc> blks;
     std::vector<tkv::MergeDesc> merges;
     std::vector<int32_t> merge_slots;
     std::vector<int32_t> wg_off;              // [n_wg + 1] each persistent workgroup's range in stages
     std::vector<tkv::StageDesc> stages;       // per workgroup, in processing order
+    std::vector<tkv::WaveDesc> wave_desc;     // wave-kernel items, each wave's list contiguous
+    std::vector<int32_t> wave_off;            // [n_waves + 1] each wave's range in wave_desc
     int32_t n_slots = 0;
     // workspace layout (byte offsets)
-    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wg = 0, off_stages = 0, off_zero = 0;
+    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wg = 0, off_stages = 0, off_wdesc = 0, off_woff = 0;
     size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;
     std::vector<uint8_t> image;  // host copy of the descriptor region
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)

@@ -23,6 +23,7 @@
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <numeric>
 #include <queue>
 #include <unordered_map>
@@ -39,6 +40,8 @@ using tkv::TokDesc;
 namespace {
 
 constexpr int kChunkBlocks = 16;  // longest key run of one shared item (256 tokens)
+static_assert(kChunkBlocks <= tkv::kWaveBlocks && kChunkBlocks % 2 == 0,
+              "a wave item holds its key blocks (an even number after padding) in one record");
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
@@ -223,15 +226,26 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                                           static_cast<int32_t>(slots_of[q].size()), 0});
             p->merge_slots.insert(p->merge_slots.end(), slots_of[q].begin(), slots_of[q].end());
         }
+        // Narrow chunks (at most kWaveRows query rows in all, G <= 16) go to the wave kernel, one
+        // wave per 16-row tile; wider chunks use the workgroup kernel's 64-row tiles, which share
+        // each staged K/V block among four waves.
+        int32_t wave_max_rows = tkv::kWaveRows;
+        if (const char* env = std::getenv("TKV_WAVE_MAX_ROWS")) wave_max_rows = std::atoi(env);
         for (const Chunk& c : chunks) {
-            tile_evenly(static_cast<int32_t>(c.toks.size()), tpt, [&](int32_t a, int32_t e) {
+            const int64_t rows = static_cast<int64_t>(c.toks.size()) * G;
+            const bool wave_tiles = G <= tkv::kWaveRows && rows <= wave_max_rows;
+            const int32_t per_tile = wave_tiles ? tkv::kWaveRows / G : tpt;
+            tile_evenly(static_cast<int32_t>(c.toks.size()), per_tile, [&](int32_t a, int32_t e) {
                 const int32_t tok_off = static_cast<int32_t>(p->toks.size());
                 p->toks.insert(p->toks.end(), c.toks.begin() + a, c.toks.begin() + e);
-                for (int32_t h = 0; h < s.hkv; ++h)
-                    p->items.push_back(ItemDesc{h, tok_off, e - a, c.blk_off, c.n_blk, c.pos0, tkv::kItemShared, 0});
+                for (int32_t h = 0; h < s.hkv; ++h) {
+                    const ItemDesc d{h, tok_off, e - a, c.blk_off, c.n_blk, c.pos0,
+                                     wave_tiles ? tkv::kItemWave : tkv::kItemShared, 0};
+                    (wave_tiles ? p->wave_items : p->items).push_back(d);
+                }
             });
         }
-        st.n_items_shared = static_cast<int32_t>(p->items.size());
+        st.n_items_shared = static_cast<int32_t>(p->items.size() + p->wave_items.size());
 
         // ------------------------------------------------------------ row items (large rows)
         for (int32_t r = 0; r < n_rows; ++r) {
@@ -255,8 +269,95 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                     p->items.push_back(ItemDesc{h, tok_off, e - a, row_blk_off, nbk, 0, tkv::kItemRow, 0});
             });
         }
-        st.n_items = static_cast<int32_t>(p->items.size());
+        st.n_items = static_cast<int32_t>(p->items.size() + p->wave_items.size());
         st.n_items_row = st.n_items - st.n_items_shared;
+        std::stable_sort(p->wave_items.begin(), p->wave_items.end(),
+                         [](const ItemDesc& a, const ItemDesc& b) { return a.n_blk > b.n_blk; });
+        // Wave streams.  Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+        // L2), so wave w runs on XCD (w / 4) % 8.  All tiles of one (chunk, KV head) -- which read
+        // the same K/V blocks -- go to one XCD, spread over its waves at the same depth of their
+        // lists, so the repeated reads of a shared chunk hit that XCD's L2.  Groups are assigned
+        // to XCDs and items to the XCD's waves by longest processing time first.
+        {
+            const int32_t n_items = static_cast<int32_t>(p->wave_items.size());
+            int32_t target = tkv::kWaveWorkers;
+            if (const char* env = std::getenv("TKV_WAVES")) target = std::max(4, std::atoi(env));
+            const int32_t n_w = n_items ? (std::min(target, n_items) + 3) / 4 * 4 : 0;
+            constexpr int32_t kXcds = 8;
+            std::vector<std::vector<int32_t>> xcd_waves(kXcds);
+            for (int32_t w = 0; w < n_w; ++w) xcd_waves[(w / 4) % kXcds].push_back(w);
+            // groups of items sharing key blocks: same chunk (first block entry) and KV head
+            std::map<std::pair<int32_t, int32_t>, int32_t> gid;
+            std::vector<std::vector<int32_t>> groups;
+            std::vector<int64_t> gcost;
+            for (int32_t i = 0; i < n_items; ++i) {
+                const ItemDesc& it = p->wave_items[i];
+                auto ins = gid.emplace(std::make_pair(it.blk_off, it.kvh), static_cast<int32_t>(groups.size()));
+                if (ins.second) {
+                    groups.emplace_back();
+                    gcost.push_back(0);
+                }
+                groups[ins.first->second].push_back(i);
+                gcost[ins.first->second] += it.n_blk + 1;
+            }
+            std::vector<int32_t> gorder(groups.size());
+            std::iota(gorder.begin(), gorder.end(), 0);
+            std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a, int32_t b) { return gcost[a] > gcost[b]; });
+            using Load = std::pair<int64_t, int32_t>;
+            std::priority_queue<Load, std::vector<Load>, std::greater<Load>> xheap;
+            for (int32_t x = 0; x < kXcds; ++x)
+                if (!xcd_waves[x].empty()) xheap.push({0, x});
+            std::vector<std::vector<int32_t>> xcd_items(kXcds);
+            for (int32_t g2 : gorder) {
+                Load l = xheap.top();
+                xheap.pop();
+                xcd_items[l.second].insert(xcd_items[l.second].end(), groups[g2].begin(), groups[g2].end());
+                // cost per wave of the XCD (the counts differ only for small grids)
+                l.first += gcost[g2] * 1024 / static_cast<int64_t>(xcd_waves[l.second].size());
+                xheap.push(l);
+            }
+            std::vector<std::vector<int32_t>> lists(n_w);
+            for (int32_t x = 0; x < kXcds; ++x) {
+                std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
+                for (int32_t w : xcd_waves[x]) heap.push({0, w});
+                for (int32_t i : xcd_items[x]) {
+                    Load l = heap.top();
+                    heap.pop();
+                    lists[l.second].push_back(i);
+                    l.first += p->wave_items[i].n_blk + 1;
+                    heap.push(l);
+                }
+            }
+            p->wave_off.assign(1, 0);
+            for (int32_t w = 0; w < n_w; ++w) {
+                for (int32_t i : lists[w]) {
+                    const ItemDesc& it = p->wave_items[i];
+                    tkv::WaveDesc wd{};
+                    int32_t pos = it.pos0;
+                    // the kernel walks blocks in pairs: an odd key list gets an empty (length 0) block
+                    const int32_t nb_even = (it.n_blk + 1) & ~1;
+                    for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
+                        const bool in = j < it.n_blk;
+                        const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
+                        wd.e[2 * j] = bd.blk;
+                        wd.e[2 * j + 1] = in ? bd.len : 0;
+                        wd.e[2 * (32 + j) + 1] = pos;
+                        if (in) pos += bd.len;
+                    }
+                    for (int32_t t = 0; t < tkv::kWaveRows; ++t) {
+                        const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
+                        wd.e[2 * (16 + t)] = td.qtok;
+                        wd.e[2 * (16 + t) + 1] = td.limit;
+                        wd.e[2 * (32 + t)] = td.slot;
+                    }
+                    wd.e[96] = it.kvh;
+                    wd.e[97] = it.n_tok;
+                    wd.e[98] = nb_even;
+                    p->wave_desc.push_back(wd);
+                }
+                p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
+            }
+        }
         st.n_slots = p->n_slots;
         st.n_merge = static_cast<int32_t>(p->merges.size());
 
@@ -328,8 +429,10 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         off = align256(off + bytes(p->wg_off.size(), sizeof(int32_t)));
         p->off_stages = off;
         off = align256(off + bytes(p->stages.size(), sizeof(tkv::StageDesc)));
-        p->off_zero = off;  // one row of zero bf16 values, read in place of missing keys
-        off = align256(off + 512);
+        p->off_wdesc = off;
+        off = align256(off + bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
+        p->off_woff = off;
+        off = align256(off + bytes(p->wave_off.size(), sizeof(int32_t)));
         p->desc_bytes = off;
         p->off_po = off;
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq * s.d, sizeof(float)));
@@ -347,6 +450,8 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         put(p->off_mslots, p->merge_slots.data(), bytes(p->merge_slots.size(), sizeof(int32_t)));
         put(p->off_wg, p->wg_off.data(), bytes(p->wg_off.size(), sizeof(int32_t)));
         put(p->off_stages, p->stages.data(), bytes(p->stages.size(), sizeof(tkv::StageDesc)));
+        put(p->off_wdesc, p->wave_desc.data(), bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
+        put(p->off_woff, p->wave_off.data(), bytes(p->wave_off.size(), sizeof(int32_t)));
     } catch (...) {
         delete p;
         return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
@@ -366,15 +471,18 @@ TKV_EXPORT int tkv_plan_get_stats(const tkv_plan* p, tkv_plan_stats* out) {
     return TKV_OK;
 }
 
-TKV_EXPORT int tkv_plan_get_view(const tkv_plan* p, tkv_plan_view* out) {
+TKV_EXPORT int tkv_plan_get_view(const tkv_plan* cp, tkv_plan_view* out) {
+    tkv_plan* p = const_cast<tkv_plan*>(cp);
     tkv::clear_error();
     if (!p || !out) return set_error(TKV_EINVAL, "tkv_plan_get_view: NULL argument");
-    out->items = reinterpret_cast<const int32_t*>(p->items.data());
+    p->view_items.assign(p->items.begin(), p->items.end());
+    p->view_items.insert(p->view_items.end(), p->wave_items.begin(), p->wave_items.end());
+    out->items = reinterpret_cast<const int32_t*>(p->view_items.data());
     out->toks = reinterpret_cast<const int32_t*>(p->toks.data());
     out->blks = reinterpret_cast<const int32_t*>(p->blks.data());
     out->merges = reinterpret_cast<const int32_t*>(p->merges.data());
     out->merge_slots = p->merge_slots.data();
-    out->n_items = static_cast<int32_t>(p->items.size());
+    out->n_items = static_cast<int32_t>(p->view_items.size());
     out->n_toks = static_cast<int32_t>(p->toks.size());
     out->n_blks = static_cast<int32_t>(p->blks.size());
     out->n_merge = static_cast<int32_t>(p->merges.size());
