@@ -407,83 +407,105 @@ __device__ __forceinline__ void load_v(BlockRegs<D>& r, const uint16_t* __restri
     }
 }
 
-// Item-level fields of a wave descriptor (see tkv::WaveDesc): uniform values by v_readlane, the
-// lane's own tile token by ds_bpermute from the token lanes.
-struct WaveItem {
-    int kvh, n_tok, nb;
-    int qtok, limit, slot, h;
-    bool row_ok;
+// Running softmax state and output accumulators of a wave's T column tiles of 16 query rows
+// (O^T: lane holds columns 16ct + 4kg + r of row lane%16 of each tile).
+template <int D, int T>
+struct WaveAcc {
+    f32x4_t acc[T][D / 16];
+    float m[T], l[T];
+    __device__ __forceinline__ void reset() {
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt) {
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) acc[tt][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            m[tt] = -INFINITY;
+            l[tt] = 0.f;
+        }
+    }
 };
 
-__device__ __forceinline__ WaveItem wave_item(int2 d, int t, int g, int G) {
-    WaveItem w;
-    w.kvh = __builtin_amdgcn_readlane(d.x, 48);
-    w.n_tok = __builtin_amdgcn_readlane(d.y, 48);
-    w.nb = __builtin_amdgcn_readlane(d.x, 49);
-    w.qtok = __builtin_amdgcn_ds_bpermute((16 + t) * 4, d.x);
-    w.limit = __builtin_amdgcn_ds_bpermute((16 + t) * 4, d.y);
-    w.slot = __builtin_amdgcn_ds_bpermute((32 + t) * 4, d.x);
-    w.row_ok = t < w.n_tok;
-    w.h = w.kvh * G + g;
+// The item fields a wave needs, decoded from its descriptor (see tkv::WaveDesc): uniform values
+// by v_readlane, this lane's token of each tile by ds_bpermute from the token lanes.
+template <int T>
+struct WaveItem {
+    int kvh, n_tok, nb;
+    int qtok[T], limit[T], slot[T], h[T];
+    bool ok[T];
+};
+
+template <int T>
+__device__ __forceinline__ WaveItem<T> wave_item(int4 d, const int (&tok)[T], const int (&grp)[T], int G) {
+    WaveItem<T> w;
+    w.kvh = __builtin_amdgcn_readlane(d.w, 0);
+    w.n_tok = __builtin_amdgcn_readlane(d.w, 1);
+    w.nb = __builtin_amdgcn_readlane(d.w, 2);
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        const int src = (16 + tok[tt]) * 4;
+        w.qtok[tt] = __builtin_amdgcn_ds_bpermute(src, d.x);
+        w.limit[tt] = __builtin_amdgcn_ds_bpermute(src, d.y);
+        w.slot[tt] = __builtin_amdgcn_ds_bpermute(src, d.z);
+        w.ok[tt] = tok[tt] < w.n_tok;
+        w.h[tt] = w.kvh * G + grp[tt];
+    }
     return w;
 }
 
-template <int D>
-__device__ __forceinline__ void load_q(bf16x8_t (&qf)[D / 32], const uint16_t* __restrict__ q, const WaveItem& w,
-                                       int hq, int kg) {
-    const uint16_t* qrow = q + (static_cast<size_t>(w.qtok) * hq + w.h) * D + kg * 8;
+template <int D, int T>
+__device__ __forceinline__ void load_q(bf16x8_t (&qf)[T][D / 32], const uint16_t* __restrict__ q,
+                                       const WaveItem<T>& w, int hq, int kg) {
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
+    for (int tt = 0; tt < T; ++tt) {
+        const uint16_t* qrow = q + (static_cast<size_t>(w.qtok[tt]) * hq + w.h[tt]) * D + kg * 8;
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) qf[tt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
+    }
 }
 
-// Running softmax state and output accumulator of a wave's 16 query rows (O^T: lane holds
-// columns 16ct + 4kg + r of row lane%16).
-template <int D>
-struct WaveAcc {
-    f32x4_t acc[D / 16];
-    float m, l;
-    __device__ __forceinline__ void reset() {
+// One 16-key block against the wave's T tiles; the block's registers are refilled with the next
+// block of the wave's stream as soon as each half (K, then V) has been consumed.
+template <int D, int T, int VROW>
+__device__ __forceinline__ void wave_block(WaveAcc<D, T>& A, BlockRegs<D>& r, const bf16x8_t (&qf)[T][D / 32],
+                                           int len, int pos, const int (&limit)[T],
+                                           const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
+                                           size_t boff_n, int len_n, uint8_t* vs, const uint8_t* vrd, int lane,
+                                           int kg, float sl2) {
+    // S^T = K Q^T for every tile (independent MFMA chains), then the K registers take the next loads
+    f32x4_t s[T];
 #pragma unroll
-        for (int c = 0; c < D / 16; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        m = -INFINITY;
-        l = 0.f;
-    }
-};
-
-// One 16-key block against the wave's 16 query rows; the block's registers are refilled with the
-// block two ahead in the wave's stream as soon as each half (K, then V) has been consumed.
-template <int D, int VROW>
-__device__ __forceinline__ void wave_block(WaveAcc<D>& A, BlockRegs<D>& r, const bf16x8_t (&qf)[D / 32], int len,
-                                           int pos, int limit, const uint16_t* __restrict__ kpool,
-                                           const uint16_t* __restrict__ vpool, size_t boff_n, int len_n,
-                                           uint8_t* vs, const uint8_t* vrd, int lane, int kg, float sl2) {
-    // S^T = K Q^T, then the K registers take the next loads
-    f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int tt = 0; tt < T; ++tt) s[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) s = mfma_16x16x32(__builtin_bit_cast(bf16x8_t, r.k[ks]), qf[ks], s);
+    for (int ks = 0; ks < D / 32; ++ks)
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt) s[tt] = mfma_16x16x32(__builtin_bit_cast(bf16x8_t, r.k[ks]), qf[tt][ks], s[tt]);
     load_k<D>(r, kpool, boff_n, len_n, lane);
-    // lane holds keys 4kg + e of row lane%16; mask only partial blocks and rows with a causal limit inside
-    if (__builtin_amdgcn_ballot_w64(!(len == 16 && limit >= pos + 15)) != 0) {
-        const int vlen = min(len, limit - pos + 1);
+    s16x4_t pb[T];
 #pragma unroll
-        for (int x = 0; x < 4; ++x)
-            if (4 * kg + x >= vlen) s[x] = -INFINITY;
-    }
-    const float mx = rowmax4(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
-    const float m_new = fmaxf(A.m, mx);
-    const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
-    float psum = 0.f;
+    for (int tt = 0; tt < T; ++tt) {
+        // lane holds keys 4kg + e of its row; mask only partial blocks and rows with a causal limit inside
+        if (__builtin_amdgcn_ballot_w64(!(len == 16 && limit[tt] >= pos + 15)) != 0) {
+            const int vlen = min(len, limit[tt] - pos + 1);
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
-        s[x] = __builtin_amdgcn_exp2f(fmaf(s[x], sl2, -msc));
-        psum += s[x];
-    }
-    const float alpha = m_new == A.m ? 1.f : __builtin_amdgcn_exp2f(A.m * sl2 - msc);
-    A.l = fmaf(A.l, alpha, psum);
-    A.m = m_new;
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
+            for (int x = 0; x < 4; ++x)
+                if (4 * kg + x >= vlen) s[tt][x] = -INFINITY;
+        }
+        const float mx = rowmax4(fmaxf(fmaxf(s[tt][0], s[tt][1]), fmaxf(s[tt][2], s[tt][3])));
+        const float m_new = fmaxf(A.m[tt], mx);
+        const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
+        float psum = 0.f;
 #pragma unroll
-        for (int c = 0; c < D / 16; ++c) A.acc[c] *= alpha;
+        for (int x = 0; x < 4; ++x) {
+            s[tt][x] = __builtin_amdgcn_exp2f(fmaf(s[tt][x], sl2, -msc));
+            psum += s[tt][x];
+        }
+        const float alpha = m_new == A.m[tt] ? 1.f : __builtin_amdgcn_exp2f(A.m[tt] * sl2 - msc);
+        A.l[tt] = fmaf(A.l[tt], alpha, psum);
+        A.m[tt] = m_new;
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) A.acc[tt][c] *= alpha;
+        }
+        pb[tt] = __builtin_bit_cast(s16x4_t, uint2{pack_bf16x2(s[tt][0], s[tt][1]), pack_bf16x2(s[tt][2], s[tt][3])});
     }
     // V rows into this wave's LDS region, then the V registers take the next loads
 #pragma unroll
@@ -493,226 +515,185 @@ __device__ __forceinline__ void wave_block(WaveAcc<D>& A, BlockRegs<D>& r, const
     }
     load_v<D>(r, vpool, boff_n, len_n, lane);
     // O^T += V^T P^T: P^T as the S^T result sits in the lanes, V^T by transposing LDS reads
-    const s16x4_t pb = __builtin_bit_cast(s16x4_t, uint2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])});
 #pragma unroll
     for (int ct = 0; ct < D / 16; ++ct) {
         const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vrd + ct * 32)));
-        A.acc[ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb, A.acc[ct], 0, 0, 0);
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
+            A.acc[tt][ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[tt], A.acc[tt][ct], 0, 0, 0);
+    }
+}
+
+// One wave's list of items [e0, e1), all of T column tiles.  The next key block is always in
+// flight, across item boundaries too (the last block of an item prefetches the first of the next);
+// the next item's descriptor is fetched at the start of an item.
+template <int D, int T>
+__device__ __forceinline__ void wave_run(const int4* __restrict__ wdesc, int e0, int e1,
+                                         const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+                                         const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
+                                         float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse,
+                                         int hq, int hkv, int G, float sl2, uint8_t* vs, int lane) {
+    constexpr int VROW = 2 * D + 32;  // LDS bytes per V row: the padding spreads 4 rows over 32 banks
+    const int col = lane & 15, kg = lane >> 4;
+    int tok[T], grp[T];
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        const int row = 16 * tt + col;
+        tok[tt] = min(row / G, tkv::kWaveToks - 1);
+        grp[tt] = row - (row / G) * G;
+    }
+    const size_t blk_stride = static_cast<size_t>(hkv) * (16 * D);
+    const uint8_t* vrd = vs + (4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
+
+    int4 dc = wdesc[static_cast<size_t>(e0) * 64 + lane];
+    int4 dn = wdesc[static_cast<size_t>(min(e0 + 1, e1 - 1)) * 64 + lane];
+    WaveItem<T> ic = wave_item<T>(dc, tok, grp, G);
+    bf16x8_t qf[T][D / 32];
+    load_q<D, T>(qf, q, ic, hq, kg);
+    BlockRegs<D> r;
+    {
+        const int len0 = __builtin_amdgcn_readlane(dc.y, 0);
+        const size_t b0 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 0)) * blk_stride +
+                          static_cast<size_t>(ic.kvh) * (16 * D);
+        load_k<D>(r, kpool, b0, len0, lane);
+        load_v<D>(r, vpool, b0, len0, lane);
+    }
+    WaveAcc<D, T> A;
+    for (int e = e0;; ++e) {
+        const bool more = e + 1 < e1;
+        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
+        const size_t kvh_off_n = static_cast<size_t>(__builtin_amdgcn_readlane(dn.w, 0)) * (16 * D);
+        A.reset();
+        const int nb = ic.nb;
+        for (int b = 0; b < nb; ++b) {
+            // the block after this one: the next of this item, or the first of the next item
+            // (a lane-wise select of the descriptor, then v_readlane: no branches)
+            const bool last = b + 1 == nb;
+            const int bn = last ? 0 : b + 1;
+            const int src_x = last ? dn.x : dc.x;
+            const int src_y = last ? (more ? dn.y : 0) : dc.y;
+            const size_t boff_n = static_cast<size_t>(__builtin_amdgcn_readlane(src_x, bn)) * blk_stride +
+                                  (last ? kvh_off_n : kvh_off);
+            wave_block<D, T, VROW>(A, r, qf, __builtin_amdgcn_readlane(dc.y, b), __builtin_amdgcn_readlane(dc.z, b),
+                                   ic.limit, kpool, vpool, boff_n, __builtin_amdgcn_readlane(src_y, bn), vs, vrd,
+                                   lane, kg, sl2);
+        }
+        // normalise and write each tile's final output or partial
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt) {
+            float l_tot = A.l[tt] + __shfl_xor(A.l[tt], 16);
+            l_tot += __shfl_xor(l_tot, 32);
+            if (!ic.ok[tt]) continue;
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            const float lse_v = l_tot > 0.f ? (A.m[tt] * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
+            if (ic.slot[tt] < 0) {
+                uint16_t* orow = o + (static_cast<size_t>(ic.qtok[tt]) * hq + ic.h[tt]) * D;
+#pragma unroll
+                for (int ct = 0; ct < D / 16; ++ct) {
+                    uint2 wv;
+                    wv.x = pack_bf16x2(A.acc[tt][ct][0] * inv, A.acc[tt][ct][1] * inv);
+                    wv.y = pack_bf16x2(A.acc[tt][ct][2] * inv, A.acc[tt][ct][3] * inv);
+                    *reinterpret_cast<uint2*>(orow + ct * 16 + kg * 4) = wv;
+                }
+                if (lse && kg == 0) lse[static_cast<size_t>(ic.qtok[tt]) * hq + ic.h[tt]] = lse_v;
+            } else {
+                float* prow = po + (static_cast<size_t>(ic.slot[tt]) * hq + ic.h[tt]) * D;
+#pragma unroll
+                for (int ct = 0; ct < D / 16; ++ct)
+                    *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) =
+                        make_float4(A.acc[tt][ct][0] * inv, A.acc[tt][ct][1] * inv, A.acc[tt][ct][2] * inv,
+                                    A.acc[tt][ct][3] * inv);
+                if (kg == 0) plse[static_cast<size_t>(ic.slot[tt]) * hq + ic.h[tt]] = lse_v;
+            }
+        }
+        if (!more) break;
+        dc = dn;
+        dn = wdesc[static_cast<size_t>(min(e + 2, e1 - 1)) * 64 + lane];
+        ic = wave_item<T>(dc, tok, grp, G);
+        load_q<D, T>(qf, q, ic, hq, kg);
     }
 }
 
 // Each wave walks its own list of items (a contiguous range of the descriptor stream) with no
-// barrier.  Key blocks go in pairs through two register sets, so the two blocks after the one
-// being contracted are always in flight, across item boundaries too (every item has an even
-// number of blocks); the descriptor two items ahead and the query rows of the next item are
-// fetched at the start of an item.
+// barrier; its tile width T (1..3 tiles of 16 query rows) is fixed per wave by the planner.
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_wave(
-    const int2* __restrict__ wdesc, const int32_t* __restrict__ woff, const uint16_t* __restrict__ q,
-    const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
-    float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
-    constexpr int VROW = 2 * D + 32;  // LDS bytes per V row: the padding spreads 4 rows over 32 banks
+    const int4* __restrict__ wdesc, const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
+    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq,
+    int hkv, int G, float sl2) {
+    constexpr int VROW = 2 * D + 32;
     __shared__ __attribute__((aligned(16))) uint8_t Vs[4][16 * VROW];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int w = blockIdx.x * 4 + wave;
-    const int e0 = woff[w], e1 = woff[w + 1];
+    const int e0 = woff[w], e1 = woff[w + 1], T = wtiles[w];
     if (e0 >= e1) return;  // waves are independent: no barrier follows
-    const int col = lane & 15, kg = lane >> 4;
-    const int t = col / G, g = col - t * G;
-    const size_t blk_stride = static_cast<size_t>(hkv) * (16 * D);
-    uint8_t* vs = Vs[wave];
-    const int j = lane & 15;
-    const uint8_t* vrd = vs + (4 * kg + (j >> 2)) * VROW + (4 * (j & 3)) * 2;
-
-    int2 dc = wdesc[static_cast<size_t>(e0) * 64 + lane];
-    int2 dn = wdesc[static_cast<size_t>(min(e0 + 1, e1 - 1)) * 64 + lane];
-    WaveItem ic = wave_item(dc, t, g, G);
-    bf16x8_t qf[D / 32];
-    load_q<D>(qf, q, ic, hq, kg);
-    BlockRegs<D> ra, rb;  // blocks 2i and 2i+1 of the stream
-    {
-        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
-        const int len0 = __builtin_amdgcn_readlane(dc.y, 0), len1 = __builtin_amdgcn_readlane(dc.y, 1);
-        const size_t b0 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 0)) * blk_stride + kvh_off;
-        const size_t b1 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 1)) * blk_stride + kvh_off;
-        load_k<D>(ra, kpool, b0, len0, lane);
-        load_v<D>(ra, vpool, b0, len0, lane);
-        load_k<D>(rb, kpool, b1, len1, lane);
-        load_v<D>(rb, vpool, b1, len1, lane);
-    }
-    WaveAcc<D> A;
-    for (int e = e0;; ++e) {
-        const bool more = e + 1 < e1;
-        // next item's query rows, and the descriptor of the item after it
-        const WaveItem in = wave_item(dn, t, g, G);
-        bf16x8_t qn[D / 32];
-        load_q<D>(qn, q, in, hq, kg);
-        const int2 dnn = wdesc[static_cast<size_t>(min(e + 2, e1 - 1)) * 64 + lane];
-        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
-        const size_t kvh_off_n = static_cast<size_t>(in.kvh) * (16 * D);
-        A.reset();
-        const int nb = ic.nb;  // even
-        for (int b = 0; b < nb; b += 2) {
-            // blocks b + 2 and b + 3 of this item, or blocks 0 and 1 of the next
-            // (a lane-wise select of the descriptor, then v_readlane: no branches)
-            const bool cross = b + 2 >= nb;
-            const int bn = cross ? 0 : b + 2;
-            const int src_x = cross ? dn.x : dc.x;
-            const int src_y = cross ? (more ? dn.y : 0) : dc.y;
-            const int blk_a = __builtin_amdgcn_readlane(src_x, bn), blk_b = __builtin_amdgcn_readlane(src_x, bn + 1);
-            const int len_a = __builtin_amdgcn_readlane(src_y, bn), len_b = __builtin_amdgcn_readlane(src_y, bn + 1);
-            const size_t off_n = cross ? kvh_off_n : kvh_off;
-            wave_block<D, VROW>(A, ra, qf, __builtin_amdgcn_readlane(dc.y, b), __builtin_amdgcn_readlane(dc.y, 32 + b),
-                                ic.limit, kpool, vpool, static_cast<size_t>(blk_a) * blk_stride + off_n, len_a, vs,
-                                vrd, lane, kg, sl2);
-            wave_block<D, VROW>(A, rb, qf, __builtin_amdgcn_readlane(dc.y, b + 1),
-                                __builtin_amdgcn_readlane(dc.y, 33 + b), ic.limit, kpool, vpool,
-                                static_cast<size_t>(blk_b) * blk_stride + off_n, len_b, vs, vrd, lane, kg, sl2);
-        }
-        // normalise and write the final output or the partial
-        float l_tot = A.l + __shfl_xor(A.l, 16);
-        l_tot += __shfl_xor(l_tot, 32);
-        if (ic.row_ok) {
-            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-            const float lse_v = l_tot > 0.f ? (A.m * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
-            if (ic.slot < 0) {
-                uint16_t* orow = o + (static_cast<size_t>(ic.qtok) * hq + ic.h) * D;
-#pragma unroll
-                for (int ct = 0; ct < D / 16; ++ct) {
-                    uint2 wv;
-                    wv.x = pack_bf16x2(A.acc[ct][0] * inv, A.acc[ct][1] * inv);
-                    wv.y = pack_bf16x2(A.acc[ct][2] * inv, A.acc[ct][3] * inv);
-                    *reinterpret_cast<uint2*>(orow + ct * 16 + kg * 4) = wv;
-                }
-                if (lse && kg == 0) lse[static_cast<size_t>(ic.qtok) * hq + ic.h] = lse_v;
-            } else {
-                float* prow = po + (static_cast<size_t>(ic.slot) * hq + ic.h) * D;
-#pragma unroll
-                for (int ct = 0; ct < D / 16; ++ct)
-                    *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) = make_float4(
-                        A.acc[ct][0] * inv, A.acc[ct][1] * inv, A.acc[ct][2] * inv, A.acc[ct][3] * inv);
-                if (kg == 0) plse[static_cast<size_t>(ic.slot) * hq + ic.h] = lse_v;
-            }
-        }
-        if (!more) break;
-        ic = in;
-        dc = dn;
-        dn = dnn;
-#pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) qf[ks] = qn[ks];
-    }
+    if (T == 1)
+        wave_run<D, 1>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
+    else if (T == 2)
+        wave_run<D, 2>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
+    else
+        wave_run<D, 3>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
 }
 
-// Log-sum-exp merge of one query token's partials (one workgroup per token).  Slot ids, then all
-// partial lse values, then all partial outputs are each fetched in one parallel round, so the
-// token costs three memory latencies however many partials it has (up to kMergeChunk at a time).
-constexpr int kMergeChunk = 32;
-
+// Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
+// are contiguous): every thread owns float4 columns of one head and folds the partials in with an
+// online softmax, eight partials' outputs and lse values in flight at a time -- one round of
+// memory latency per eight partials, no barriers.
 template <int D>
 __global__ __launch_bounds__(kThreads) void merge_partials(const tkv::MergeDesc* __restrict__ md,
-                                                           const int32_t* __restrict__ mslots,
                                                            const float* __restrict__ po,
                                                            const float* __restrict__ plse,
                                                            uint16_t* __restrict__ o, float* __restrict__ lse, int hq) {
-    extern __shared__ float sm[];              // w[kMergeChunk][hq], mx[hq], sum[hq]
-    __shared__ int sid[kMergeChunk];
-    float* w = sm;
-    float* mxs = sm + kMergeChunk * hq;
-    float* sums = mxs + hq;
-    const tkv::MergeDesc m = md[blockIdx.x];
-    const int tid = threadIdx.x;
     constexpr int C4 = D / 4;
-    // pass 1: running max and sum over all partials, chunk by chunk
-    for (int h = tid; h < hq; h += kThreads) {
-        mxs[h] = -INFINITY;
-        sums[h] = 0.f;
-    }
-    for (int c0 = 0; c0 < m.n_slots; c0 += kMergeChunk) {
-        const int n = min(kMergeChunk, m.n_slots - c0);
-        __syncthreads();
-        if (tid < n) sid[tid] = mslots[m.slot_off + c0 + tid];
-        __syncthreads();
-        for (int i = tid; i < n * hq; i += kThreads) {
-            const int j = i / hq, h = i - j * hq;
-            w[i] = plse[static_cast<size_t>(sid[j]) * hq + h];
-        }
-        __syncthreads();
-        for (int h = tid; h < hq; h += kThreads) {
-            float mx = mxs[h];
-            for (int j = 0; j < n; ++j) mx = fmaxf(mx, w[j * hq + h]);
-            float sum = mx == -INFINITY ? 0.f : sums[h] * __expf(mxs[h] - mx);
-            if (mx != -INFINITY)
-                for (int j = 0; j < n; ++j) sum += __expf(w[j * hq + h] - mx);
-            mxs[h] = mx;
-            sums[h] = sum;
-        }
-    }
-    __syncthreads();
-    for (int h = tid; h < hq; h += kThreads)
-        if (lse) lse[static_cast<size_t>(m.qtok) * hq + h] = sums[h] > 0.f ? mxs[h] + __logf(sums[h]) : -INFINITY;
-    // pass 2: weighted sum of the partial outputs
-    constexpr int kPer = (64 * C4 + kThreads - 1) / kThreads;   // float4 chunks per thread for hq <= 64
-    float4 acc[kPer];
+    const tkv::MergeDesc m = md[blockIdx.x];
+    const size_t s0 = static_cast<size_t>(m.slot_off);
+    const int n = m.n_slots;
+    const float4* po4 = reinterpret_cast<const float4*>(po);
+    for (int idx = threadIdx.x; idx < hq * C4; idx += kThreads) {
+        const int h = idx / C4;
+        float mx = -INFINITY, sum = 0.f;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j0 = 0; j0 < n; j0 += 8) {
+            float4 x[8];
+            float lj[8];
 #pragma unroll
-    for (int u = 0; u < kPer; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int h0 = 0; h0 < hq; h0 += 64) {
-        const int hn = min(64, hq - h0);
-        for (int c0 = 0; c0 < m.n_slots; c0 += kMergeChunk) {
-            const int n = min(kMergeChunk, m.n_slots - c0);
-            __syncthreads();
-            if (tid < n) sid[tid] = mslots[m.slot_off + c0 + tid];
-            __syncthreads();
-            for (int i = tid; i < n * hn; i += kThreads) {
-                const int j = i / hn, h = h0 + i - j * hn;
-                const float s = sums[h];
-                w[j * hq + h] = s > 0.f ? __expf(plse[static_cast<size_t>(sid[j]) * hq + h] - mxs[h]) / s : 0.f;
+            for (int v = 0; v < 8; ++v) {
+                const size_t sl = s0 + min(j0 + v, n - 1);
+                x[v] = po4[(sl * hq) * C4 + idx];
+                lj[v] = j0 + v < n ? plse[sl * hq + h] : -INFINITY;
             }
-            __syncthreads();
+            float cm = lj[0];
 #pragma unroll
-            for (int u = 0; u < kPer; ++u) {
-                const int idx = tid + u * kThreads;
-                if (idx >= hn * C4) continue;
-                const int h = h0 + idx / C4, c = (idx % C4) * 4;
-                float4 a = acc[u];
-                int j = 0;
-                for (; j + 4 <= n; j += 4) {   // four independent loads in flight
-                    float4 x[4];
+            for (int v = 1; v < 8; ++v) cm = fmaxf(cm, lj[v]);
+            const float m_new = fmaxf(mx, cm);
+            if (m_new == -INFINITY) continue;  // no key seen yet
+            const float a = __expf(mx - m_new);
+            sum *= a;
+            acc.x *= a;
+            acc.y *= a;
+            acc.z *= a;
+            acc.w *= a;
 #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        x[v] = *reinterpret_cast<const float4*>(po + (static_cast<size_t>(sid[j + v]) * hq + h) * D + c);
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const float ww = w[(j + v) * hq + h];
-                        a.x += ww * x[v].x;
-                        a.y += ww * x[v].y;
-                        a.z += ww * x[v].z;
-                        a.w += ww * x[v].w;
-                    }
-                }
-                for (; j < n; ++j) {
-                    const float4 x = *reinterpret_cast<const float4*>(po + (static_cast<size_t>(sid[j]) * hq + h) * D + c);
-                    const float ww = w[j * hq + h];
-                    a.x += ww * x.x;
-                    a.y += ww * x.y;
-                    a.z += ww * x.z;
-                    a.w += ww * x.w;
-                }
-                acc[u] = a;
+            for (int v = 0; v < 8; ++v) {
+                const float wv = __expf(lj[v] - m_new);  // 0 for padding entries (lj = -inf)
+                sum += wv;
+                acc.x = fmaf(wv, x[v].x, acc.x);
+                acc.y = fmaf(wv, x[v].y, acc.y);
+                acc.z = fmaf(wv, x[v].z, acc.z);
+                acc.w = fmaf(wv, x[v].w, acc.w);
             }
+            mx = m_new;
         }
-#pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int idx = tid + u * kThreads;
-            if (idx >= hn * C4) continue;
-            const int h = h0 + idx / C4, c = (idx % C4) * 4;
-            uint2 out;
-            out.x = pack_bf16x2(acc[u].x, acc[u].y);
-            out.y = pack_bf16x2(acc[u].z, acc[u].w);
-            *reinterpret_cast<uint2*>(o + (static_cast<size_t>(m.qtok) * hq + h) * D + c) = out;
-            acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+        const float inv = sum > 0.f ? 1.f / sum : 0.f;
+        uint2 wv;
+        wv.x = pack_bf16x2(acc.x * inv, acc.y * inv);
+        wv.y = pack_bf16x2(acc.z * inv, acc.w * inv);
+        *reinterpret_cast<uint2*>(o + (static_cast<size_t>(m.qtok) * hq) * D + idx * 4) = wv;
+        if (lse && idx % C4 == 0)
+            lse[static_cast<size_t>(m.qtok) * hq + h] = sum > 0.f ? mx + __logf(sum) : -INFINITY;
     }
 }
 
@@ -736,11 +717,11 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
                     hipStream_t st) {
     uint8_t* ws = static_cast<uint8_t*>(p->d_ws);
     const auto* merges = reinterpret_cast<const MergeDesc*>(ws + p->off_merges);
-    const auto* mslots = reinterpret_cast<const int32_t*>(ws + p->off_mslots);
     const auto* wg_off = reinterpret_cast<const int32_t*>(ws + p->off_wg);
     const auto* stages = reinterpret_cast<const StageDesc*>(ws + p->off_stages);
-    const auto* wdesc = reinterpret_cast<const int2*>(ws + p->off_wdesc);
+    const auto* wdesc = reinterpret_cast<const int4*>(ws + p->off_wdesc);
     const auto* woff = reinterpret_cast<const int32_t*>(ws + p->off_woff);
+    const auto* wtiles = reinterpret_cast<const int32_t*>(ws + p->off_wtiles);
     const auto* toks = reinterpret_cast<const TokDesc*>(ws + p->off_toks);
     const auto* blks = reinterpret_cast<const BlkDesc*>(ws + p->off_blks);
     float* po = reinterpret_cast<float*>(ws + p->off_po);
@@ -763,16 +744,15 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of 4
     if (n_wave > 0)
         hipLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / 4)), dim3(kThreads), 0, st,
-                           wdesc, woff, static_cast<const uint16_t*>(q),
+                           wdesc, woff, wtiles, static_cast<const uint16_t*>(q),
                            static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                            static_cast<uint16_t*>(o), lse, po, plse, hq, hkv, p->group, sl2);
     e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
     if (ev) (void)hipEventRecord(ev[1], st);
     if (!p->merges.empty()) {
-        hipLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(kThreads),
-                           (kMergeChunk + 2) * hq * sizeof(float), st,
-                           merges, mslots, po, plse, static_cast<uint16_t*>(o), lse, hq);
+        hipLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(kThreads), 0, st,
+                           merges, po, plse, static_cast<uint16_t*>(o), lse, hq);
         e = hipGetLastError();
         if (e != hipSuccess) return set_error(TKV_EHIP, "merge launch: %s", hipGetErrorString(e));
     }

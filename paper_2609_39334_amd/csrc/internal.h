@@ -23,9 +23,11 @@ constexpr int kTileRows = 64;  // query rows (token x head) per work item
 constexpr int kPersistentWGs = 768;  // resident workgroups of the attention kernel (3 per CU on 256 CUs)
 constexpr int kItemShared = 0;  // tile of several rows' tokens over one segment chunk (workgroup kernel)
 constexpr int kItemRow = 1;     // tile of one row's tokens over its whole path (workgroup kernel)
-constexpr int kItemWave = 2;    // tile of <= kWaveRows rows over one segment chunk (wave kernel)
-constexpr int kWaveRows = 16;   // query rows of a wave-kernel tile
+constexpr int kItemWave = 2;    // tile of <= 16 T rows over one segment chunk (wave kernel)
+constexpr int kWaveRows = 16;   // query rows of one MFMA column tile of the wave kernel
+constexpr int kWaveMaxTiles = 3;  // column tiles a wave contracts against each K/V block
 constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
+constexpr int kWaveToks = 48;   // query tokens of a wave-kernel item (16 kWaveMaxTiles / G)
 constexpr int kWaveWorkers = 2048;  // waves of the wave kernel (each streams a list of items)
 
 // One work item = one workgroup: a tile of query tokens (each with all G query heads of one KV
@@ -73,19 +75,20 @@ struct StageDesc {
 constexpr int kStageFirst = 1;
 constexpr int kStageLast = 2;
 
-// A wave-kernel item as one 512-byte record that a wave loads with one 8-byte load per lane
-// (lane l gets e[l]); block fields come out with v_readlane, token fields with ds_bpermute.
-//   e[j]      (j < 16): {pool block id, length} of key block j (block 0's id, length 0 past n_blk)
-//   e[16 + t] (t < 16): {query token, causal limit} of tile token t (token 0's past n_tok)
-//   e[32 + j]:          {partial slot of tile token j (-1: final output), path position of block j}
-//   e[48]:              {KV head, tile tokens}     e[49]: {key blocks rounded up to even, 0}
+// A wave-kernel item as one 1-KB record that a wave loads with one 16-byte load per lane (lane l
+// gets e[l]); block fields come out with v_readlane, token fields with ds_bpermute.
+//   e[j]      (j < 16): {pool block id, length, path position, header word j} of key block j
+//                       (block 0's id and length 0 past the item's blocks); header words:
+//                       0 KV head, 1 tile tokens, 2 key blocks
+//   e[16 + t] (t < 48): {query token, causal limit, partial slot (-1: final output), 0} of tile
+//                       token t (token 0's past the tile)
 struct WaveDesc {
-    int32_t e[128];
+    int32_t e[256];
 };
 
 struct MergeDesc {
     int32_t qtok;
-    int32_t slot_off;  // first entry in the merge slot list
+    int32_t slot_off;  // first partial slot of the token (its slots are contiguous)
     int32_t n_slots;
     int32_t pad;
 };
@@ -108,9 +111,10 @@ struct tkv_plan {
     std::vector<tkv::StageDesc> stages;       // per workgroup, in processing order
     std::vector<tkv::WaveDesc> wave_desc;     // wave-kernel items, each wave's list contiguous
     std::vector<int32_t> wave_off;            // [n_waves + 1] each wave's range in wave_desc
+    std::vector<int32_t> wave_tiles;          // [n_waves] column tiles of every item of the wave
     int32_t n_slots = 0;
     // workspace layout (byte offsets)
-    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wg = 0, off_stages = 0, off_wdesc = 0, off_woff = 0;
+    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wg = 0, off_stages = 0, off_wdesc = 0, off_woff = 0, off_wtiles = 0;
     size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;
     std::vector<uint8_t> image;  // host copy of the descriptor region
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)

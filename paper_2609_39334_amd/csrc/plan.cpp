@@ -40,8 +40,7 @@ using tkv::TokDesc;
 namespace {
 
 constexpr int kChunkBlocks = 16;  // longest key run of one shared item (256 tokens)
-static_assert(kChunkBlocks <= tkv::kWaveBlocks && kChunkBlocks % 2 == 0,
-              "a wave item holds its key blocks (an even number after padding) in one record");
+static_assert(kChunkBlocks <= tkv::kWaveBlocks, "a wave item holds its key blocks in one record");
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
@@ -212,36 +211,38 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 if (!c.toks.empty()) chunks.push_back(std::move(c));
             });
         }
-        // partial slots for tokens covered by more than one chunk
-        std::vector<std::vector<int32_t>> slots_of(st.n_qtok);
+        // partial slots for tokens covered by more than one chunk: each token's slots are
+        // contiguous (in chunk order), so the merge reads a token's partials as one range
+        std::vector<int32_t> slot_next(st.n_qtok, -1);
+        for (int32_t q = 0; q < st.n_qtok; ++q) {
+            if (cover[q] < 2) continue;
+            p->merges.push_back(MergeDesc{q, p->n_slots, cover[q], 0});
+            slot_next[q] = p->n_slots;
+            p->n_slots += cover[q];
+        }
         for (Chunk& c : chunks)
             for (TokDesc& t : c.toks)
-                if (cover[t.qtok] > 1) {
-                    t.slot = p->n_slots++;
-                    slots_of[t.qtok].push_back(t.slot);
-                }
-        for (int32_t q = 0; q < st.n_qtok; ++q) {
-            if (slots_of[q].empty()) continue;
-            p->merges.push_back(MergeDesc{q, static_cast<int32_t>(p->merge_slots.size()),
-                                          static_cast<int32_t>(slots_of[q].size()), 0});
-            p->merge_slots.insert(p->merge_slots.end(), slots_of[q].begin(), slots_of[q].end());
-        }
-        // Narrow chunks (at most kWaveRows query rows in all, G <= 16) go to the wave kernel, one
-        // wave per 16-row tile; wider chunks use the workgroup kernel's 64-row tiles, which share
-        // each staged K/V block among four waves.
-        int32_t wave_max_rows = tkv::kWaveRows;
-        if (const char* env = std::getenv("TKV_WAVE_MAX_ROWS")) wave_max_rows = std::atoi(env);
+                if (cover[t.qtok] > 1) t.slot = slot_next[t.qtok]++;
+        p->merge_slots.resize(p->n_slots);
+        std::iota(p->merge_slots.begin(), p->merge_slots.end(), 0);
+        // Chunks of groups with G <= 16 go to the wave kernel: a wave contracts each K/V block
+        // against T column tiles of 16 rows (T = 1..3 as the chunk's rows need), so a chunk of
+        // up to 48 rows is read once.  Chunks wider than TKV_WAVE_MAX_ROWS (and groups with
+        // G > 16) use the workgroup kernel's 64-row tiles.
+        int64_t wave_max_rows = int64_t{1} << 40;
+        if (const char* env = std::getenv("TKV_WAVE_MAX_ROWS")) wave_max_rows = std::atoll(env);
         for (const Chunk& c : chunks) {
             const int64_t rows = static_cast<int64_t>(c.toks.size()) * G;
-            const bool wave_tiles = G <= tkv::kWaveRows && rows <= wave_max_rows;
-            const int32_t per_tile = wave_tiles ? tkv::kWaveRows / G : tpt;
+            const bool wave = G <= tkv::kWaveRows && rows <= wave_max_rows;
+            const int32_t T = static_cast<int32_t>(std::min<int64_t>(tkv::kWaveMaxTiles, (rows + 15) / 16));
+            const int32_t per_tile = wave ? tkv::kWaveRows * T / G : tpt;
             tile_evenly(static_cast<int32_t>(c.toks.size()), per_tile, [&](int32_t a, int32_t e) {
                 const int32_t tok_off = static_cast<int32_t>(p->toks.size());
                 p->toks.insert(p->toks.end(), c.toks.begin() + a, c.toks.begin() + e);
                 for (int32_t h = 0; h < s.hkv; ++h) {
                     const ItemDesc d{h, tok_off, e - a, c.blk_off, c.n_blk, c.pos0,
-                                     wave_tiles ? tkv::kItemWave : tkv::kItemShared, 0};
-                    (wave_tiles ? p->wave_items : p->items).push_back(d);
+                                     wave ? tkv::kItemWave : tkv::kItemShared, wave ? T : 0};
+                    (wave ? p->wave_items : p->items).push_back(d);
                 }
             });
         }
@@ -273,89 +274,106 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         st.n_items_row = st.n_items - st.n_items_shared;
         std::stable_sort(p->wave_items.begin(), p->wave_items.end(),
                          [](const ItemDesc& a, const ItemDesc& b) { return a.n_blk > b.n_blk; });
-        // Wave streams.  Workgroups are dispatched round-robin over the 8 XCDs (each with its own
-        // L2), so wave w runs on XCD (w / 4) % 8.  All tiles of one (chunk, KV head) -- which read
-        // the same K/V blocks -- go to one XCD, spread over its waves at the same depth of their
-        // lists, so the repeated reads of a shared chunk hit that XCD's L2.  Groups are assigned
-        // to XCDs and items to the XCD's waves by longest processing time first.
+        // Wave streams.  Every wave runs items of one tile width T (its code path is fixed);
+        // waves are split over the widths in proportion to their work.  Workgroups are dispatched
+        // round-robin over the 8 XCDs (each with its own L2), so wave w runs on XCD (w / 4) % 8:
+        // all tiles of one (chunk, KV head), which read the same K/V blocks, go to one XCD.
+        // Groups are assigned to XCDs, and items to the XCD's waves, longest processing time first.
         {
             const int32_t n_items = static_cast<int32_t>(p->wave_items.size());
             int32_t target = tkv::kWaveWorkers;
             if (const char* env = std::getenv("TKV_WAVES")) target = std::max(4, std::atoi(env));
-            const int32_t n_w = n_items ? (std::min(target, n_items) + 3) / 4 * 4 : 0;
-            constexpr int32_t kXcds = 8;
-            std::vector<std::vector<int32_t>> xcd_waves(kXcds);
-            for (int32_t w = 0; w < n_w; ++w) xcd_waves[(w / 4) % kXcds].push_back(w);
-            // groups of items sharing key blocks: same chunk (first block entry) and KV head
-            std::map<std::pair<int32_t, int32_t>, int32_t> gid;
-            std::vector<std::vector<int32_t>> groups;
-            std::vector<int64_t> gcost;
+            auto cost = [](const ItemDesc& it) { return static_cast<int64_t>(it.n_blk) * (3 + it.pad) + 4; };
+            std::vector<std::vector<int32_t>> by_t(tkv::kWaveMaxTiles + 1);
+            std::vector<int64_t> cost_t(tkv::kWaveMaxTiles + 1, 0);
+            int64_t cost_all = 0;
             for (int32_t i = 0; i < n_items; ++i) {
-                const ItemDesc& it = p->wave_items[i];
-                auto ins = gid.emplace(std::make_pair(it.blk_off, it.kvh), static_cast<int32_t>(groups.size()));
-                if (ins.second) {
-                    groups.emplace_back();
-                    gcost.push_back(0);
-                }
-                groups[ins.first->second].push_back(i);
-                gcost[ins.first->second] += it.n_blk + 1;
-            }
-            std::vector<int32_t> gorder(groups.size());
-            std::iota(gorder.begin(), gorder.end(), 0);
-            std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a, int32_t b) { return gcost[a] > gcost[b]; });
-            using Load = std::pair<int64_t, int32_t>;
-            std::priority_queue<Load, std::vector<Load>, std::greater<Load>> xheap;
-            for (int32_t x = 0; x < kXcds; ++x)
-                if (!xcd_waves[x].empty()) xheap.push({0, x});
-            std::vector<std::vector<int32_t>> xcd_items(kXcds);
-            for (int32_t g2 : gorder) {
-                Load l = xheap.top();
-                xheap.pop();
-                xcd_items[l.second].insert(xcd_items[l.second].end(), groups[g2].begin(), groups[g2].end());
-                // cost per wave of the XCD (the counts differ only for small grids)
-                l.first += gcost[g2] * 1024 / static_cast<int64_t>(xcd_waves[l.second].size());
-                xheap.push(l);
-            }
-            std::vector<std::vector<int32_t>> lists(n_w);
-            for (int32_t x = 0; x < kXcds; ++x) {
-                std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-                for (int32_t w : xcd_waves[x]) heap.push({0, w});
-                for (int32_t i : xcd_items[x]) {
-                    Load l = heap.top();
-                    heap.pop();
-                    lists[l.second].push_back(i);
-                    l.first += p->wave_items[i].n_blk + 1;
-                    heap.push(l);
-                }
+                by_t[p->wave_items[i].pad].push_back(i);
+                cost_t[p->wave_items[i].pad] += cost(p->wave_items[i]);
+                cost_all += cost(p->wave_items[i]);
             }
             p->wave_off.assign(1, 0);
-            for (int32_t w = 0; w < n_w; ++w) {
-                for (int32_t i : lists[w]) {
+            constexpr int32_t kXcds = 8;
+            for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
+                const std::vector<int32_t>& its = by_t[T];
+                if (its.empty()) continue;
+                // waves of this width: a share of the target, whole workgroups, at most one per item
+                const int64_t share = (static_cast<int64_t>(target) * cost_t[T] + cost_all - 1) / cost_all;
+                const int32_t n_w = static_cast<int32_t>(
+                    (std::min<int64_t>(std::max<int64_t>(share, 4), static_cast<int64_t>(its.size())) + 3) / 4 * 4);
+                const int32_t w0 = static_cast<int32_t>(p->wave_tiles.size());  // a multiple of 4
+                std::vector<std::vector<int32_t>> xcd_waves(kXcds);
+                for (int32_t w = 0; w < n_w; ++w) xcd_waves[((w0 + w) / 4) % kXcds].push_back(w);
+                std::map<std::pair<int32_t, int32_t>, int32_t> gid;
+                std::vector<std::vector<int32_t>> groups;
+                std::vector<int64_t> gcost;
+                for (int32_t i : its) {
                     const ItemDesc& it = p->wave_items[i];
-                    tkv::WaveDesc wd{};
-                    int32_t pos = it.pos0;
-                    // the kernel walks blocks in pairs: an odd key list gets an empty (length 0) block
-                    const int32_t nb_even = (it.n_blk + 1) & ~1;
-                    for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
-                        const bool in = j < it.n_blk;
-                        const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
-                        wd.e[2 * j] = bd.blk;
-                        wd.e[2 * j + 1] = in ? bd.len : 0;
-                        wd.e[2 * (32 + j) + 1] = pos;
-                        if (in) pos += bd.len;
+                    auto ins = gid.emplace(std::make_pair(it.blk_off, it.kvh), static_cast<int32_t>(groups.size()));
+                    if (ins.second) {
+                        groups.emplace_back();
+                        gcost.push_back(0);
                     }
-                    for (int32_t t = 0; t < tkv::kWaveRows; ++t) {
-                        const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
-                        wd.e[2 * (16 + t)] = td.qtok;
-                        wd.e[2 * (16 + t) + 1] = td.limit;
-                        wd.e[2 * (32 + t)] = td.slot;
-                    }
-                    wd.e[96] = it.kvh;
-                    wd.e[97] = it.n_tok;
-                    wd.e[98] = nb_even;
-                    p->wave_desc.push_back(wd);
+                    groups[ins.first->second].push_back(i);
+                    gcost[ins.first->second] += cost(it);
                 }
-                p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
+                std::vector<int32_t> gorder(groups.size());
+                std::iota(gorder.begin(), gorder.end(), 0);
+                std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a, int32_t b) { return gcost[a] > gcost[b]; });
+                using Load = std::pair<int64_t, int32_t>;
+                std::priority_queue<Load, std::vector<Load>, std::greater<Load>> xheap;
+                for (int32_t x = 0; x < kXcds; ++x)
+                    if (!xcd_waves[x].empty()) xheap.push({0, x});
+                std::vector<std::vector<int32_t>> xcd_items(kXcds);
+                for (int32_t g2 : gorder) {
+                    Load l = xheap.top();
+                    xheap.pop();
+                    xcd_items[l.second].insert(xcd_items[l.second].end(), groups[g2].begin(), groups[g2].end());
+                    l.first += gcost[g2] * 1024 / static_cast<int64_t>(xcd_waves[l.second].size());
+                    xheap.push(l);
+                }
+                std::vector<std::vector<int32_t>> lists(n_w);
+                for (int32_t x = 0; x < kXcds; ++x) {
+                    std::stable_sort(xcd_items[x].begin(), xcd_items[x].end(), [&](int32_t a, int32_t b) {
+                        return p->wave_items[a].n_blk > p->wave_items[b].n_blk;
+                    });
+                    std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
+                    for (int32_t w : xcd_waves[x]) heap.push({0, w});
+                    for (int32_t i : xcd_items[x]) {
+                        Load l = heap.top();
+                        heap.pop();
+                        lists[l.second].push_back(i);
+                        l.first += cost(p->wave_items[i]);
+                        heap.push(l);
+                    }
+                }
+                for (int32_t w = 0; w < n_w; ++w) {
+                    for (int32_t i : lists[w]) {
+                        const ItemDesc& it = p->wave_items[i];
+                        tkv::WaveDesc wd{};
+                        int32_t pos = it.pos0;
+                        for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
+                            const bool in = j < it.n_blk;
+                            const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
+                            wd.e[4 * j] = bd.blk;
+                            wd.e[4 * j + 1] = in ? bd.len : 0;
+                            wd.e[4 * j + 2] = pos;
+                            if (in) pos += bd.len;
+                        }
+                        wd.e[3] = it.kvh;
+                        wd.e[7] = it.n_tok;
+                        wd.e[11] = it.n_blk;
+                        for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
+                            const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
+                            wd.e[4 * (16 + t)] = td.qtok;
+                            wd.e[4 * (16 + t) + 1] = td.limit;
+                            wd.e[4 * (16 + t) + 2] = td.slot;
+                        }
+                        p->wave_desc.push_back(wd);
+                    }
+                    p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
+                    p->wave_tiles.push_back(T);
+                }
             }
         }
         st.n_slots = p->n_slots;
@@ -433,6 +451,8 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         off = align256(off + bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
         p->off_woff = off;
         off = align256(off + bytes(p->wave_off.size(), sizeof(int32_t)));
+        p->off_wtiles = off;
+        off = align256(off + bytes(p->wave_tiles.size(), sizeof(int32_t)));
         p->desc_bytes = off;
         p->off_po = off;
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq * s.d, sizeof(float)));
@@ -452,6 +472,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         put(p->off_stages, p->stages.data(), bytes(p->stages.size(), sizeof(tkv::StageDesc)));
         put(p->off_wdesc, p->wave_desc.data(), bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
         put(p->off_woff, p->wave_off.data(), bytes(p->wave_off.size(), sizeof(int32_t)));
+        put(p->off_wtiles, p->wave_tiles.data(), bytes(p->wave_tiles.size(), sizeof(int32_t)));
     } catch (...) {
         delete p;
         return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
