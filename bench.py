@@ -28,6 +28,16 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 MALL_BYTES = 256 << 20
 
 
+def kernel_sources_digest():
+    """sha256 over the sources that decide what the attention kernels do (kernels, planner)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("attn.hip", "plan.cpp", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_39334_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def _args():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -39,7 +49,11 @@ def _args():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU baseline sample")
     ap.add_argument("--kv-copies", type=int, default=0,
                     help="device copies of the K/V pool rotated over the steps (0: enough to defeat the 256 MB MALL)")
-    ap.add_argument("--traffic", default=None, help="JSON file with measured per-launch HBM bytes of the main kernel")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="JSON with per-launch HBM bytes of the main kernel from rocprofv3 counters (used only if "
+                         "the kernel sources are unchanged since they were taken)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run one plain 256 MiB device-to-device copy first (calibrates HBM byte counters)")
     return ap.parse_args()
 
 
@@ -104,6 +118,12 @@ def main():
     stream = torch.cuda.current_stream()
     call = plan.decode if L.decode else plan.verify
 
+    if a.calib_copy:                         # a copy kernel of known size for the PMC byte counters
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for i in range(a.warmup):
         call(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
     ev0 = torch.cuda.Event(enable_timing=True)
@@ -125,7 +145,7 @@ def main():
     n_rec, ms_main, ms_merge = tkv.tkv_plan_profile_read(plan.h)
     tkv.tkv_plan_profile(plan.h, 0)
     t_main = ms_main / max(1, n_rec) / 1e3
-    t_merge = ms_merge / max(1, n_rec) / 1e3
+    t_merge = ms_merge / max(1, n_rec) / 1e3 if st["n_merge"] else 0.0
 
     # ------------------------------------------------------------------ accounting
     b_uniq = st["uniq_kv_tokens"] * s.hkv * s.d * 2 * 2            # K and V, bf16
@@ -135,12 +155,23 @@ def main():
     traffic = None
     if a.traffic and os.path.exists(a.traffic):
         with open(a.traffic) as f:
-            tr = json.load(f)
-        if tr.get("workload") == a.workload:
+            tr = json.load(f).get(a.workload)
+        if tr and tr.get("sources_sha256") == kernel_sources_digest():
             traffic = tr.get("bytes_per_launch")
-    roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "kernel": "attn_items", "algorithmic_bytes": b_uniq, "kernel_us": round(t_main * 1e6, 2)}
+    main_kernels = ([] if st["n_items"] == st["n_items_wave"] else ["attn_persist"]) + \
+                   (["attn_wave"] if st["n_items_wave"] else [])
+    # the bound is the one the work's arithmetic intensity puts it under (ridge: peak flop/s over
+    # peak bytes/s); decode is HBM-bound, multi-token verify of long steps is MFMA-bound
+    mfma_bound = flops / b_uniq > MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if mfma_bound:
+        achieved_tf = flops / t_main / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved_tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
+                "kernel": "+".join(main_kernels), "algorithmic_flops": flops, "kernel_us": round(t_main * 1e6, 2)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "+".join(main_kernels), "algorithmic_bytes": b_uniq, "kernel_us": round(t_main * 1e6, 2)}
 
     # ------------------------------------------------------------------ CPU baseline (oracle)
     cpu = None
@@ -186,8 +217,9 @@ def main():
         "hbm_frac_whole_call": round(b_uniq / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
         "mfma_frac_whole_call": round(flops / (ms_step / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
         "logical_candidate_tokens_per_s": round(st["logical_qtok"] / (ms_step / 1e3), 1),
-        "kernel_us": {"attn_items": round(t_main * 1e6, 2), "merge_partials": round(t_merge * 1e6, 2)},
+        "kernel_us": {"+".join(main_kernels): round(t_main * 1e6, 2), "merge_partials": round(t_merge * 1e6, 2)},
         "plan": {"items": st["n_items"], "shared_items": st["n_items_shared"], "row_items": st["n_items_row"],
+                 "wave_items": st["n_items_wave"], "waves": st["n_waves"],
                  "partial_slots": st["n_slots"], "merged_tokens": st["n_merge"], "segments": st["n_segments"],
                  "shared_segments": st["n_shared_segments"]},
         "host_ms": {"block_manager": round(t_bm * 1e3, 2), "coalesce": round(t_coal * 1e3, 3),

@@ -160,6 +160,8 @@ void tkv_plan_destroy(tkv_plan* plan);
 typedef struct {
     int32_t n_rows, n_qtok, n_items, n_items_shared, n_items_row, n_slots, n_merge;
     int32_t n_segments, n_shared_segments;
+    int32_t n_items_wave;   /* items run by the wave kernel (a subset of the shared items) */
+    int32_t n_waves;        /* waves of the wave kernel */
     int64_t logical_qtok;   /* sum of multiplicity * q_len */
     int64_t uniq_kv_tokens; /* tokens in the union of the rows' blocks */
     int64_t path_kv_tokens; /* sum over rows of kv_len (what per-row gathering would read) */
@@ -169,7 +171,9 @@ int tkv_plan_get_stats(const tkv_plan* plan, tkv_plan_stats* out);
 
 /* Read-only view of the plan's host descriptor arrays (valid until tkv_plan_destroy), for tests
  * and tools.  Formats (int32 words):
- *   items[n_items][8]  {kv_head, tok_off, n_tok, blk_off, n_blk, pos0, kind (0 shared, 1 row), 0}
+ *   items[n_items][8]  {kv_head, tok_off, n_tok, blk_off, n_blk, pos0, kind, tiles}: kind 0 shared
+ *                      chunk (workgroup kernel), 1 whole-path row tile, 2 shared chunk on the wave
+ *                      kernel with `tiles` column tiles of 16 query rows (0 for kinds 0 and 1)
  *   toks[n_toks][4]    {query token, largest visible key position, partial slot or -1, 0}
  *   blks[n_blks][2]    {block id, block length}
  *   merges[n_merge][4] {query token, offset into merge_slots, slot count, 0}
@@ -193,8 +197,9 @@ int tkv_verify(const tkv_plan* plan, const void* q, const void* k, const void* v
                float* lse, void* hip_stream);
 
 /* Instrumentation.  tkv_plan_profile(plan, max_calls) makes the next max_calls attention calls on
- * this plan record HIP events before the main attention kernel, after it, and after the merge
- * kernel, on the call's stream (0 turns recording off and frees the events).
+ * this plan record HIP events taken from the kernel dispatches' own start and end timestamps: the
+ * main attention phase (start of its first kernel to end of its last) and the merge kernel
+ * (0 turns recording off and frees the events).
  * tkv_plan_profile_read waits for the recorded events and returns the number of recorded calls
  * and the summed milliseconds of the main kernel and of the merge kernel over those calls, then
  * starts a new recording window.  EINVAL, EHIP. */

@@ -34,7 +34,8 @@ class tkv_shape(ctypes.Structure):
 
 class tkv_plan_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("n_rows", "n_qtok", "n_items", "n_items_shared", "n_items_row",
-                                              "n_slots", "n_merge", "n_segments", "n_shared_segments")] + \
+                                              "n_slots", "n_merge", "n_segments", "n_shared_segments",
+                                              "n_items_wave", "n_waves")] + \
                [(n, ctypes.c_int64) for n in ("logical_qtok", "uniq_kv_tokens", "path_kv_tokens", "flops")]
 
 

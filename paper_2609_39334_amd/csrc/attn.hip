@@ -13,6 +13,7 @@
 //
 // merge_partials: log-sum-exp merge of the per-segment partials of one query token (all heads):
 //   lse = log sum_j exp(lse_j),  o = sum_j exp(lse_j - lse) o_j.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -728,35 +729,40 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     float* plse = reinterpret_cast<float*>(ws + p->off_plse);
     const float sl2 = 1.4426950408889634f / std::sqrt(static_cast<float>(D));
     const int hq = p->shape.hq, hkv = p->shape.hkv;
+    // Instrumented calls time the kernels by the dispatch packets' own start/end timestamps
+    // (hipExtLaunchKernelGGL events): the main phase from the start of its first kernel to the
+    // end of its last, and the merge kernel.
     hipEvent_t* ev = nullptr;
-    if (p->prof_n < p->prof_max) {
-        ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 3 * p->prof_n++;
-        (void)hipEventRecord(ev[0], st);
-    }
+    if (p->prof_n < p->prof_max) ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 4 * p->prof_n++;
     const int n_wg = static_cast<int>(p->wg_off.size()) - 1;
+    const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of 4
+    hipEvent_t main_start = ev ? ev[0] : nullptr, main_stop = ev ? ev[1] : nullptr;
     if (n_wg > 0)
-        hipLaunchKernelGGL(attn_persist<D>, dim3(static_cast<unsigned>(n_wg)), dim3(kThreads), 0, st, stages, wg_off,
-                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                           static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
-                           p->group, sl2);
+        hipExtLaunchKernelGGL(attn_persist<D>, dim3(static_cast<unsigned>(n_wg)), dim3(kThreads), 0, st, main_start,
+                              n_wave > 0 ? nullptr : main_stop, 0, stages, wg_off, static_cast<const uint16_t*>(q),
+                              static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                              static_cast<uint16_t*>(o), lse, po, plse, hq, hkv, p->group, sl2);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
-    const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of 4
     if (n_wave > 0)
-        hipLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / 4)), dim3(kThreads), 0, st,
-                           wdesc, woff, wtiles, static_cast<const uint16_t*>(q),
-                           static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                           static_cast<uint16_t*>(o), lse, po, plse, hq, hkv, p->group, sl2);
+        hipExtLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / 4)), dim3(kThreads), 0, st,
+                              n_wg > 0 ? nullptr : main_start, main_stop, 0, wdesc, woff, wtiles,
+                              static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                              static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
+                              p->group, sl2);
     e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
-    if (ev) (void)hipEventRecord(ev[1], st);
     if (!p->merges.empty()) {
-        hipLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(kThreads), 0, st,
-                           merges, po, plse, static_cast<uint16_t*>(o), lse, hq);
+        hipExtLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(kThreads), 0, st,
+                              ev ? ev[2] : nullptr, ev ? ev[3] : nullptr, 0, merges,
+                              static_cast<const float*>(po), static_cast<const float*>(plse),
+                              static_cast<uint16_t*>(o), lse, hq);
         e = hipGetLastError();
         if (e != hipSuccess) return set_error(TKV_EHIP, "merge launch: %s", hipGetErrorString(e));
+    } else if (ev) {
+        (void)hipEventRecord(ev[2], st);
+        (void)hipEventRecord(ev[3], st);
     }
-    if (ev) (void)hipEventRecord(ev[2], st);
     return TKV_OK;
 }
 
@@ -783,7 +789,7 @@ TKV_EXPORT int tkv_plan_profile(tkv_plan* p, int32_t max_calls) {
     tkv::clear_error();
     if (!p || max_calls < 0) return tkv::set_error(TKV_EINVAL, "tkv_plan_profile: bad argument");
     free_events(p);
-    for (int32_t i = 0; i < 3 * max_calls; ++i) {
+    for (int32_t i = 0; i < 4 * max_calls; ++i) {
         hipEvent_t e;
         const hipError_t rc = hipEventCreate(&e);
         if (rc != hipSuccess) {
@@ -801,11 +807,11 @@ TKV_EXPORT int tkv_plan_profile_read(tkv_plan* p, int32_t* n_calls, float* ms_ma
     if (!p || !n_calls || !ms_main || !ms_merge) return tkv::set_error(TKV_EINVAL, "tkv_plan_profile_read: NULL argument");
     float a = 0.f, b = 0.f;
     for (int32_t i = 0; i < p->prof_n; ++i) {
-        hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 3 * i;
-        hipError_t rc = hipEventSynchronize(ev[2]);
+        hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 4 * i;
+        hipError_t rc = hipEventSynchronize(ev[3]);
         float t0 = 0.f, t1 = 0.f;
         if (rc == hipSuccess) rc = hipEventElapsedTime(&t0, ev[0], ev[1]);
-        if (rc == hipSuccess) rc = hipEventElapsedTime(&t1, ev[1], ev[2]);
+        if (rc == hipSuccess) rc = hipEventElapsedTime(&t1, ev[2], ev[3]);
         if (rc != hipSuccess) return tkv::set_error(TKV_EHIP, "tkv_plan_profile_read: %s", hipGetErrorString(rc));
         a += t0;
         b += t1;

@@ -376,6 +376,8 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 }
             }
         }
+        st.n_items_wave = static_cast<int32_t>(p->wave_items.size());
+        st.n_waves = static_cast<int32_t>(p->wave_tiles.size());
         st.n_slots = p->n_slots;
         st.n_merge = static_cast<int32_t>(p->merges.size());
 
