@@ -158,7 +158,7 @@ def main():
             tr = json.load(f).get(a.workload)
         if tr and tr.get("sources_sha256") == kernel_sources_digest():
             traffic = tr.get("bytes_per_launch")
-    main_kernels = ([] if st["n_items"] == st["n_items_wave"] else ["attn_persist"]) + \
+    main_kernels = ([] if st["n_items"] == st["n_items_wave"] else ["attn_tile"]) + \
                    (["attn_wave"] if st["n_items_wave"] else [])
     # the bound is the one the work's arithmetic intensity puts it under (ridge: peak flop/s over
     # peak bytes/s); decode is HBM-bound, multi-token verify of long steps is MFMA-bound

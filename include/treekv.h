@@ -4,7 +4,7 @@
  *
  * The problem (SpecScale, arXiv 2609.39334): a beam search with a process reward model keeps a
  * tree of candidate reasoning paths (Sec. 2.2).  Speculation multiplies the live candidates and
- * the decode work (Sec. 3.2.1) and fragments verification (Sec. 3.2.2); computation
+ * the decode work and fragments verification (Sec. 3.2); computation
  * deduplication runs one forward pass per distinct prefix (Sec. 4.2); early pruning releases
  * losers (Sec. 4.1).  All candidates read one paged KV cache with prefix sharing (Sec. 5.1).
  * This library provides, for one attention layer:

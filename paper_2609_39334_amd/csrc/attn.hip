@@ -1,24 +1,27 @@
 // Tree-shared paged attention kernels for gfx950 (MI355X).
 //
-// attn_persist: persistent workgroups, each walking its list of work items (see plan.cpp).  An item is a tile of up to 64 query
-// rows -- query tokens x the G query heads of one KV head -- and an ordered list of KV blocks.
-// K/V blocks are staged through LDS four at a time (64 keys) and every wave contracts them
-// against its 16 query rows on bf16 MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulation):
-//   S^T = K Q^T   (A = 16 keys x 32 d from LDS, B = Q^T held in registers),
-//   O^T += V^T P^T (A = V^T from a transposed LDS copy, B = P^T straight from the S^T registers),
-// with an online softmax in between (exp2, scale folded into one FMA).  Computing the transposed
-// products keeps each lane's query row fixed across both contractions, so the running max, sum
-// and the O rescale never leave the lane.  Masking is per key: slots beyond a block's length are
-// never loaded (zero-filled in LDS) and keys past a token's causal limit get -inf.
+// Every kernel contracts a tile of query rows -- query tokens x the G query heads of one KV head --
+// against an ordered list of 16-token K/V blocks on bf16 MFMA with fp32 accumulation, computing the
+// transposed products so that each lane keeps one query row throughout:
+//   S^T = K Q^T     v_mfma_f32_16x16x32_bf16 (A = 16 keys x 32 dims, B = Q^T held in registers),
+//   O^T += V^T P^T  v_mfma_f32_16x16x16_bf16 (A = V^T read transposed from LDS with
+//                   ds_read_b64_tr_b16, B = P^T exactly as the S^T result sits in the lanes),
+// with an online softmax in between (exp2 with the scale folded into one FMA; O rescaled only when
+// a row's running max moves).  Keys past a block's length are never loaded (row reads are clamped
+// to the block's last token and masked) and keys past a token's causal limit get -inf.
 //
-// merge_partials: log-sum-exp merge of the per-segment partials of one query token (all heads):
-//   lse = log sum_j exp(lse_j),  o = sum_j exp(lse_j - lse) o_j.
+// attn_wave:  decode-shaped work (G <= 16): every wave is an independent worker walking its own
+//             list of items, each a tile of up to 48 rows over a chunk of <= 16 blocks, with the
+//             next block always in flight; no LDS sharing, no barriers.
+// attn_tile:  wide tiles (multi-token verify rows, G > 16): one workgroup of four waves per item,
+//             128 rows (32 per wave) against 64-key stages of K/V double-buffered through LDS.
+// merge_partials: log-sum-exp merge of the partial results of a query token's chunks:
+//             lse = log sum_j exp(lse_j),  o = sum_j exp(lse_j - lse) o_j.
+
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
-
 #include <cmath>
 #include <cstdint>
-
 #include "internal.h"
 
 namespace {
@@ -42,323 +45,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 constexpr int kThreads = 256;
-constexpr int kKeysPerStage = 64;  // four 16-token blocks
-
-// One stage as the kernel sees it after decoding its descriptor (scalar registers).
-struct StageInfo {
-    int len[4], pos[4];
-    int kvh, n_tok, flags;
-};
-
-// Lane l loads 16-byte word min(l & 7, 4) of the stage descriptor's header: lanes 0..3 hold
-// blocks[0..3] = {blk, len, pos, -} and lane 4 holds {kvh, n_tok, flags, -}, so a block's fields
-// come out with v_readlane at a (uniform) lane index -- no select chains, no branches.
-__device__ __forceinline__ int4 load_hdr(const tkv::StageDesc* __restrict__ stages, int gs, int lane) {
-    return reinterpret_cast<const int4*>(stages + gs)[min(lane & 7, 4)];
-}
-__device__ __forceinline__ int4 load_tok(const tkv::StageDesc* __restrict__ stages, int gs, int t) {
-    return reinterpret_cast<const int4*>(stages[gs].toks)[t];
-}
-
-__device__ __forceinline__ StageInfo decode_hdr(const int4& h) {
-    StageInfo si;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        si.len[j] = __builtin_amdgcn_readlane(h.y, j);
-        si.pos[j] = __builtin_amdgcn_readlane(h.z, j);
-    }
-    si.kvh = __builtin_amdgcn_readlane(h.x, 4);
-    si.n_tok = __builtin_amdgcn_readlane(h.y, 4);
-    si.flags = __builtin_amdgcn_readlane(h.z, 4);
-    return si;
-}
-
-// Registers of one stage owned by this thread: K in row layout, V as KPV consecutive keys x 8
-// dims (transposed into key-contiguous words on the way to LDS).
-template <int D>
-struct StageRegs {
-    static constexpr int DCH = D / 8;                          // 16-byte chunks per row
-    static constexpr int KPT = kKeysPerStage * DCH / kThreads;  // K chunks per thread
-    static constexpr int KPV = D == 128 ? 4 : 2;                // V keys per thread
-    u32x4_t k[KPT];
-    u32x4_t v[KPV];
-};
-
-// All loads are straight-line (so the compiler's wait counts stay exact and nothing drains the
-// prefetch early).  A thread's block is uniform across its wave, read from the header with
-// v_readlane; a slot past the block's length reads the block's last row (masked in the softmax,
-// so it contributes exactly 0); an absent block reads the stage's first block.  valid = false
-// turns every length to 0 (the fetch past the end of the stream reads one row per block).
-template <int D>
-__device__ __forceinline__ void stage_load(StageRegs<D>& r, const int4& h, bool valid, int kvh,
-                                           const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-                                           int hkv, int tid, int wave_u) {
-    constexpr int DCH = StageRegs<D>::DCH;
-#pragma unroll
-    for (int i = 0; i < StageRegs<D>::KPT; ++i) {
-        const int c = tid + kThreads * i;
-        const int dc = c % DCH, sl = (c / DCH) & 15;
-        const int j = D == 128 ? i : 2 * i + (wave_u >> 1);   // c / (16 * DCH), uniform per wave
-        const int id = __builtin_amdgcn_readlane(h.x, j);
-        const int len = valid ? __builtin_amdgcn_readlane(h.y, j) : 0;
-        const int se = min(sl, max(len - 1, 0));
-        const uint16_t* base = kpool + (static_cast<size_t>(id) * hkv + kvh) * (16 * D);
-        r.k[i] = *reinterpret_cast<const u32x4_t*>(base + se * D + dc * 8);
-    }
-    constexpr int KPV = StageRegs<D>::KPV;
-    const int id = __builtin_amdgcn_readlane(h.x, wave_u);   // this wave's V keys lie in block `wave`
-    const int len = valid ? __builtin_amdgcn_readlane(h.y, wave_u) : 0;
-    const uint16_t* base = vpool + (static_cast<size_t>(id) * hkv + kvh) * (16 * D);
-    const int kq = tid / DCH, dc = tid % DCH;   // keys KPV*kq .. +KPV-1 of the stage, dims 8dc..8dc+7
-#pragma unroll
-    for (int i = 0; i < KPV; ++i) {
-        const int sl = (KPV * kq + i) & 15;
-        const int se = min(sl, max(len - 1, 0));
-        r.v[i] = *reinterpret_cast<const u32x4_t*>(base + se * D + dc * 8);
-    }
-}
-
-template <int D, int KSTR, int VSTR>
-__device__ __forceinline__ void stage_store(const StageRegs<D>& r, uint16_t* Ks, uint16_t* Vt, int tid) {
-    constexpr int DCH = StageRegs<D>::DCH;
-#pragma unroll
-    for (int i = 0; i < StageRegs<D>::KPT; ++i) {
-        const int c = tid + kThreads * i;
-        const int dc = c % DCH, key = c / DCH;
-        *reinterpret_cast<u32x4_t*>(&Ks[key * KSTR + dc * 8]) = r.k[i];
-    }
-    const int kq = tid / DCH, dc = tid % DCH;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        // dim 8dc+e of consecutive keys -> bf16 pairs (key 2m in the low half)
-        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-        if constexpr (D == 128) {
-            uint2 out;
-            out.x = __builtin_amdgcn_perm(r.v[1][e >> 1], r.v[0][e >> 1], sel);
-            out.y = __builtin_amdgcn_perm(r.v[3][e >> 1], r.v[2][e >> 1], sel);
-            *reinterpret_cast<uint2*>(&Vt[(dc * 8 + e) * VSTR + 4 * kq]) = out;
-        } else {
-            *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + e) * VSTR + 2 * kq]) =
-                __builtin_amdgcn_perm(r.v[1][e >> 1], r.v[0][e >> 1], sel);
-        }
-    }
-}
-
-// Per-lane view of the current item's query row: lane (wave w, column c) owns tile row 16w + c,
-// i.e. query token t = row / G of the tile and head g = row % G of the item's KV head.
-template <int D>
-struct RowState {
-    int qtok, limit, slot, h;
-    bool row_ok, wave_active;
-    bf16x8_t qf[D / 32];  // this row's query, k-step ks holding dims 32ks + 8kg .. +7
-};
-
-// Rows of a stage's item from its decoded header and this lane's token entry (loaded a step
-// earlier, so the query loads below depend on nothing in flight).  A row past the tile reads
-// token 0's entry of the descriptor (zero-filled) and is never written.
-template <int D>
-__device__ __forceinline__ void make_rows(RowState<D>& rs, const StageInfo& si, const int4& tk,
-                                          const uint16_t* __restrict__ q, int hq, int G, int wave, int t, int g,
-                                          int kg) {
-    rs.row_ok = t < si.n_tok;
-    rs.wave_active = wave * 16 < si.n_tok * G;
-    rs.qtok = tk.x;
-    rs.limit = tk.y;
-    rs.slot = tk.z;
-    rs.h = si.kvh * G + g;
-    const uint16_t* qrow = q + (static_cast<size_t>(rs.qtok) * hq + rs.h) * D + kg * 8;
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) rs.qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
-}
-
-// Workgroup barrier that orders LDS only.  __syncthreads() also waits for every outstanding global
-// load (its release fence), which would drain the K/V prefetch at each stage.
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// Compute-side state of the current item.
-template <int D>
-struct Acc {
-    f32x4_t acc[D / 16];
-    float m_run, l_run;
-    __device__ __forceinline__ void reset() {
-#pragma unroll
-        for (int c = 0; c < D / 16; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        m_run = -INFINITY;
-        l_run = 0.f;
-    }
-};
-
-template <int D, int KSTR, int VSTR>
-__device__ __forceinline__ void contract_stage(Acc<D>& A, const RowState<D>& rs, const StageInfo& sb,
-                                               const uint16_t* Ks, const uint16_t* Vt, int col, int kg, float sl2) {
-    constexpr int NKS = D / 32, NCT = D / 16;
-    f32x4_t s[4];
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-        s[st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-            const uint4 a = *reinterpret_cast<const uint4*>(&Ks[(st * 16 + col) * KSTR + ks * 32 + kg * 8]);
-            s[st] = mfma_16x16x32(as_bf16x8(a), rs.qf[ks], s[st]);
-        }
-    }
-    // lane holds keys st*16 + 4*kg + r (r = 0..3) of its query row.  Masking is needed only when a
-    // block is partial or some row of the wave has a causal limit inside the stage (wave-uniform).
-    const bool row_full = sb.len[0] + sb.len[1] + sb.len[2] + sb.len[3] == 64 && rs.limit >= sb.pos[0] + 63;
-    if (__builtin_amdgcn_ballot_w64(!row_full) != 0) {
-#pragma unroll
-        for (int st = 0; st < 4; ++st) {
-            const int vlen = min(sb.len[st], rs.limit - sb.pos[st] + 1);  // visible slots of this block
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                if (4 * kg + r >= vlen) s[st][r] = -INFINITY;
-        }
-    }
-    float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                     fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-    mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[2][0], s[2][1]), fmaxf(s[2][2], s[2][3])),
-                         fmaxf(fmaxf(s[3][0], s[3][1]), fmaxf(s[3][2], s[3][3]))));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(A.m_run, mx);
-    // exp2(-inf) = 0, so masked keys need no select; a row with no visible key yet keeps msc = 0
-    const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
-    float psum = 0.f;
-#pragma unroll
-    for (int st = 0; st < 4; ++st)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            s[st][r] = __builtin_amdgcn_exp2f(fmaf(s[st][r], sl2, -msc));
-            psum += s[st][r];
-        }
-    const float alpha = m_new == A.m_run ? 1.f : __builtin_amdgcn_exp2f(A.m_run * sl2 - msc);
-    A.l_run = fmaf(A.l_run, alpha, psum);
-    A.m_run = m_new;
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {  // rescale only when some row's max grew
-#pragma unroll
-        for (int c = 0; c < NCT; ++c) A.acc[c] *= alpha;
-    }
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-        // k index e of this lane: keys 32kk + 4kg + e (e < 4) and 32kk + 16 + 4kg + (e - 4)
-        uint4 pu;
-        pu.x = pack_bf16x2(s[2 * kk][0], s[2 * kk][1]);
-        pu.y = pack_bf16x2(s[2 * kk][2], s[2 * kk][3]);
-        pu.z = pack_bf16x2(s[2 * kk + 1][0], s[2 * kk + 1][1]);
-        pu.w = pack_bf16x2(s[2 * kk + 1][2], s[2 * kk + 1][3]);
-        const bf16x8_t pf = as_bf16x8(pu);
-#pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) {
-            const uint16_t* vrow = &Vt[(ct * 16 + col) * VSTR + kk * 32 + kg * 4];
-            const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-            const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
-            A.acc[ct] = mfma_16x16x32(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pf, A.acc[ct]);
-        }
-    }
-}
-
-template <int D>
-__device__ __forceinline__ void write_item(const Acc<D>& A, const RowState<D>& rs, int kg, uint16_t* __restrict__ o,
-                                           float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse,
-                                           int hq, float sl2) {
-    constexpr int NCT = D / 16;
-    float l_tot = A.l_run + __shfl_xor(A.l_run, 16);
-    l_tot += __shfl_xor(l_tot, 32);
-    if (!rs.row_ok) return;
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float lse_v = l_tot > 0.f ? (A.m_run * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
-    // lane holds output columns ct*16 + 4*kg + r of its row
-    if (rs.slot < 0) {
-        uint16_t* orow = o + (static_cast<size_t>(rs.qtok) * hq + rs.h) * D;
-#pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) {
-            uint2 w;
-            w.x = pack_bf16x2(A.acc[ct][0] * inv, A.acc[ct][1] * inv);
-            w.y = pack_bf16x2(A.acc[ct][2] * inv, A.acc[ct][3] * inv);
-            *reinterpret_cast<uint2*>(orow + ct * 16 + kg * 4) = w;
-        }
-        if (lse && kg == 0) lse[static_cast<size_t>(rs.qtok) * hq + rs.h] = lse_v;
-    } else {
-        float* prow = po + (static_cast<size_t>(rs.slot) * hq + rs.h) * D;
-#pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
-            *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) =
-                make_float4(A.acc[ct][0] * inv, A.acc[ct][1] * inv, A.acc[ct][2] * inv, A.acc[ct][3] * inv);
-        if (kg == 0) plse[static_cast<size_t>(rs.slot) * hq + rs.h] = lse_v;
-    }
-}
-
-// One workgroup per resident slot (persistent): it walks the planner's stream of 64-key stages
-// for this slot (items split into stages, items back to back).  While stage k is contracted from
-// LDS, stage k+1's K/V and its item's query rows are in flight into registers, and stage k+2's
-// descriptor is in flight too -- every load of the loop body is straight-line and depends on
-// nothing issued in the same step.  At an item boundary the rows are swapped in by selects.
-template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 3))) void attn_persist(
-    const tkv::StageDesc* __restrict__ stages, const int32_t* __restrict__ wg_off, const uint16_t* __restrict__ q,
-    const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
-    float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
-    constexpr int KSTR = D + 8;                // K row stride in LDS (elements): 16-B reads spread over banks
-    constexpr int VSTR = kKeysPerStage + 4;    // V^T row stride (elements): 8-B reads of 16 rows spread over banks
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeysPerStage * KSTR];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VSTR];
-
-    const int s0 = wg_off[blockIdx.x], s1 = wg_off[blockIdx.x + 1];
-    if (s0 >= s1) return;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    const int col = lane & 15, kg = lane >> 4;
-    const int mrow = wave * 16 + col;  // this lane's row of the tile (token-major, head-minor)
-    const int t = mrow / G, g = mrow - t * G;
-    const int trow = min(t, tkv::kTileRows - 1);
-
-    int4 h = load_hdr(stages, s0, lane);
-    int4 tk = load_tok(stages, s0, trow);
-    StageInfo si = decode_hdr(h);
-    StageRegs<D> r;
-    stage_load<D>(r, h, true, si.kvh, kpool, vpool, hkv, tid, wave_u);
-    RowState<D> rs, rs_n;
-    make_rows<D>(rs, si, tk, q, hq, G, wave, t, g, kg);
-    int gnext = s0 + 1;  // next stage to fetch
-    h = load_hdr(stages, min(gnext, s1 - 1), lane);
-    tk = load_tok(stages, min(gnext, s1 - 1), trow);
-    Acc<D> A;
-    A.reset();
-
-    for (;;) {
-        const StageInfo cur = si;
-        lds_barrier();  // the previous stage's LDS reads are done
-        stage_store<D, KSTR, VSTR>(r, Ks, Vt, tid);
-        lds_barrier();
-        const bool has_next = gnext < s1;
-        si = decode_hdr(h);
-        make_rows<D>(rs_n, si, tk, q, hq, G, wave, t, g, kg);
-        stage_load<D>(r, h, has_next, si.kvh, kpool, vpool, hkv, tid, wave_u);
-        ++gnext;
-        h = load_hdr(stages, min(gnext, s1 - 1), lane);
-        tk = load_tok(stages, min(gnext, s1 - 1), trow);
-        if (__builtin_amdgcn_readfirstlane(rs.wave_active))
-            contract_stage<D, KSTR, VSTR>(A, rs, cur, Ks, Vt, col, kg, sl2);
-        const bool last = cur.flags & tkv::kStageLast;
-        if (last) {
-            write_item<D>(A, rs, kg, o, lse, po, plse, hq, sl2);
-            if (!has_next) break;
-            A.reset();
-        }
-        rs.qtok = last ? rs_n.qtok : rs.qtok;
-        rs.limit = last ? rs_n.limit : rs.limit;
-        rs.slot = last ? rs_n.slot : rs.slot;
-        rs.h = last ? rs_n.h : rs.h;
-        rs.row_ok = last ? rs_n.row_ok : rs.row_ok;
-        rs.wave_active = last ? rs_n.wave_active : rs.wave_active;
-#pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) rs.qf[ks] = last ? rs_n.qf[ks] : rs.qf[ks];
-    }
-}
 
 // ============================================================================ wave-private kernel
 // For tiles of at most 16 query rows (decode rows: the G heads of a few tokens) every wave is an
@@ -425,6 +111,118 @@ struct WaveAcc {
     }
 };
 
+// Online-softmax update of T column tiles with one 16-key block of scores (lane holds keys
+// 4kg + x of its row): mask keys past the block's length or the row's causal limit, fold the block
+// into the running max / sum, rescale O when a row's max moved, and pack P^T as bf16 for the PV MFMA.
+template <int D, int T>
+__device__ __forceinline__ void softmax_step(WaveAcc<D, T>& A, f32x4_t (&s)[T], int len, int pos,
+                                             const int (&limit)[T], int kg, float sl2, s16x4_t (&pb)[T]) {
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        // mask only partial blocks and rows with a causal limit inside the block
+        if (__builtin_amdgcn_ballot_w64(!(len == 16 && limit[tt] >= pos + 15)) != 0) {
+            const int vlen = min(len, limit[tt] - pos + 1);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                if (4 * kg + x >= vlen) s[tt][x] = -INFINITY;
+        }
+        const float mx = rowmax4(fmaxf(fmaxf(s[tt][0], s[tt][1]), fmaxf(s[tt][2], s[tt][3])));
+        const float m_new = fmaxf(A.m[tt], mx);
+        const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
+        float psum = 0.f;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            s[tt][x] = __builtin_amdgcn_exp2f(fmaf(s[tt][x], sl2, -msc));
+            psum += s[tt][x];
+        }
+        const float alpha = m_new == A.m[tt] ? 1.f : __builtin_amdgcn_exp2f(A.m[tt] * sl2 - msc);
+        A.l[tt] = fmaf(A.l[tt], alpha, psum);
+        A.m[tt] = m_new;
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) A.acc[tt][c] *= alpha;
+        }
+        pb[tt] = __builtin_bit_cast(s16x4_t, uint2{pack_bf16x2(s[tt][0], s[tt][1]), pack_bf16x2(s[tt][2], s[tt][3])});
+    }
+}
+
+// The same update for a pair of 16-key blocks (A then B) folded in as one 32-key step; P^T comes
+// out as the B operand of v_mfma_f32_16x16x32_bf16 with k = 8kg + e holding key 4kg + e of block A
+// (e < 4) and key 4kg + e - 4 of block B (e >= 4) -- the order of the V^T operand built from the
+// two blocks' transposed LDS reads.
+template <int D, int T>
+__device__ __forceinline__ void softmax_pair(WaveAcc<D, T>& A, f32x4_t (&sa)[T], f32x4_t (&sb)[T], int len_a,
+                                             int pos_a, int len_b, int pos_b, const int (&limit)[T], int kg,
+                                             float sl2, bf16x8_t (&pb)[T]) {
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        if (__builtin_amdgcn_ballot_w64(!(len_a == 16 && limit[tt] >= pos_a + 15)) != 0) {
+            const int vlen = min(len_a, limit[tt] - pos_a + 1);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                if (4 * kg + x >= vlen) sa[tt][x] = -INFINITY;
+        }
+        if (__builtin_amdgcn_ballot_w64(!(len_b == 16 && limit[tt] >= pos_b + 15)) != 0) {
+            const int vlen = min(len_b, limit[tt] - pos_b + 1);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                if (4 * kg + x >= vlen) sb[tt][x] = -INFINITY;
+        }
+        const float mx = rowmax4(fmaxf(fmaxf(fmaxf(sa[tt][0], sa[tt][1]), fmaxf(sa[tt][2], sa[tt][3])),
+                                       fmaxf(fmaxf(sb[tt][0], sb[tt][1]), fmaxf(sb[tt][2], sb[tt][3]))));
+        const float m_new = fmaxf(A.m[tt], mx);
+        const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
+        float psum = 0.f;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            sa[tt][x] = __builtin_amdgcn_exp2f(fmaf(sa[tt][x], sl2, -msc));
+            sb[tt][x] = __builtin_amdgcn_exp2f(fmaf(sb[tt][x], sl2, -msc));
+            psum += sa[tt][x] + sb[tt][x];
+        }
+        const float alpha = m_new == A.m[tt] ? 1.f : __builtin_amdgcn_exp2f(A.m[tt] * sl2 - msc);
+        A.l[tt] = fmaf(A.l[tt], alpha, psum);
+        A.m[tt] = m_new;
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) A.acc[tt][c] *= alpha;
+        }
+        pb[tt] = __builtin_bit_cast(bf16x8_t, uint4{pack_bf16x2(sa[tt][0], sa[tt][1]), pack_bf16x2(sa[tt][2], sa[tt][3]),
+                                                    pack_bf16x2(sb[tt][0], sb[tt][1]), pack_bf16x2(sb[tt][2], sb[tt][3])});
+    }
+}
+
+// Normalise one column tile's rows and write them: the final bf16 output and lse (slot < 0) or an
+// fp32 partial and its lse.  Lane holds columns 16ct + 4kg + r of its row; l is summed over the
+// four lanes of the row.
+template <int D>
+__device__ __forceinline__ void write_rows(const f32x4_t (&acc)[D / 16], float m, float l, bool ok, int qtok, int h,
+                                           int slot, int kg, uint16_t* __restrict__ o, float* __restrict__ lse,
+                                           float* __restrict__ po, float* __restrict__ plse, int hq, float sl2) {
+    float l_tot = l + __shfl_xor(l, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (!ok) return;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float lse_v = l_tot > 0.f ? (m * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
+    if (slot < 0) {
+        uint16_t* orow = o + (static_cast<size_t>(qtok) * hq + h) * D;
+#pragma unroll
+        for (int ct = 0; ct < D / 16; ++ct) {
+            uint2 wv;
+            wv.x = pack_bf16x2(acc[ct][0] * inv, acc[ct][1] * inv);
+            wv.y = pack_bf16x2(acc[ct][2] * inv, acc[ct][3] * inv);
+            *reinterpret_cast<uint2*>(orow + ct * 16 + kg * 4) = wv;
+        }
+        if (lse && kg == 0) lse[static_cast<size_t>(qtok) * hq + h] = lse_v;
+    } else {
+        float* prow = po + (static_cast<size_t>(slot) * hq + h) * D;
+#pragma unroll
+        for (int ct = 0; ct < D / 16; ++ct)
+            *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) =
+                make_float4(acc[ct][0] * inv, acc[ct][1] * inv, acc[ct][2] * inv, acc[ct][3] * inv);
+        if (kg == 0) plse[static_cast<size_t>(slot) * hq + h] = lse_v;
+    }
+}
+
 // The item fields a wave needs, decoded from its descriptor (see tkv::WaveDesc): uniform values
 // by v_readlane, this lane's token of each tile by ds_bpermute from the token lanes.
 template <int T>
@@ -481,33 +279,7 @@ __device__ __forceinline__ void wave_block(WaveAcc<D, T>& A, BlockRegs<D>& r, co
         for (int tt = 0; tt < T; ++tt) s[tt] = mfma_16x16x32(__builtin_bit_cast(bf16x8_t, r.k[ks]), qf[tt][ks], s[tt]);
     load_k<D>(r, kpool, boff_n, len_n, lane);
     s16x4_t pb[T];
-#pragma unroll
-    for (int tt = 0; tt < T; ++tt) {
-        // lane holds keys 4kg + e of its row; mask only partial blocks and rows with a causal limit inside
-        if (__builtin_amdgcn_ballot_w64(!(len == 16 && limit[tt] >= pos + 15)) != 0) {
-            const int vlen = min(len, limit[tt] - pos + 1);
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
-                if (4 * kg + x >= vlen) s[tt][x] = -INFINITY;
-        }
-        const float mx = rowmax4(fmaxf(fmaxf(s[tt][0], s[tt][1]), fmaxf(s[tt][2], s[tt][3])));
-        const float m_new = fmaxf(A.m[tt], mx);
-        const float msc = m_new == -INFINITY ? 0.f : m_new * sl2;
-        float psum = 0.f;
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-            s[tt][x] = __builtin_amdgcn_exp2f(fmaf(s[tt][x], sl2, -msc));
-            psum += s[tt][x];
-        }
-        const float alpha = m_new == A.m[tt] ? 1.f : __builtin_amdgcn_exp2f(A.m[tt] * sl2 - msc);
-        A.l[tt] = fmaf(A.l[tt], alpha, psum);
-        A.m[tt] = m_new;
-        if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
-#pragma unroll
-            for (int c = 0; c < D / 16; ++c) A.acc[tt][c] *= alpha;
-        }
-        pb[tt] = __builtin_bit_cast(s16x4_t, uint2{pack_bf16x2(s[tt][0], s[tt][1]), pack_bf16x2(s[tt][2], s[tt][3])});
-    }
+    softmax_step<D, T>(A, s, len, pos, limit, kg, sl2, pb);
     // V rows into this wave's LDS region, then the V registers take the next loads
 #pragma unroll
     for (int i = 0; i < D / 32; ++i) {
@@ -582,32 +354,9 @@ __device__ __forceinline__ void wave_run(const int4* __restrict__ wdesc, int e0,
         }
         // normalise and write each tile's final output or partial
 #pragma unroll
-        for (int tt = 0; tt < T; ++tt) {
-            float l_tot = A.l[tt] + __shfl_xor(A.l[tt], 16);
-            l_tot += __shfl_xor(l_tot, 32);
-            if (!ic.ok[tt]) continue;
-            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-            const float lse_v = l_tot > 0.f ? (A.m[tt] * sl2 + log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
-            if (ic.slot[tt] < 0) {
-                uint16_t* orow = o + (static_cast<size_t>(ic.qtok[tt]) * hq + ic.h[tt]) * D;
-#pragma unroll
-                for (int ct = 0; ct < D / 16; ++ct) {
-                    uint2 wv;
-                    wv.x = pack_bf16x2(A.acc[tt][ct][0] * inv, A.acc[tt][ct][1] * inv);
-                    wv.y = pack_bf16x2(A.acc[tt][ct][2] * inv, A.acc[tt][ct][3] * inv);
-                    *reinterpret_cast<uint2*>(orow + ct * 16 + kg * 4) = wv;
-                }
-                if (lse && kg == 0) lse[static_cast<size_t>(ic.qtok[tt]) * hq + ic.h[tt]] = lse_v;
-            } else {
-                float* prow = po + (static_cast<size_t>(ic.slot[tt]) * hq + ic.h[tt]) * D;
-#pragma unroll
-                for (int ct = 0; ct < D / 16; ++ct)
-                    *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) =
-                        make_float4(A.acc[tt][ct][0] * inv, A.acc[tt][ct][1] * inv, A.acc[tt][ct][2] * inv,
-                                    A.acc[tt][ct][3] * inv);
-                if (kg == 0) plse[static_cast<size_t>(ic.slot[tt]) * hq + ic.h[tt]] = lse_v;
-            }
-        }
+        for (int tt = 0; tt < T; ++tt)
+            write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], ic.ok[tt], ic.qtok[tt], ic.h[tt], ic.slot[tt], kg, o, lse, po,
+                          plse, hq, sl2);
         if (!more) break;
         dc = dn;
         dn = wdesc[static_cast<size_t>(min(e + 2, e1 - 1)) * 64 + lane];
@@ -638,6 +387,172 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     else
         wave_run<D, 3>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
 }
+
+// ============================================================================ tile kernel
+constexpr int kTileRowsWG = 128;  // query rows of an attn_tile item (4 waves x 2 column tiles x 16)
+
+// One 64-key stage (4 blocks) of K/V, each wave fetching one block: lane l reads 16 bytes of rows
+// 4i + l/16 (clamped to the block's last token), so each load instruction covers 1 KB of the
+// block contiguously.
+template <int D>
+struct StageRegs {
+    u32x4_t k[D / 32], v[D / 32];
+};
+
+template <int D>
+__device__ __forceinline__ void stage_load(StageRegs<D>& r, const uint16_t* __restrict__ kpool,
+                                           const uint16_t* __restrict__ vpool, size_t boff, int len, int lane) {
+    constexpr int RPI = 64 * 8 / D;  // rows per load instruction (16 bytes per lane)
+    const int last = max(len - 1, 0);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+        const int row = min(i * RPI + lane / (D / 8), last);
+        const size_t off = boff + static_cast<size_t>(row) * D + (lane % (D / 8)) * 8;
+        r.k[i] = *reinterpret_cast<const u32x4_t*>(kpool + off);
+        r.v[i] = *reinterpret_cast<const u32x4_t*>(vpool + off);
+    }
+}
+
+template <int D, int KSTR, int VROW>
+__device__ __forceinline__ void stage_store(const StageRegs<D>& r, uint16_t* ks, uint8_t* vs, int wave, int lane) {
+    constexpr int RPI = 64 * 8 / D;
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+        const int row = 16 * wave + i * RPI + lane / (D / 8);
+        const int col = (lane % (D / 8)) * 8;
+        *reinterpret_cast<u32x4_t*>(ks + row * KSTR + col) = r.k[i];
+        *reinterpret_cast<u32x4_t*>(vs + row * VROW + col * 2) = r.v[i];
+    }
+}
+
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// One workgroup per item: a tile of up to 128 query rows (wave w owns rows 32w .. 32w+31 as two
+// column tiles) against the item's key blocks, four blocks per stage.  Stage s+1 is fetched into
+// registers while stage s is contracted from LDS; one barrier per stage (the two LDS buffers
+// alternate, so a buffer is rewritten only after every wave has passed the barrier that follows
+// its last use).
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_tile(
+    const tkv::ItemDesc* __restrict__ items, const tkv::TokDesc* __restrict__ toks,
+    const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
+    float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
+    constexpr int T = 2;
+    constexpr int KSTR = D + 8;       // K row stride (elements): 16-byte reads of 16 rows hit distinct banks
+    constexpr int VROW = 2 * D + 32;  // V row stride (bytes): transposed 8-byte reads spread over the banks
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][64 * KSTR];
+    __shared__ __attribute__((aligned(16))) uint8_t Vs[2][64 * VROW];
+    const tkv::ItemDesc it = items[blockIdx.x];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, kg = lane >> 4;
+    const size_t blk_stride = static_cast<size_t>(hkv) * (16 * D);
+    const size_t kvh_off = static_cast<size_t>(it.kvh) * (16 * D);
+    const int2* bd = reinterpret_cast<const int2*>(blks + it.blk_off);
+    const int nb = it.n_blk;
+    const int n_stages = (nb + 3) / 4;
+
+    // this lane's query row of each column tile
+    bf16x8_t qf[T][D / 32];
+    int limit[T], qtok[T], slot[T], h[T];
+    bool ok[T];
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        const int row = 32 * wave + 16 * tt + col;
+        const int t = row / G;
+        ok[tt] = t < it.n_tok;
+        const tkv::TokDesc td = toks[it.tok_off + min(t, it.n_tok - 1)];
+        qtok[tt] = td.qtok;
+        limit[tt] = ok[tt] ? td.limit : -1;
+        slot[tt] = td.slot;
+        h[tt] = it.kvh * G + (row - t * G);
+        const uint16_t* qrow = q + (static_cast<size_t>(qtok[tt]) * hq + h[tt]) * D + kg * 8;
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) qf[tt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
+    }
+    const bool wave_active = __builtin_amdgcn_ballot_w64(ok[0] || ok[1]) != 0;
+
+    // block descriptors of a stage: lane l holds block 4s + (l & 3) (the item's last block past its end)
+    auto stage_desc = [&](int st) { return bd[min(4 * st + (lane & 3), nb - 1)]; };
+    int2 dcur = stage_desc(0), dnxt = stage_desc(1);
+    StageRegs<D> r;
+    {
+        const int len = 4 * 0 + wave < nb ? __builtin_amdgcn_readlane(dcur.y, wave) : 0;
+        stage_load<D>(r, kpool, vpool, static_cast<size_t>(__builtin_amdgcn_readlane(dcur.x, wave)) * blk_stride + kvh_off,
+                      len, lane);
+    }
+    WaveAcc<D, T> A;
+    A.reset();
+    int pos = it.pos0;
+    for (int st = 0; st < n_stages; ++st) {
+        const int buf = st & 1;
+        uint16_t* ks = Ks[buf];
+        uint8_t* vs = Vs[buf];
+        stage_store<D, KSTR, VROW>(r, ks, vs, wave, lane);
+        lds_barrier();
+        // fetch the next stage while this one is contracted
+        {
+            const int bn = 4 * (st + 1) + wave;
+            const int len = bn < nb ? __builtin_amdgcn_readlane(dnxt.y, wave) : 0;
+            stage_load<D>(r, kpool, vpool,
+                          static_cast<size_t>(__builtin_amdgcn_readlane(dnxt.x, wave)) * blk_stride + kvh_off, len, lane);
+        }
+        const int2 dthis = dcur;
+        dcur = dnxt;
+        dnxt = stage_desc(st + 2);
+        if (!wave_active) continue;
+#pragma unroll
+        for (int jp = 0; jp < 2; ++jp) {
+            const int ja = 2 * jp, jb = 2 * jp + 1;
+            const int len_a = 4 * st + ja < nb ? __builtin_amdgcn_readlane(dthis.y, ja) : 0;
+            const int len_b = 4 * st + jb < nb ? __builtin_amdgcn_readlane(dthis.y, jb) : 0;
+            const int pos_a = pos, pos_b = pos + len_a;
+            pos = pos_b + len_b;
+            // skip a pair that no row of this wave may see (past every causal limit, or absent)
+            if (len_a == 0 || __builtin_amdgcn_ballot_w64(limit[0] >= pos_a || limit[1] >= pos_a) == 0) continue;
+            f32x4_t sa[T], sb[T];
+#pragma unroll
+            for (int tt = 0; tt < T; ++tt) {
+                sa[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                sb[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int kk = 0; kk < D / 32; ++kk) {
+                const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(ks + (16 * ja + col) * KSTR + 32 * kk + 8 * kg);
+                const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(ks + (16 * jb + col) * KSTR + 32 * kk + 8 * kg);
+#pragma unroll
+                for (int tt = 0; tt < T; ++tt) {
+                    sa[tt] = mfma_16x16x32(ka, qf[tt][kk], sa[tt]);
+                    sb[tt] = mfma_16x16x32(kb, qf[tt][kk], sb[tt]);
+                }
+            }
+            bf16x8_t pb[T];
+            softmax_pair<D, T>(A, sa, sb, len_a, pos_a, len_b, pos_b, limit, kg, sl2, pb);
+            const uint8_t* vra = vs + (16 * ja + 4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
+            const uint8_t* vrb = vra + 16 * VROW;
+#pragma unroll
+            for (int ct = 0; ct < D / 16; ++ct) {
+                const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vra + ct * 32)));
+                const s16x4_t vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vrb + ct * 32)));
+                const bf16x8_t vab = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                for (int tt = 0; tt < T; ++tt) A.acc[tt][ct] = mfma_16x16x32(vab, pb[tt], A.acc[tt][ct]);
+            }
+        }
+    }
+    if (!wave_active) return;
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt)
+        write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], ok[tt], qtok[tt], h[tt], slot[tt], kg, o, lse, po, plse, hq, sl2);
+}
+
 
 // Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
 // are contiguous): every thread owns float4 columns of one head and folds the partials in with an
@@ -718,8 +633,7 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
                     hipStream_t st) {
     uint8_t* ws = static_cast<uint8_t*>(p->d_ws);
     const auto* merges = reinterpret_cast<const MergeDesc*>(ws + p->off_merges);
-    const auto* wg_off = reinterpret_cast<const int32_t*>(ws + p->off_wg);
-    const auto* stages = reinterpret_cast<const StageDesc*>(ws + p->off_stages);
+    const auto* items = reinterpret_cast<const ItemDesc*>(ws + p->off_items);
     const auto* wdesc = reinterpret_cast<const int4*>(ws + p->off_wdesc);
     const auto* woff = reinterpret_cast<const int32_t*>(ws + p->off_woff);
     const auto* wtiles = reinterpret_cast<const int32_t*>(ws + p->off_wtiles);
@@ -734,19 +648,19 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     // end of its last, and the merge kernel.
     hipEvent_t* ev = nullptr;
     if (p->prof_n < p->prof_max) ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 4 * p->prof_n++;
-    const int n_wg = static_cast<int>(p->wg_off.size()) - 1;
+    const int n_tile = static_cast<int>(p->items.size());
     const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of 4
     hipEvent_t main_start = ev ? ev[0] : nullptr, main_stop = ev ? ev[1] : nullptr;
-    if (n_wg > 0)
-        hipExtLaunchKernelGGL(attn_persist<D>, dim3(static_cast<unsigned>(n_wg)), dim3(kThreads), 0, st, main_start,
-                              n_wave > 0 ? nullptr : main_stop, 0, stages, wg_off, static_cast<const uint16_t*>(q),
+    if (n_tile > 0)
+        hipExtLaunchKernelGGL(attn_tile<D>, dim3(static_cast<unsigned>(n_tile)), dim3(kThreads), 0, st, main_start,
+                              n_wave > 0 ? nullptr : main_stop, 0, items, toks, blks, static_cast<const uint16_t*>(q),
                               static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                               static_cast<uint16_t*>(o), lse, po, plse, hq, hkv, p->group, sl2);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
     if (n_wave > 0)
         hipExtLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / 4)), dim3(kThreads), 0, st,
-                              n_wg > 0 ? nullptr : main_start, main_stop, 0, wdesc, woff, wtiles,
+                              n_tile > 0 ? nullptr : main_start, main_stop, 0, wdesc, woff, wtiles,
                               static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                               static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
                               p->group, sl2);

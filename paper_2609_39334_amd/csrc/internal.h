@@ -19,8 +19,8 @@ void clear_error();
 
 // ------------------------------------------------------------------ device descriptors
 constexpr int kBlock = 16;     // tokens per KV block
-constexpr int kTileRows = 64;  // query rows (token x head) per work item
-constexpr int kPersistentWGs = 768;  // resident workgroups of the attention kernel (3 per CU on 256 CUs)
+constexpr int kTileRows = 64;     // rows (q_len x G) from which a row is verified whole, not through segments
+constexpr int kTileRowsWG = 128;  // query rows of a workgroup-kernel tile (4 waves x 2 column tiles x 16)
 constexpr int kItemShared = 0;  // tile of several rows' tokens over one segment chunk (workgroup kernel)
 constexpr int kItemRow = 1;     // tile of one row's tokens over its whole path (workgroup kernel)
 constexpr int kItemWave = 2;    // tile of <= 16 T rows over one segment chunk (wave kernel)
@@ -30,13 +30,13 @@ constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
 constexpr int kWaveToks = 48;   // query tokens of a wave-kernel item (16 kWaveMaxTiles / G)
 constexpr int kWaveWorkers = 2048;  // waves of the wave kernel (each streams a list of items)
 
-// One work item = one workgroup: a tile of query tokens (each with all G query heads of one KV
+// One work item: a tile of query tokens (each with all G query heads of one KV
 // head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the
 // keys at positions <= its `limit`; keys are numbered along the path starting at `pos0`.
 struct ItemDesc {
     int32_t kvh;      // KV head
     int32_t tok_off;  // first TokDesc of the tile
-    int32_t n_tok;    // query tokens in the tile (n_tok * G <= kTileRows)
+    int32_t n_tok;    // query tokens in the tile (n_tok * G <= kTileRowsWG, or <= 16 tiles for the wave kernel)
     int32_t blk_off;  // first BlkDesc of the key list
     int32_t n_blk;    // blocks in the key list
     int32_t pos0;     // path position of the first key
@@ -55,25 +55,6 @@ struct BlkDesc {
     int32_t blk;  // pool block id
     int32_t len;  // tokens in the block (1..16)
 };
-
-// One 64-key stage of a persistent workgroup's stream.  The planner lays out each workgroup's
-// stages contiguously; the kernel loads a stage's descriptor one step before it fetches the
-// stage's K/V, so every address it needs (blocks and the query rows of the tile) is at hand
-// without a dependent load.  Lane l of a wave reads 16 bytes: blocks[l] (l < 4) or the item
-// fields (l == 4) into the header registers, and toks[row token] into its row registers.
-struct StageBlock {
-    int32_t blk;  // pool block id (block 0 of the stage where the stage has fewer blocks)
-    int32_t len;  // tokens in the block (0 = absent)
-    int32_t pos;  // path position of the block's first key
-    int32_t pad;
-};
-struct StageDesc {
-    StageBlock blocks[4];
-    int32_t kvh, n_tok, flags, pad;  // the item's KV head, tile size, kStageFirst | kStageLast
-    TokDesc toks[kTileRows];         // the item's tile tokens (n_tok used)
-};
-constexpr int kStageFirst = 1;
-constexpr int kStageLast = 2;
 
 // A wave-kernel item as one 1-KB record that a wave loads with one 16-byte load per lane (lane l
 // gets e[l]); block fields come out with v_readlane, token fields with ds_bpermute.
@@ -107,14 +88,12 @@ struct tkv_plan {
     std::vector<tkv::BlkDesc> blks;
     std::vector<tkv::MergeDesc> merges;
     std::vector<int32_t> merge_slots;
-    std::vector<int32_t> wg_off;              // [n_wg + 1] each persistent workgroup's range in stages
-    std::vector<tkv::StageDesc> stages;       // per workgroup, in processing order
     std::vector<tkv::WaveDesc> wave_desc;     // wave-kernel items, each wave's list contiguous
     std::vector<int32_t> wave_off;            // [n_waves + 1] each wave's range in wave_desc
     std::vector<int32_t> wave_tiles;          // [n_waves] column tiles of every item of the wave
     int32_t n_slots = 0;
     // workspace layout (byte offsets)
-    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wg = 0, off_stages = 0, off_wdesc = 0, off_woff = 0, off_wtiles = 0;
+    size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wdesc = 0, off_woff = 0, off_wtiles = 0;
     size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;
     std::vector<uint8_t> image;  // host copy of the descriptor region
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)

@@ -1,4 +1,4 @@
-// Planner: per-row block tables -> shared segments -> device work list.
+// Planner: per-row block tables -> shared segments -> device work lists.
 //
 // The paper's lever (computation deduplication, Sec. 4.2, over prefix-shared paged KV, Sec. 5.1)
 // is that many candidates reference the same prompt and step blocks.  The planner finds those
@@ -7,18 +7,20 @@
 //  * shared items, for rows whose query tile is small (q_len * G < kTileRows: decode rows and
 //    short verify rows).  A segment is a maximal run of trie nodes passed by the same set of rows;
 //    each segment (split into chunks of <= kChunkBlocks blocks) becomes items whose tile holds the
-//    query tokens of *every* row that references it, so each shared K/V block is staged once per
+//    query tokens of *every* row that references it, so each shared K/V block is read once per
 //    tile and contracted against all of them.  Each (token, chunk) result is a partial (o, lse)
 //    that a log-sum-exp merge combines -- unless the chunk is the token's only one, in which case
-//    the item writes the final output.
+//    the item writes the final output.  With G <= 16 these items go to the wave kernel (tiles of
+//    up to 48 rows, per-wave work lists built here); otherwise to the workgroup kernel.
 //  * row items, for rows whose own query tokens fill a tile (verify rows with q_len * G >=
-//    kTileRows).  A tile of one row's tokens walks the row's whole path (truncated at the tile's
-//    causal limit) and writes the final output; shared context blocks are then re-read from L2 by
-//    the tiles of other rows instead of being merged through HBM partials.
+//    kTileRows).  A workgroup-kernel tile of one row's tokens (128 rows) walks the row's whole
+//    path, truncated at the tile's largest causal limit, and writes the final output; the shared
+//    context blocks are re-read from L2 by the tiles of the other rows, which the launch order
+//    keeps on the same XCD.
 //
 // Positions: key j of a row is the j-th token along its path; token i of a row with q_len L and
-// kv_len N sees positions <= N - L + i (bottom-right causal, the prefill-only verification pass of
-// Sec. 3.2.2; decode is L = 1).  A shared segment sits at the same positions in every row through
+// kv_len N sees positions <= N - L + i (bottom-right causal, the single-pass verification of
+// Sec. 3.2; decode is L = 1).  A shared segment sits at the same positions in every row through
 // it, so one per-token limit suffices.
 #include <algorithm>
 #include <cstdlib>
@@ -121,7 +123,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         tkv_plan_stats& st = p->stats;
         st.n_rows = n_rows;
         st.n_qtok = n_rows ? q_indptr[n_rows] : 0;
-        const int32_t tpt = tkv::kTileRows / G;  // query tokens per tile
+        const int32_t tpt = tkv::kTileRowsWG / G;  // query tokens per workgroup-kernel tile
 
         // ------------------------------------------------------------ accounting
         {
@@ -381,55 +383,63 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         st.n_slots = p->n_slots;
         st.n_merge = static_cast<int32_t>(p->merges.size());
 
-        // Longest items first, then longest-processing-time assignment to the persistent
-        // workgroups: each item goes to the least-loaded workgroup (cost = key blocks + a fixed
-        // per-item overhead), so every workgroup streams about the same number of bytes.
-        std::stable_sort(p->items.begin(), p->items.end(),
-                         [](const ItemDesc& a, const ItemDesc& b) { return a.n_blk > b.n_blk; });
+        // Tile items run one workgroup each, dispatched in launch order with workgroup i on XCD
+        // i % 8.  Items that read the same keys -- the same first block and KV head (a row's path
+        // root, or a shared chunk) -- go to one XCD so that their repeated reads hit its L2.  Groups
+        // are assigned to XCDs longest processing time first (cost = key blocks x active waves);
+        // each XCD's list runs longest first and the lists are interleaved into the launch order.
         {
-            const int32_t n_items = static_cast<int32_t>(p->items.size());
-            int32_t target = tkv::kPersistentWGs;
-            if (const char* env = std::getenv("TKV_PERSISTENT_WGS")) target = std::max(1, std::atoi(env));
-            const int32_t n_wg = std::min<int32_t>(target, n_items);
-            std::vector<std::vector<int32_t>> lists(n_wg);
-            using Load = std::pair<int64_t, int32_t>;
-            std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-            for (int32_t w = 0; w < n_wg; ++w) heap.push({0, w});
-            for (int32_t i = 0; i < n_items; ++i) {
-                Load l = heap.top();
-                heap.pop();
-                lists[l.second].push_back(i);
-                l.first += p->items[i].n_blk + 2;
-                heap.push(l);
-            }
-            p->wg_off.assign(1, 0);
-            for (int32_t w = 0; w < n_wg; ++w) {
-                for (int32_t i : lists[w]) {
-                    const ItemDesc& it = p->items[i];
-                    int32_t pos = it.pos0;
-                    for (int32_t b0 = 0; b0 < it.n_blk; b0 += 4) {
-                        tkv::StageDesc sd{};
-                        for (int32_t j = 0; j < 4; ++j) {
-                            sd.blocks[j].pos = pos;
-                            if (b0 + j < it.n_blk) {
-                                const BlkDesc& bd = p->blks[it.blk_off + b0 + j];
-                                sd.blocks[j].blk = bd.blk;
-                                sd.blocks[j].len = bd.len;
-                                pos += bd.len;
-                            } else {
-                                sd.blocks[j].blk = sd.blocks[0].blk;  // read in place of the missing block, then masked
-                                sd.blocks[j].len = 0;
-                            }
-                        }
-                        sd.kvh = it.kvh;
-                        sd.n_tok = it.n_tok;
-                        sd.flags = (b0 == 0 ? tkv::kStageFirst : 0) | (b0 + 4 >= it.n_blk ? tkv::kStageLast : 0);
-                        for (int32_t t = 0; t < it.n_tok; ++t) sd.toks[t] = p->toks[it.tok_off + t];
-                        p->stages.push_back(sd);
-                    }
+            constexpr int32_t kXcds = 8;
+            auto cost = [&](const ItemDesc& it) {
+                return static_cast<int64_t>(it.n_blk) * ((static_cast<int64_t>(it.n_tok) * G + 31) / 32) + 1;
+            };
+            std::map<std::pair<int32_t, int32_t>, int32_t> gid;
+            std::vector<std::vector<int32_t>> groups;
+            std::vector<int64_t> gcost;
+            for (int32_t i = 0; i < static_cast<int32_t>(p->items.size()); ++i) {
+                const ItemDesc& it = p->items[i];
+                auto ins = gid.emplace(std::make_pair(p->blks[it.blk_off].blk, it.kvh), static_cast<int32_t>(groups.size()));
+                if (ins.second) {
+                    groups.emplace_back();
+                    gcost.push_back(0);
                 }
-                p->wg_off.push_back(static_cast<int32_t>(p->stages.size()));
+                groups[ins.first->second].push_back(i);
+                gcost[ins.first->second] += cost(it);
             }
+            std::vector<int32_t> gorder(groups.size());
+            std::iota(gorder.begin(), gorder.end(), 0);
+            std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a2, int32_t b2) { return gcost[a2] > gcost[b2]; });
+            using Load = std::pair<int64_t, int32_t>;
+            std::priority_queue<Load, std::vector<Load>, std::greater<Load>> xheap;
+            for (int32_t x = 0; x < kXcds; ++x) xheap.push({0, x});
+            std::vector<std::vector<int32_t>> xl(kXcds);
+            for (int32_t g2 : gorder) {
+                Load l = xheap.top();
+                xheap.pop();
+                xl[l.second].insert(xl[l.second].end(), groups[g2].begin(), groups[g2].end());
+                l.first += gcost[g2];
+                xheap.push(l);
+            }
+            for (auto& v : xl)
+                std::stable_sort(v.begin(), v.end(), [&](int32_t a2, int32_t b2) { return cost(p->items[a2]) > cost(p->items[b2]); });
+            std::vector<ItemDesc> ordered;
+            ordered.reserve(p->items.size());
+            std::vector<size_t> next(kXcds, 0);
+            while (ordered.size() < p->items.size()) {
+                for (int32_t x = 0; x < kXcds && ordered.size() < p->items.size(); ++x) {
+                    int32_t src = x;
+                    if (next[src] >= xl[src].size()) {  // this XCD's list is done: lend it the longest remaining one
+                        size_t best = 0;
+                        for (int32_t y = 0; y < kXcds; ++y)
+                            if (xl[y].size() - next[y] > best) {
+                                best = xl[y].size() - next[y];
+                                src = y;
+                            }
+                    }
+                    ordered.push_back(p->items[xl[src][next[src]++]]);
+                }
+            }
+            p->items.swap(ordered);
         }
 
         // ------------------------------------------------------------ workspace layout
@@ -445,10 +455,6 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         off = align256(off + bytes(p->merges.size(), sizeof(MergeDesc)));
         p->off_mslots = off;
         off = align256(off + bytes(p->merge_slots.size(), sizeof(int32_t)));
-        p->off_wg = off;
-        off = align256(off + bytes(p->wg_off.size(), sizeof(int32_t)));
-        p->off_stages = off;
-        off = align256(off + bytes(p->stages.size(), sizeof(tkv::StageDesc)));
         p->off_wdesc = off;
         off = align256(off + bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
         p->off_woff = off;
@@ -470,8 +476,6 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         put(p->off_blks, p->blks.data(), bytes(p->blks.size(), sizeof(BlkDesc)));
         put(p->off_merges, p->merges.data(), bytes(p->merges.size(), sizeof(MergeDesc)));
         put(p->off_mslots, p->merge_slots.data(), bytes(p->merge_slots.size(), sizeof(int32_t)));
-        put(p->off_wg, p->wg_off.data(), bytes(p->wg_off.size(), sizeof(int32_t)));
-        put(p->off_stages, p->stages.data(), bytes(p->stages.size(), sizeof(tkv::StageDesc)));
         put(p->off_wdesc, p->wave_desc.data(), bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
         put(p->off_woff, p->wave_off.data(), bytes(p->wave_off.size(), sizeof(int32_t)));
         put(p->off_wtiles, p->wave_tiles.data(), bytes(p->wave_tiles.size(), sizeof(int32_t)));
