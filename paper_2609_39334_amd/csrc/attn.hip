@@ -191,6 +191,41 @@ __device__ __forceinline__ void softmax_pair(WaveAcc<D, T>& A, f32x4_t (&sa)[T],
     }
 }
 
+// Online softmax over a pair of already-masked 16-key blocks with a lazily moved exponent base: the
+// base m (per row) only moves when a row's new maximum exceeds it by more than 2^8 in probability
+// scale, so O and l are rescaled rarely; P = exp2((s - m) * scale) then stays below 2^8, well
+// inside fp32 / bf16 range, and the result is exact up to rounding for any base (the lse adds m
+// back).  P^T is packed as in softmax_pair.
+template <int D, int T>
+__device__ __forceinline__ void softmax_pair_lazy(WaveAcc<D, T>& A, f32x4_t (&sa)[T], f32x4_t (&sb)[T], float sl2,
+                                                  bf16x8_t (&pb)[T]) {
+    constexpr float kSlack = 8.f;  // log2 of the largest P allowed before the base moves
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        const float mx = rowmax4(fmaxf(fmaxf(fmaxf(sa[tt][0], sa[tt][1]), fmaxf(sa[tt][2], sa[tt][3])),
+                                       fmaxf(fmaxf(sb[tt][0], sb[tt][1]), fmaxf(sb[tt][2], sb[tt][3]))));
+        if (__builtin_amdgcn_ballot_w64(mx != -INFINITY && (A.m[tt] == -INFINITY || (mx - A.m[tt]) * sl2 > kSlack)) != 0) {
+            const float m_new = fmaxf(A.m[tt], mx);
+            const float alpha = A.m[tt] == m_new ? 1.f : __builtin_amdgcn_exp2f((A.m[tt] - m_new) * sl2);
+            A.l[tt] *= alpha;
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) A.acc[tt][c] *= alpha;
+            A.m[tt] = m_new;
+        }
+        const float msc = A.m[tt] == -INFINITY ? 0.f : A.m[tt] * sl2;
+        float psum = 0.f;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            sa[tt][x] = __builtin_amdgcn_exp2f(fmaf(sa[tt][x], sl2, -msc));
+            sb[tt][x] = __builtin_amdgcn_exp2f(fmaf(sb[tt][x], sl2, -msc));
+            psum += sa[tt][x] + sb[tt][x];
+        }
+        A.l[tt] += psum;
+        pb[tt] = __builtin_bit_cast(bf16x8_t, uint4{pack_bf16x2(sa[tt][0], sa[tt][1]), pack_bf16x2(sa[tt][2], sa[tt][3]),
+                                                    pack_bf16x2(sb[tt][0], sb[tt][1]), pack_bf16x2(sb[tt][2], sb[tt][3])});
+    }
+}
+
 // Normalise one column tile's rows and write them: the final bf16 output and lse (slot < 0) or an
 // fp32 partial and its lse.  Lane holds columns 16ct + 4kg + r of its row; l is summed over the
 // four lanes of the row.
@@ -506,33 +541,53 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         dcur = dnxt;
         dnxt = stage_desc(st + 2);
         if (!wave_active) continue;
+        int len[4], bpos[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            len[j] = 4 * st + j < nb ? __builtin_amdgcn_readlane(dthis.y, j) : 0;
+            bpos[j] = pos;
+            pos += len[j];
+        }
+        // S^T for all four blocks first (32 independent MFMAs), so that each pair's softmax below
+        // overlaps MFMAs still in flight
+        f32x4_t sc[4][T];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int tt = 0; tt < T; ++tt) sc[j][tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < D / 32; ++kk) {
+            bf16x8_t kf[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                kf[j] = *reinterpret_cast<const bf16x8_t*>(ks + (16 * j + col) * KSTR + 32 * kk + 8 * kg);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int tt = 0; tt < T; ++tt) sc[j][tt] = mfma_16x16x32(kf[j], qf[tt][kk], sc[j][tt]);
+        }
+        // one uniform decision per stage: mask only if a block is partial or absent, or some row's
+        // causal limit falls inside the stage
+        const int stage_end = pos;  // one past the last key position of the stage
+        if (len[3] != 16 || len[0] + len[1] + len[2] != 48 ||
+            __builtin_amdgcn_ballot_w64((ok[0] && limit[0] < stage_end - 1) || (ok[1] && limit[1] < stage_end - 1)) != 0) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int tt = 0; tt < T; ++tt) {
+                    const int vlen = min(len[j], limit[tt] - bpos[j] + 1);
+#pragma unroll
+                    for (int x = 0; x < 4; ++x)
+                        if (4 * kg + x >= vlen) sc[j][tt][x] = -INFINITY;
+                }
+        }
 #pragma unroll
         for (int jp = 0; jp < 2; ++jp) {
             const int ja = 2 * jp, jb = 2 * jp + 1;
-            const int len_a = 4 * st + ja < nb ? __builtin_amdgcn_readlane(dthis.y, ja) : 0;
-            const int len_b = 4 * st + jb < nb ? __builtin_amdgcn_readlane(dthis.y, jb) : 0;
-            const int pos_a = pos, pos_b = pos + len_a;
-            pos = pos_b + len_b;
             // skip a pair that no row of this wave may see (past every causal limit, or absent)
-            if (len_a == 0 || __builtin_amdgcn_ballot_w64(limit[0] >= pos_a || limit[1] >= pos_a) == 0) continue;
-            f32x4_t sa[T], sb[T];
-#pragma unroll
-            for (int tt = 0; tt < T; ++tt) {
-                sa[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                sb[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            }
-#pragma unroll
-            for (int kk = 0; kk < D / 32; ++kk) {
-                const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(ks + (16 * ja + col) * KSTR + 32 * kk + 8 * kg);
-                const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(ks + (16 * jb + col) * KSTR + 32 * kk + 8 * kg);
-#pragma unroll
-                for (int tt = 0; tt < T; ++tt) {
-                    sa[tt] = mfma_16x16x32(ka, qf[tt][kk], sa[tt]);
-                    sb[tt] = mfma_16x16x32(kb, qf[tt][kk], sb[tt]);
-                }
-            }
+            if (len[ja] == 0 || __builtin_amdgcn_ballot_w64(limit[0] >= bpos[ja] || limit[1] >= bpos[ja]) == 0) continue;
             bf16x8_t pb[T];
-            softmax_pair<D, T>(A, sa, sb, len_a, pos_a, len_b, pos_b, limit, kg, sl2, pb);
+            softmax_pair_lazy<D, T>(A, sc[ja], sc[jb], sl2, pb);
             const uint8_t* vra = vs + (16 * ja + 4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
             const uint8_t* vrb = vra + 16 * VROW;
 #pragma unroll
