@@ -191,6 +191,21 @@ __device__ __forceinline__ void softmax_pair(WaveAcc<D, T>& A, f32x4_t (&sa)[T],
     }
 }
 
+// Mask the scores of one 16-key block for T column tiles (lane holds keys 4kg + x of its row):
+// keys past the block's length or past the row's causal limit get -inf; full, visible blocks skip it.
+template <int T>
+__device__ __forceinline__ void mask_block(f32x4_t (&s)[T], int len, int pos, const int (&limit)[T], int kg) {
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        if (__builtin_amdgcn_ballot_w64(!(len == 16 && limit[tt] >= pos + 15)) != 0) {
+            const int vlen = min(len, limit[tt] - pos + 1);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                if (4 * kg + x >= vlen) s[tt][x] = -INFINITY;
+        }
+    }
+}
+
 // Online softmax over a pair of already-masked 16-key blocks with a lazily moved exponent base: the
 // base m (per row) only moves when a row's new maximum exceeds it by more than 2^8 in probability
 // scale, so O and l are rescaled rarely; P = exp2((s - m) * scale) then stays below 2^8, well
@@ -400,25 +415,137 @@ __device__ __forceinline__ void wave_run(const int4* __restrict__ wdesc, int e0,
     }
 }
 
+// The same walk for T <= 2, two blocks at a time: two register sets hold a pair of K/V blocks, and
+// the next pair's loads (across item boundaries too; every item has an even block count) are in
+// flight while the current pair is contracted; the pair goes through one 32-key online-softmax
+// step with a lazily moved base and through PV on v_mfma_f32_16x16x32_bf16.
+template <int D, int T>
+__device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, int e0, int e1,
+                                              const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+                                              const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
+                                              float* __restrict__ lse, float* __restrict__ po,
+                                              float* __restrict__ plse, int hq, int hkv, int G, float sl2,
+                                              uint8_t* vs, int lane) {
+    constexpr int VROW = 2 * D + 32;
+    const int col = lane & 15, kg = lane >> 4;
+    int tok[T], grp[T];
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        const int row = 16 * tt + col;
+        tok[tt] = min(row / G, tkv::kWaveToks - 1);
+        grp[tt] = row - (row / G) * G;
+    }
+    const size_t blk_stride = static_cast<size_t>(hkv) * (16 * D);
+    const uint8_t* vra = vs + (4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
+    const uint8_t* vrb = vra + 16 * VROW;
+
+    int4 dc = wdesc[static_cast<size_t>(e0) * 64 + lane];
+    int4 dn = wdesc[static_cast<size_t>(min(e0 + 1, e1 - 1)) * 64 + lane];
+    WaveItem<T> ic = wave_item<T>(dc, tok, grp, G);
+    bf16x8_t qf[T][D / 32];
+    load_q<D, T>(qf, q, ic, hq, kg);
+    BlockRegs<D> ra, rb;
+    {
+        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
+        const int len0 = __builtin_amdgcn_readlane(dc.y, 0), len1 = __builtin_amdgcn_readlane(dc.y, 1);
+        const size_t b0 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 0)) * blk_stride + kvh_off;
+        const size_t b1 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 1)) * blk_stride + kvh_off;
+        load_k<D>(ra, kpool, b0, len0, lane);
+        load_v<D>(ra, vpool, b0, len0, lane);
+        load_k<D>(rb, kpool, b1, len1, lane);
+        load_v<D>(rb, vpool, b1, len1, lane);
+    }
+    WaveAcc<D, T> A;
+    for (int e = e0;; ++e) {
+        const bool more = e + 1 < e1;
+        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
+        const size_t kvh_off_n = static_cast<size_t>(__builtin_amdgcn_readlane(dn.w, 0)) * (16 * D);
+        A.reset();
+        const int nb = ic.nb;  // even
+        for (int b = 0; b < nb; b += 2) {
+            // the next pair: blocks b + 2, b + 3 of this item, or blocks 0, 1 of the next item
+            const bool cross = b + 2 >= nb;
+            const int bn = cross ? 0 : b + 2;
+            const int src_x = cross ? dn.x : dc.x;
+            const int src_y = cross ? (more ? dn.y : 0) : dc.y;
+            const size_t off_n = cross ? kvh_off_n : kvh_off;
+            const size_t boff_na = static_cast<size_t>(__builtin_amdgcn_readlane(src_x, bn)) * blk_stride + off_n;
+            const size_t boff_nb = static_cast<size_t>(__builtin_amdgcn_readlane(src_x, bn + 1)) * blk_stride + off_n;
+            const int len_na = __builtin_amdgcn_readlane(src_y, bn), len_nb = __builtin_amdgcn_readlane(src_y, bn + 1);
+            const int len_a = __builtin_amdgcn_readlane(dc.y, b), len_b = __builtin_amdgcn_readlane(dc.y, b + 1);
+            const int pos_a = __builtin_amdgcn_readlane(dc.z, b), pos_b = __builtin_amdgcn_readlane(dc.z, b + 1);
+            // S^T for both blocks, then the K registers take the next pair
+            f32x4_t sa[T], sb[T];
+#pragma unroll
+            for (int tt = 0; tt < T; ++tt) {
+                sa[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                sb[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+#pragma unroll
+                for (int tt = 0; tt < T; ++tt) {
+                    sa[tt] = mfma_16x16x32(__builtin_bit_cast(bf16x8_t, ra.k[ks]), qf[tt][ks], sa[tt]);
+                    sb[tt] = mfma_16x16x32(__builtin_bit_cast(bf16x8_t, rb.k[ks]), qf[tt][ks], sb[tt]);
+                }
+            load_k<D>(ra, kpool, boff_na, len_na, lane);
+            load_k<D>(rb, kpool, boff_nb, len_nb, lane);
+            mask_block<T>(sa, len_a, pos_a, ic.limit, kg);
+            mask_block<T>(sb, len_b, pos_b, ic.limit, kg);
+            bf16x8_t pb[T];
+            softmax_pair_lazy<D, T>(A, sa, sb, sl2, pb);
+            // both blocks' V rows into this wave's LDS region, then the V registers take the next pair
+#pragma unroll
+            for (int i = 0; i < D / 32; ++i) {
+                const int c = lane + 64 * i;
+                *reinterpret_cast<u32x4_t*>(vs + (c / (D / 8)) * VROW + (c % (D / 8)) * 16) = ra.v[i];
+                *reinterpret_cast<u32x4_t*>(vs + (16 + c / (D / 8)) * VROW + (c % (D / 8)) * 16) = rb.v[i];
+            }
+            load_v<D>(ra, vpool, boff_na, len_na, lane);
+            load_v<D>(rb, vpool, boff_nb, len_nb, lane);
+            // O^T += V^T P^T over the 32 keys: V^T from the two blocks' transposed LDS reads
+#pragma unroll
+            for (int ct = 0; ct < D / 16; ++ct) {
+                const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vra + ct * 32)));
+                const s16x4_t vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vrb + ct * 32)));
+                const bf16x8_t vab = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                for (int tt = 0; tt < T; ++tt) A.acc[tt][ct] = mfma_16x16x32(vab, pb[tt], A.acc[tt][ct]);
+            }
+        }
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
+            write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], ic.ok[tt], ic.qtok[tt], ic.h[tt], ic.slot[tt], kg, o, lse, po,
+                          plse, hq, sl2);
+        if (!more) break;
+        dc = dn;
+        dn = wdesc[static_cast<size_t>(min(e + 2, e1 - 1)) * 64 + lane];
+        ic = wave_item<T>(dc, tok, grp, G);
+        load_q<D, T>(qf, q, ic, hq, kg);
+    }
+}
+
 // Each wave walks its own list of items (a contiguous range of the descriptor stream) with no
 // barrier; its tile width T (1..3 tiles of 16 query rows) is fixed per wave by the planner.
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_wave(
+__global__ __launch_bounds__(64 * tkv::kWaveWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_wave(
     const int4* __restrict__ wdesc, const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
     uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq,
     int hkv, int G, float sl2) {
     constexpr int VROW = 2 * D + 32;
-    __shared__ __attribute__((aligned(16))) uint8_t Vs[4][16 * VROW];
+    __shared__ __attribute__((aligned(16))) uint8_t Vs[tkv::kWaveWG][32 * VROW];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int w = blockIdx.x * 4 + wave;
+    const int w = blockIdx.x * tkv::kWaveWG + wave;
     const int e0 = woff[w], e1 = woff[w + 1], T = wtiles[w];
     if (e0 >= e1) return;  // waves are independent: no barrier follows
     if (T == 1)
-        wave_run<D, 1>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
+        wave_run_pair<D, 1>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
     else if (T == 2)
-        wave_run<D, 2>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
+        wave_run_pair<D, 2>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
     else
         wave_run<D, 3>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
 }
@@ -704,7 +831,7 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     hipEvent_t* ev = nullptr;
     if (p->prof_n < p->prof_max) ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 4 * p->prof_n++;
     const int n_tile = static_cast<int>(p->items.size());
-    const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of 4
+    const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of kWaveWG
     hipEvent_t main_start = ev ? ev[0] : nullptr, main_stop = ev ? ev[1] : nullptr;
     if (n_tile > 0)
         hipExtLaunchKernelGGL(attn_tile<D>, dim3(static_cast<unsigned>(n_tile)), dim3(kThreads), 0, st, main_start,
@@ -714,7 +841,7 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
     if (n_wave > 0)
-        hipExtLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / 4)), dim3(kThreads), 0, st,
+        hipExtLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / kWaveWG)), dim3(64 * kWaveWG), 0, st,
                               n_tile > 0 ? nullptr : main_start, main_stop, 0, wdesc, woff, wtiles,
                               static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                               static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,

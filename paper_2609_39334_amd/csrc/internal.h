@@ -28,7 +28,8 @@ constexpr int kWaveRows = 16;   // query rows of one MFMA column tile of the wav
 constexpr int kWaveMaxTiles = 3;  // column tiles a wave contracts against each K/V block
 constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
 constexpr int kWaveToks = 48;   // query tokens of a wave-kernel item (16 kWaveMaxTiles / G)
-constexpr int kWaveWorkers = 2048;  // waves of the wave kernel (each streams a list of items)
+constexpr int kWaveWorkers = 2048;  // waves of the wave kernel: 2 workgroups of kWaveWG on each of 256 CUs
+constexpr int kWaveWG = 4;      // waves per workgroup of the wave kernel (independent; no barriers)
 
 // One work item: a tile of query tokens (each with all G query heads of one KV
 // head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the
@@ -60,7 +61,8 @@ struct BlkDesc {
 // gets e[l]); block fields come out with v_readlane, token fields with ds_bpermute.
 //   e[j]      (j < 16): {pool block id, length, path position, header word j} of key block j
 //                       (block 0's id and length 0 past the item's blocks); header words:
-//                       0 KV head, 1 tile tokens, 2 key blocks
+//                       0 KV head, 1 tile tokens, 2 key blocks (rounded up to even for tile widths
+//                       1 and 2, whose waves walk blocks in pairs)
 //   e[16 + t] (t < 48): {query token, causal limit, partial slot (-1: final output), 0} of tile
 //                       token t (token 0's past the tile)
 struct WaveDesc {

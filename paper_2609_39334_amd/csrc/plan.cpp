@@ -276,15 +276,18 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         st.n_items_row = st.n_items - st.n_items_shared;
         std::stable_sort(p->wave_items.begin(), p->wave_items.end(),
                          [](const ItemDesc& a, const ItemDesc& b) { return a.n_blk > b.n_blk; });
-        // Wave streams.  Every wave runs items of one tile width T (its code path is fixed);
-        // waves are split over the widths in proportion to their work.  Workgroups are dispatched
-        // round-robin over the 8 XCDs (each with its own L2), so wave w runs on XCD (w / 4) % 8:
-        // all tiles of one (chunk, KV head), which read the same K/V blocks, go to one XCD.
-        // Groups are assigned to XCDs, and items to the XCD's waves, longest processing time first.
+        // Wave streams.  Every wave runs items of one tile width T (its code path is fixed); waves
+        // are split over the widths in proportion to their work.  Workgroups of kWaveWG waves are
+        // dispatched round-robin over the 8 XCDs (each with its own L2), so wave w runs on XCD
+        // (w / kWaveWG) % 8: all tiles of one (chunk, KV head), which read the same K/V blocks, go
+        // to one XCD.  Groups are assigned to XCDs, and items to the XCD's waves, longest
+        // processing time first; each XCD's heaviest waves take its first workgroups, which the
+        // dispatcher starts first.
         {
+            constexpr int32_t kXcds = 8;
             const int32_t n_items = static_cast<int32_t>(p->wave_items.size());
             int32_t target = tkv::kWaveWorkers;
-            if (const char* env = std::getenv("TKV_WAVES")) target = std::max(4, std::atoi(env));
+            if (const char* env = std::getenv("TKV_WAVES")) target = std::max(kXcds, std::atoi(env));
             auto cost = [](const ItemDesc& it) { return static_cast<int64_t>(it.n_blk) * (3 + it.pad) + 4; };
             std::vector<std::vector<int32_t>> by_t(tkv::kWaveMaxTiles + 1);
             std::vector<int64_t> cost_t(tkv::kWaveMaxTiles + 1, 0);
@@ -294,18 +297,44 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 cost_t[p->wave_items[i].pad] += cost(p->wave_items[i]);
                 cost_all += cost(p->wave_items[i]);
             }
-            p->wave_off.assign(1, 0);
-            constexpr int32_t kXcds = 8;
+            struct Wave {
+                int32_t T;
+                int64_t cost;
+                std::vector<int32_t> items;
+            };
+            // waves per XCD of each width: shares of the target in proportion to the work (at
+            // least one, at most one per item on the XCD), the remainder going to the widths
+            // with the largest fractional share, so that a large batch fills the target exactly
+            std::vector<int32_t> per_xt(tkv::kWaveMaxTiles + 1, 0);
+            {
+                const int32_t target_x = std::max(1, target / kXcds);
+                std::vector<double> frac(tkv::kWaveMaxTiles + 1, 0.0);
+                int32_t used = 0;
+                for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
+                    if (by_t[T].empty()) continue;
+                    const double want = static_cast<double>(target_x) * cost_t[T] / cost_all;
+                    const int32_t cap = static_cast<int32_t>((by_t[T].size() + kXcds - 1) / kXcds);
+                    per_xt[T] = std::min(cap, std::max(1, static_cast<int32_t>(want)));
+                    frac[T] = per_xt[T] < cap ? want - per_xt[T] : -1.0;
+                    used += per_xt[T];
+                }
+                while (used < target_x) {
+                    int32_t best = -1;
+                    for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T)
+                        if (frac[T] >= 0.0 && (best < 0 || frac[T] > frac[best])) best = T;
+                    if (best < 0) break;
+                    ++per_xt[best];
+                    ++used;
+                    const int32_t cap = static_cast<int32_t>((by_t[best].size() + kXcds - 1) / kXcds);
+                    frac[best] = per_xt[best] < cap ? frac[best] - 1.0 + 1e-9 * cost_t[best] : -1.0;
+                    if (frac[best] < 0.0 && per_xt[best] < cap) frac[best] = 0.0;
+                }
+            }
+            std::vector<std::vector<Wave>> xcd_waves(kXcds);
             for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
                 const std::vector<int32_t>& its = by_t[T];
                 if (its.empty()) continue;
-                // waves of this width: a share of the target, whole workgroups, at most one per item
-                const int64_t share = (static_cast<int64_t>(target) * cost_t[T] + cost_all - 1) / cost_all;
-                const int32_t n_w = static_cast<int32_t>(
-                    (std::min<int64_t>(std::max<int64_t>(share, 4), static_cast<int64_t>(its.size())) + 3) / 4 * 4);
-                const int32_t w0 = static_cast<int32_t>(p->wave_tiles.size());  // a multiple of 4
-                std::vector<std::vector<int32_t>> xcd_waves(kXcds);
-                for (int32_t w = 0; w < n_w; ++w) xcd_waves[((w0 + w) / 4) % kXcds].push_back(w);
+                const int32_t per_x = per_xt[T];
                 std::map<std::pair<int32_t, int32_t>, int32_t> gid;
                 std::vector<std::vector<int32_t>> groups;
                 std::vector<int64_t> gcost;
@@ -321,37 +350,53 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 }
                 std::vector<int32_t> gorder(groups.size());
                 std::iota(gorder.begin(), gorder.end(), 0);
-                std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a, int32_t b) { return gcost[a] > gcost[b]; });
+                std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a2, int32_t b2) { return gcost[a2] > gcost[b2]; });
                 using Load = std::pair<int64_t, int32_t>;
                 std::priority_queue<Load, std::vector<Load>, std::greater<Load>> xheap;
-                for (int32_t x = 0; x < kXcds; ++x)
-                    if (!xcd_waves[x].empty()) xheap.push({0, x});
+                for (int32_t x = 0; x < kXcds; ++x) xheap.push({0, x});
                 std::vector<std::vector<int32_t>> xcd_items(kXcds);
                 for (int32_t g2 : gorder) {
                     Load l = xheap.top();
                     xheap.pop();
                     xcd_items[l.second].insert(xcd_items[l.second].end(), groups[g2].begin(), groups[g2].end());
-                    l.first += gcost[g2] * 1024 / static_cast<int64_t>(xcd_waves[l.second].size());
+                    l.first += gcost[g2];
                     xheap.push(l);
                 }
-                std::vector<std::vector<int32_t>> lists(n_w);
                 for (int32_t x = 0; x < kXcds; ++x) {
-                    std::stable_sort(xcd_items[x].begin(), xcd_items[x].end(), [&](int32_t a, int32_t b) {
-                        return p->wave_items[a].n_blk > p->wave_items[b].n_blk;
+                    if (xcd_items[x].empty()) continue;
+                    std::stable_sort(xcd_items[x].begin(), xcd_items[x].end(), [&](int32_t a2, int32_t b2) {
+                        return p->wave_items[a2].n_blk > p->wave_items[b2].n_blk;
                     });
+                    const int32_t nw = std::min<int32_t>(per_x, static_cast<int32_t>(xcd_items[x].size()));
+                    std::vector<Wave> ws(nw, Wave{T, 0, {}});
                     std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-                    for (int32_t w : xcd_waves[x]) heap.push({0, w});
+                    for (int32_t w = 0; w < nw; ++w) heap.push({0, w});
                     for (int32_t i : xcd_items[x]) {
                         Load l = heap.top();
                         heap.pop();
-                        lists[l.second].push_back(i);
+                        ws[l.second].items.push_back(i);
+                        ws[l.second].cost += cost(p->wave_items[i]);
                         l.first += cost(p->wave_items[i]);
                         heap.push(l);
                     }
+                    xcd_waves[x].insert(xcd_waves[x].end(), ws.begin(), ws.end());
                 }
-                for (int32_t w = 0; w < n_w; ++w) {
-                    for (int32_t i : lists[w]) {
+            }
+            // launch order: workgroup k holds kWaveWG waves of XCD k % 8, heaviest first; an XCD
+            // whose list has run out lends its slots to the longest remaining list
+            for (auto& v : xcd_waves)
+                std::stable_sort(v.begin(), v.end(), [](const Wave& a2, const Wave& b2) { return a2.cost > b2.cost; });
+            size_t n_total = 0;
+            for (auto& v : xcd_waves) n_total += v.size();
+            const size_t n_slots_w = (n_total + tkv::kWaveWG - 1) / tkv::kWaveWG * tkv::kWaveWG;
+            std::vector<size_t> next(kXcds, 0);
+            p->wave_off.assign(1, 0);
+            auto emit = [&](const Wave* wv) {
+                if (wv) {
+                    for (int32_t i : wv->items) {
                         const ItemDesc& it = p->wave_items[i];
+                        // widths 1 and 2 walk blocks in pairs: an odd key list gets an empty block
+                        const int32_t nb_run = it.pad <= 2 ? (it.n_blk + 1) & ~1 : it.n_blk;
                         tkv::WaveDesc wd{};
                         int32_t pos = it.pos0;
                         for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
@@ -364,7 +409,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                         }
                         wd.e[3] = it.kvh;
                         wd.e[7] = it.n_tok;
-                        wd.e[11] = it.n_blk;
+                        wd.e[11] = nb_run;
                         for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
                             const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
                             wd.e[4 * (16 + t)] = td.qtok;
@@ -373,9 +418,23 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                         }
                         p->wave_desc.push_back(wd);
                     }
-                    p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
-                    p->wave_tiles.push_back(T);
                 }
+                p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
+                p->wave_tiles.push_back(wv ? wv->T : 1);
+            };
+            for (size_t slot = 0; slot < n_slots_w; ++slot) {
+                const int32_t x = static_cast<int32_t>((slot / tkv::kWaveWG) % kXcds);
+                int32_t src = x;
+                if (next[src] >= xcd_waves[src].size()) {
+                    size_t best = 0;
+                    src = -1;
+                    for (int32_t y = 0; y < kXcds; ++y)
+                        if (xcd_waves[y].size() - next[y] > best) {
+                            best = xcd_waves[y].size() - next[y];
+                            src = y;
+                        }
+                }
+                emit(src >= 0 ? &xcd_waves[src][next[src]++] : nullptr);
             }
         }
         st.n_items_wave = static_cast<int32_t>(p->wave_items.size());
