@@ -10,11 +10,13 @@
 // a row's running max moves).  Keys past a block's length are never loaded (row reads are clamped
 // to the block's last token and masked) and keys past a token's causal limit get -inf.
 //
-// attn_wave:  decode-shaped work (G <= 16): every wave is an independent worker walking its own
-//             list of items, each a tile of up to 48 rows over a chunk of <= 16 blocks, with the
-//             next block always in flight; no LDS sharing, no barriers.
-// attn_tile:  wide tiles (multi-token verify rows, G > 16): one workgroup of four waves per item,
-//             128 rows (32 per wave) against 64-key stages of K/V double-buffered through LDS.
+// attn_wave:  decode-shaped work (G <= 16, chunks of at most kWaveMaxRows rows): every wave is an
+//             independent worker walking its own list of items, each a tile of up to 32 rows over a
+//             chunk of <= 16 blocks, with the next two blocks always in flight; no LDS sharing
+//             between waves, no barriers.
+// attn_tile:  wide tiles (multi-token verify rows, wide shared chunks, G > 16): one workgroup of
+//             four waves per item, 128 rows (32 per wave) against 64-key stages of K/V
+//             double-buffered through LDS.
 // merge_partials: log-sum-exp merge of the partial results of a query token's chunks:
 //             lse = log sum_j exp(lse_j),  o = sum_j exp(lse_j - lse) o_j.
 
@@ -300,6 +302,31 @@ __device__ __forceinline__ WaveItem<T> wave_item(int4 d, const int (&tok)[T], co
     return w;
 }
 
+// This lane's row of each column tile: token index within the tile and query head within the group.
+template <int T>
+__device__ __forceinline__ void tile_rows(int col, int G, int (&tok)[T], int (&grp)[T]) {
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        const int row = 16 * tt + col;
+        tok[tt] = min(row / G, tkv::kWaveToks - 1);
+        grp[tt] = row - (row / G) * G;
+    }
+}
+
+// Only the causal limits stay live across an item's block loop; the output fields are decoded
+// again from the descriptor when the item is written.
+template <int T>
+__device__ __forceinline__ void tile_limits(int4 d, int col, int G, int (&limit)[T]) {
+    int tok[T], grp[T];
+    tile_rows<T>(col, G, tok, grp);
+    const int n_tok = __builtin_amdgcn_readlane(d.w, 1);
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        const int lim = __builtin_amdgcn_ds_bpermute((16 + tok[tt]) * 4, d.y);
+        limit[tt] = (16 * tt + col) / G < n_tok ? lim : -1;
+    }
+}
+
 template <int D, int T>
 __device__ __forceinline__ void load_q(bf16x8_t (&qf)[T][D / 32], const uint16_t* __restrict__ q,
                                        const WaveItem<T>& w, int hq, int kg) {
@@ -311,116 +338,19 @@ __device__ __forceinline__ void load_q(bf16x8_t (&qf)[T][D / 32], const uint16_t
     }
 }
 
-// One 16-key block against the wave's T tiles; the block's registers are refilled with the next
-// block of the wave's stream as soon as each half (K, then V) has been consumed.
-template <int D, int T, int VROW>
-__device__ __forceinline__ void wave_block(WaveAcc<D, T>& A, BlockRegs<D>& r, const bf16x8_t (&qf)[T][D / 32],
-                                           int len, int pos, const int (&limit)[T],
-                                           const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-                                           size_t boff_n, int len_n, uint8_t* vs, const uint8_t* vrd, int lane,
-                                           int kg, float sl2) {
-    // S^T = K Q^T for every tile (independent MFMA chains), then the K registers take the next loads
-    f32x4_t s[T];
-#pragma unroll
-    for (int tt = 0; tt < T; ++tt) s[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks)
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt) s[tt] = mfma_16x16x32(__builtin_bit_cast(bf16x8_t, r.k[ks]), qf[tt][ks], s[tt]);
-    load_k<D>(r, kpool, boff_n, len_n, lane);
-    s16x4_t pb[T];
-    softmax_step<D, T>(A, s, len, pos, limit, kg, sl2, pb);
-    // V rows into this wave's LDS region, then the V registers take the next loads
-#pragma unroll
-    for (int i = 0; i < D / 32; ++i) {
-        const int c = lane + 64 * i;
-        *reinterpret_cast<u32x4_t*>(vs + (c / (D / 8)) * VROW + (c % (D / 8)) * 16) = r.v[i];
-    }
-    load_v<D>(r, vpool, boff_n, len_n, lane);
-    // O^T += V^T P^T: P^T as the S^T result sits in the lanes, V^T by transposing LDS reads
-#pragma unroll
-    for (int ct = 0; ct < D / 16; ++ct) {
-        const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vrd + ct * 32)));
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt)
-            A.acc[tt][ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[tt], A.acc[tt][ct], 0, 0, 0);
-    }
-}
-
-// One wave's list of items [e0, e1), all of T column tiles.  The next key block is always in
-// flight, across item boundaries too (the last block of an item prefetches the first of the next);
-// the next item's descriptor is fetched at the start of an item.
-template <int D, int T>
-__device__ __forceinline__ void wave_run(const int4* __restrict__ wdesc, int e0, int e1,
-                                         const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
-                                         const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
-                                         float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse,
-                                         int hq, int hkv, int G, float sl2, uint8_t* vs, int lane) {
-    constexpr int VROW = 2 * D + 32;  // LDS bytes per V row: the padding spreads 4 rows over 32 banks
-    const int col = lane & 15, kg = lane >> 4;
-    int tok[T], grp[T];
-#pragma unroll
-    for (int tt = 0; tt < T; ++tt) {
-        const int row = 16 * tt + col;
-        tok[tt] = min(row / G, tkv::kWaveToks - 1);
-        grp[tt] = row - (row / G) * G;
-    }
-    const size_t blk_stride = static_cast<size_t>(hkv) * (16 * D);
-    const uint8_t* vrd = vs + (4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
-
-    int4 dc = wdesc[static_cast<size_t>(e0) * 64 + lane];
-    int4 dn = wdesc[static_cast<size_t>(min(e0 + 1, e1 - 1)) * 64 + lane];
-    WaveItem<T> ic = wave_item<T>(dc, tok, grp, G);
-    bf16x8_t qf[T][D / 32];
-    load_q<D, T>(qf, q, ic, hq, kg);
-    BlockRegs<D> r;
-    {
-        const int len0 = __builtin_amdgcn_readlane(dc.y, 0);
-        const size_t b0 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 0)) * blk_stride +
-                          static_cast<size_t>(ic.kvh) * (16 * D);
-        load_k<D>(r, kpool, b0, len0, lane);
-        load_v<D>(r, vpool, b0, len0, lane);
-    }
-    WaveAcc<D, T> A;
-    for (int e = e0;; ++e) {
-        const bool more = e + 1 < e1;
-        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
-        const size_t kvh_off_n = static_cast<size_t>(__builtin_amdgcn_readlane(dn.w, 0)) * (16 * D);
-        A.reset();
-        const int nb = ic.nb;
-        for (int b = 0; b < nb; ++b) {
-            // the block after this one: the next of this item, or the first of the next item
-            // (a lane-wise select of the descriptor, then v_readlane: no branches)
-            const bool last = b + 1 == nb;
-            const int bn = last ? 0 : b + 1;
-            const int src_x = last ? dn.x : dc.x;
-            const int src_y = last ? (more ? dn.y : 0) : dc.y;
-            const size_t boff_n = static_cast<size_t>(__builtin_amdgcn_readlane(src_x, bn)) * blk_stride +
-                                  (last ? kvh_off_n : kvh_off);
-            wave_block<D, T, VROW>(A, r, qf, __builtin_amdgcn_readlane(dc.y, b), __builtin_amdgcn_readlane(dc.z, b),
-                                   ic.limit, kpool, vpool, boff_n, __builtin_amdgcn_readlane(src_y, bn), vs, vrd,
-                                   lane, kg, sl2);
-        }
-        // normalise and write each tile's final output or partial
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt)
-            write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], ic.ok[tt], ic.qtok[tt], ic.h[tt], ic.slot[tt], kg, o, lse, po,
-                          plse, hq, sl2);
-        if (!more) break;
-        dc = dn;
-        dn = wdesc[static_cast<size_t>(min(e + 2, e1 - 1)) * 64 + lane];
-        ic = wave_item<T>(dc, tok, grp, G);
-        load_q<D, T>(qf, q, ic, hq, kg);
-    }
-}
+// A wave's list of items: record `first` (= the wave's index), then records rest, rest + 1, ...,
+// n items in all.
+struct WaveList {
+    int first, rest, n;
+    __device__ __forceinline__ int at(int k) const { return k == 0 ? first : rest + min(k, n - 1) - 1; }
+};
 
 // The same walk for T <= 2, two blocks at a time: two register sets hold a pair of K/V blocks, and
 // the next pair's loads (across item boundaries too; every item has an even block count) are in
 // flight while the current pair is contracted; the pair goes through one 32-key online-softmax
 // step with a lazily moved base and through PV on v_mfma_f32_16x16x32_bf16.
 template <int D, int T>
-__device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, int e0, int e1,
+__device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, const WaveList& L,
                                               const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
                                               const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
                                               float* __restrict__ lse, float* __restrict__ po,
@@ -428,25 +358,26 @@ __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, in
                                               uint8_t* vs, int lane) {
     constexpr int VROW = 2 * D + 32;
     const int col = lane & 15, kg = lane >> 4;
-    int tok[T], grp[T];
-#pragma unroll
-    for (int tt = 0; tt < T; ++tt) {
-        const int row = 16 * tt + col;
-        tok[tt] = min(row / G, tkv::kWaveToks - 1);
-        grp[tt] = row - (row / G) * G;
-    }
     const size_t blk_stride = static_cast<size_t>(hkv) * (16 * D);
     const uint8_t* vra = vs + (4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
     const uint8_t* vrb = vra + 16 * VROW;
 
-    int4 dc = wdesc[static_cast<size_t>(e0) * 64 + lane];
-    int4 dn = wdesc[static_cast<size_t>(min(e0 + 1, e1 - 1)) * 64 + lane];
-    WaveItem<T> ic = wave_item<T>(dc, tok, grp, G);
+    int4 dc = wdesc[static_cast<size_t>(L.at(0)) * 64 + lane];
+    int4 dn = wdesc[static_cast<size_t>(L.at(1)) * 64 + lane];
     bf16x8_t qf[T][D / 32];
-    load_q<D, T>(qf, q, ic, hq, kg);
+    int kvh_c, nb_c, limit[T];
+    {
+        int tok[T], grp[T];
+        tile_rows<T>(col, G, tok, grp);
+        const WaveItem<T> ic = wave_item<T>(dc, tok, grp, G);
+        load_q<D, T>(qf, q, ic, hq, kg);
+        kvh_c = ic.kvh;
+        nb_c = ic.nb;
+    }
+    tile_limits<T>(dc, col, G, limit);
     BlockRegs<D> ra, rb;
     {
-        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
+        const size_t kvh_off = static_cast<size_t>(kvh_c) * (16 * D);
         const int len0 = __builtin_amdgcn_readlane(dc.y, 0), len1 = __builtin_amdgcn_readlane(dc.y, 1);
         const size_t b0 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 0)) * blk_stride + kvh_off;
         const size_t b1 = static_cast<size_t>(__builtin_amdgcn_readlane(dc.x, 1)) * blk_stride + kvh_off;
@@ -456,12 +387,12 @@ __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, in
         load_v<D>(rb, vpool, b1, len1, lane);
     }
     WaveAcc<D, T> A;
-    for (int e = e0;; ++e) {
-        const bool more = e + 1 < e1;
-        const size_t kvh_off = static_cast<size_t>(ic.kvh) * (16 * D);
+    for (int e = 0;; ++e) {
+        const bool more = e + 1 < L.n;
+        const size_t kvh_off = static_cast<size_t>(kvh_c) * (16 * D);
         const size_t kvh_off_n = static_cast<size_t>(__builtin_amdgcn_readlane(dn.w, 0)) * (16 * D);
         A.reset();
-        const int nb = ic.nb;  // even
+        const int nb = nb_c;  // even
         for (int b = 0; b < nb; b += 2) {
             // the next pair: blocks b + 2, b + 3 of this item, or blocks 0, 1 of the next item
             const bool cross = b + 2 >= nb;
@@ -490,8 +421,8 @@ __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, in
                 }
             load_k<D>(ra, kpool, boff_na, len_na, lane);
             load_k<D>(rb, kpool, boff_nb, len_nb, lane);
-            mask_block<T>(sa, len_a, pos_a, ic.limit, kg);
-            mask_block<T>(sb, len_b, pos_b, ic.limit, kg);
+            mask_block<T>(sa, len_a, pos_a, limit, kg);
+            mask_block<T>(sb, len_b, pos_b, limit, kg);
             bf16x8_t pb[T];
             softmax_pair_lazy<D, T>(A, sa, sb, sl2, pb);
             // both blocks' V rows into this wave's LDS region, then the V registers take the next pair
@@ -515,39 +446,48 @@ __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, in
                 for (int tt = 0; tt < T; ++tt) A.acc[tt][ct] = mfma_16x16x32(vab, pb[tt], A.acc[tt][ct]);
             }
         }
+        {
+            int tok[T], grp[T];
+            tile_rows<T>(col, G, tok, grp);
+            const WaveItem<T> ic = wave_item<T>(dc, tok, grp, G);
 #pragma unroll
-        for (int tt = 0; tt < T; ++tt)
-            write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], ic.ok[tt], ic.qtok[tt], ic.h[tt], ic.slot[tt], kg, o, lse, po,
-                          plse, hq, sl2);
+            for (int tt = 0; tt < T; ++tt)
+                write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], ic.ok[tt], ic.qtok[tt], ic.h[tt], ic.slot[tt], kg, o, lse,
+                              po, plse, hq, sl2);
+        }
         if (!more) break;
         dc = dn;
-        dn = wdesc[static_cast<size_t>(min(e + 2, e1 - 1)) * 64 + lane];
-        ic = wave_item<T>(dc, tok, grp, G);
-        load_q<D, T>(qf, q, ic, hq, kg);
+        dn = wdesc[static_cast<size_t>(L.at(e + 2)) * 64 + lane];
+        {
+            int tok[T], grp[T];
+            tile_rows<T>(col, G, tok, grp);
+            const WaveItem<T> ic = wave_item<T>(dc, tok, grp, G);
+            load_q<D, T>(qf, q, ic, hq, kg);
+            kvh_c = ic.kvh;
+            nb_c = ic.nb;
+        }
+        tile_limits<T>(dc, col, G, limit);
     }
 }
 
-// Each wave walks its own list of items (a contiguous range of the descriptor stream) with no
-// barrier; its tile width T (1..3 tiles of 16 query rows) is fixed per wave by the planner.
+// Wave-kernel worker: wave w of the wave grid walks its own list of items with no barrier; its tile
+// width T (1 or 2 column tiles of 16 query rows) is fixed per wave by the planner.
 template <int D>
-__global__ __launch_bounds__(64 * tkv::kWaveWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_wave(
-    const int4* __restrict__ wdesc, const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq,
-    int hkv, int G, float sl2) {
+__device__ __forceinline__ void wave_worker(int w, int wave, int lane, const int4* __restrict__ wdesc,
+                                            const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
+                                            const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+                                            const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
+                                            float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse,
+                                            int hq, int hkv, int G, float sl2, uint8_t* smem) {
     constexpr int VROW = 2 * D + 32;
-    __shared__ __attribute__((aligned(16))) uint8_t Vs[tkv::kWaveWG][32 * VROW];
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int w = blockIdx.x * tkv::kWaveWG + wave;
-    const int e0 = woff[w], e1 = woff[w + 1], T = wtiles[w];
-    if (e0 >= e1) return;  // waves are independent: no barrier follows
+    const int T = wtiles[w];
+    if (T == 0) return;
+    const WaveList L{w, woff[w], woff[w + 1] - woff[w] + 1};
+    uint8_t* vs = smem + wave * (32 * VROW);
     if (T == 1)
-        wave_run_pair<D, 1>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
-    else if (T == 2)
-        wave_run_pair<D, 2>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
+        wave_run_pair<D, 1>(wdesc, L, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, vs, lane);
     else
-        wave_run<D, 3>(wdesc, e0, e1, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, Vs[wave], lane);
+        wave_run_pair<D, 2>(wdesc, L, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, vs, lane);
 }
 
 // ============================================================================ tile kernel
@@ -593,23 +533,28 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// One workgroup per item: a tile of up to 128 query rows (wave w owns rows 32w .. 32w+31 as two
+// One workgroup per tile item: a tile of up to 128 query rows (wave w owns rows 32w .. 32w+31 as two
 // column tiles) against the item's key blocks, four blocks per stage.  Stage s+1 is fetched into
 // registers while stage s is contracted from LDS; one barrier per stage (the two LDS buffers
 // alternate, so a buffer is rewritten only after every wave has passed the barrier that follows
 // its last use).
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_tile(
-    const tkv::ItemDesc* __restrict__ items, const tkv::TokDesc* __restrict__ toks,
-    const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
-    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
-    float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
+constexpr int tile_smem_bytes() {
+    return 2 * 64 * (D + 8) * 2 + 2 * 64 * (2 * D + 32);
+}
+
+template <int D>
+__device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::TokDesc* __restrict__ toks,
+                                          const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q,
+                                          const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
+                                          uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
+                                          float* __restrict__ plse, int hq, int hkv, int G, float sl2, uint8_t* smem) {
     constexpr int T = 2;
     constexpr int KSTR = D + 8;       // K row stride (elements): 16-byte reads of 16 rows hit distinct banks
     constexpr int VROW = 2 * D + 32;  // V row stride (bytes): transposed 8-byte reads spread over the banks
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][64 * KSTR];
-    __shared__ __attribute__((aligned(16))) uint8_t Vs[2][64 * VROW];
-    const tkv::ItemDesc it = items[blockIdx.x];
+    // two stage buffers: K [2][64][KSTR] bf16, then V [2][64][VROW] bytes
+    uint16_t* const ks_base = reinterpret_cast<uint16_t*>(smem);
+    uint8_t* const vs_base = smem + 2 * 64 * KSTR * 2;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, kg = lane >> 4;
@@ -619,25 +564,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int nb = it.n_blk;
     const int n_stages = (nb + 3) / 4;
 
-    // this lane's query row of each column tile
+    // this lane's query row of each column tile (only Q and the causal limits stay live across the
+    // stages; the output fields are read again from the token descriptors at the end)
     bf16x8_t qf[T][D / 32];
-    int limit[T], qtok[T], slot[T], h[T];
-    bool ok[T];
+    int limit[T];
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) {
         const int row = 32 * wave + 16 * tt + col;
         const int t = row / G;
-        ok[tt] = t < it.n_tok;
         const tkv::TokDesc td = toks[it.tok_off + min(t, it.n_tok - 1)];
-        qtok[tt] = td.qtok;
-        limit[tt] = ok[tt] ? td.limit : -1;
-        slot[tt] = td.slot;
-        h[tt] = it.kvh * G + (row - t * G);
-        const uint16_t* qrow = q + (static_cast<size_t>(qtok[tt]) * hq + h[tt]) * D + kg * 8;
+        limit[tt] = t < it.n_tok ? td.limit : -1;
+        const uint16_t* qrow = q + (static_cast<size_t>(td.qtok) * hq + it.kvh * G + (row - t * G)) * D + kg * 8;
 #pragma unroll
         for (int ks = 0; ks < D / 32; ++ks) qf[tt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
     }
-    const bool wave_active = __builtin_amdgcn_ballot_w64(ok[0] || ok[1]) != 0;
+    const bool wave_active = __builtin_amdgcn_ballot_w64(limit[0] >= 0 || limit[1] >= 0) != 0;
 
     // block descriptors of a stage: lane l holds block 4s + (l & 3) (the item's last block past its end)
     auto stage_desc = [&](int st) { return bd[min(4 * st + (lane & 3), nb - 1)]; };
@@ -653,8 +594,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     int pos = it.pos0;
     for (int st = 0; st < n_stages; ++st) {
         const int buf = st & 1;
-        uint16_t* ks = Ks[buf];
-        uint8_t* vs = Vs[buf];
+        uint16_t* ks = ks_base + buf * (64 * KSTR);
+        uint8_t* vs = vs_base + buf * (64 * VROW);
         stage_store<D, KSTR, VROW>(r, ks, vs, wave, lane);
         lds_barrier();
         // fetch the next stage while this one is contracted
@@ -697,7 +638,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         // causal limit falls inside the stage
         const int stage_end = pos;  // one past the last key position of the stage
         if (len[3] != 16 || len[0] + len[1] + len[2] != 48 ||
-            __builtin_amdgcn_ballot_w64((ok[0] && limit[0] < stage_end - 1) || (ok[1] && limit[1] < stage_end - 1)) != 0) {
+            __builtin_amdgcn_ballot_w64((limit[0] >= 0 && limit[0] < stage_end - 1) ||
+                                        (limit[1] >= 0 && limit[1] < stage_end - 1)) != 0) {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -731,10 +673,42 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     if (!wave_active) return;
 #pragma unroll
-    for (int tt = 0; tt < T; ++tt)
-        write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], ok[tt], qtok[tt], h[tt], slot[tt], kg, o, lse, po, plse, hq, sl2);
+    for (int tt = 0; tt < T; ++tt) {
+        const int row = 32 * wave + 16 * tt + col;
+        const int t = row / G;
+        const tkv::TokDesc td = toks[it.tok_off + min(t, it.n_tok - 1)];
+        write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], t < it.n_tok, td.qtok, it.kvh * G + (row - t * G), td.slot, kg, o,
+                      lse, po, plse, hq, sl2);
+    }
 }
 
+
+// The two attention kernels, launched back to back on the caller's stream: one workgroup per tile
+// item, and the wave grid (kWaveWG independent waves per workgroup, workgroup k on XCD k % 8 as
+// the planner assumed).  Separate kernels keep each one's register allocation to its own path.
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_tile(
+    const tkv::ItemDesc* __restrict__ items, const tkv::TokDesc* __restrict__ toks,
+    const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
+    float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
+    __shared__ __attribute__((aligned(16))) uint8_t smem[tile_smem_bytes<D>()];
+    const tkv::ItemDesc it = items[blockIdx.x];
+    tile_item<D>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, smem);
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * tkv::kWaveWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_wave(
+    const int4* __restrict__ wdesc, const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
+    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq,
+    int hkv, int G, float sl2) {
+    __shared__ __attribute__((aligned(16))) uint8_t smem[tkv::kWaveWG * 32 * (2 * D + 32)];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    wave_worker<D>(blockIdx.x * tkv::kWaveWG + wave, wave, lane, wdesc, woff, wtiles, q, kpool, vpool, o, lse, po,
+                   plse, hq, hkv, G, sl2, smem);
+}
 
 // Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
 // are contiguous): every thread owns float4 columns of one head and folds the partials in with an
@@ -832,17 +806,17 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     if (p->prof_n < p->prof_max) ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 4 * p->prof_n++;
     const int n_tile = static_cast<int>(p->items.size());
     const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of kWaveWG
-    hipEvent_t main_start = ev ? ev[0] : nullptr, main_stop = ev ? ev[1] : nullptr;
     if (n_tile > 0)
-        hipExtLaunchKernelGGL(attn_tile<D>, dim3(static_cast<unsigned>(n_tile)), dim3(kThreads), 0, st, main_start,
-                              n_wave > 0 ? nullptr : main_stop, 0, items, toks, blks, static_cast<const uint16_t*>(q),
-                              static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                              static_cast<uint16_t*>(o), lse, po, plse, hq, hkv, p->group, sl2);
+        hipExtLaunchKernelGGL(attn_tile<D>, dim3(static_cast<unsigned>(n_tile)), dim3(kThreads), 0, st,
+                              ev ? ev[0] : nullptr, n_wave > 0 || !ev ? nullptr : ev[1], 0, items, toks, blks,
+                              static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                              static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
+                              p->group, sl2);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
     if (n_wave > 0)
-        hipExtLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / kWaveWG)), dim3(64 * kWaveWG), 0, st,
-                              n_tile > 0 ? nullptr : main_start, main_stop, 0, wdesc, woff, wtiles,
+        hipExtLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / kWaveWG)), dim3(64 * kWaveWG), 0,
+                              st, n_tile > 0 || !ev ? nullptr : ev[0], ev ? ev[1] : nullptr, 0, wdesc, woff, wtiles,
                               static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                               static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
                               p->group, sl2);

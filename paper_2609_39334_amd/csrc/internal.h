@@ -25,9 +25,11 @@ constexpr int kItemShared = 0;  // tile of several rows' tokens over one segment
 constexpr int kItemRow = 1;     // tile of one row's tokens over its whole path (workgroup kernel)
 constexpr int kItemWave = 2;    // tile of <= 16 T rows over one segment chunk (wave kernel)
 constexpr int kWaveRows = 16;   // query rows of one MFMA column tile of the wave kernel
-constexpr int kWaveMaxTiles = 3;  // column tiles a wave contracts against each K/V block
+constexpr int kWaveMaxTiles = 2;  // column tiles a wave contracts against each K/V block
+constexpr int kWaveMaxRows = 96;  // widest chunk (query rows) the wave kernel takes; wider ones use 128-row tiles
+constexpr int kTileMinItems = 256;  // wide chunks go to the tile kernel only if they make this many items
 constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
-constexpr int kWaveToks = 48;   // query tokens of a wave-kernel item (16 kWaveMaxTiles / G)
+constexpr int kWaveToks = 48;   // token slots of a wave-kernel record (>= 16 kWaveMaxTiles / G)
 constexpr int kWaveWorkers = 2048;  // waves of the wave kernel: 2 workgroups of kWaveWG on each of 256 CUs
 constexpr int kWaveWG = 4;      // waves per workgroup of the wave kernel (independent; no barriers)
 
@@ -90,9 +92,10 @@ struct tkv_plan {
     std::vector<tkv::BlkDesc> blks;
     std::vector<tkv::MergeDesc> merges;
     std::vector<int32_t> merge_slots;
-    std::vector<tkv::WaveDesc> wave_desc;     // wave-kernel items, each wave's list contiguous
-    std::vector<int32_t> wave_off;            // [n_waves + 1] each wave's range in wave_desc
-    std::vector<int32_t> wave_tiles;          // [n_waves] column tiles of every item of the wave
+    std::vector<tkv::WaveDesc> wave_desc;     // wave-kernel items: record w is wave w's first item,
+                                              // then each wave's further items contiguously
+    std::vector<int32_t> wave_off;            // [n_waves + 1] wave w's further items: [off[w], off[w+1])
+    std::vector<int32_t> wave_tiles;          // [n_waves] column tiles of the wave's items (0: no work)
     int32_t n_slots = 0;
     // workspace layout (byte offsets)
     size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wdesc = 0, off_woff = 0, off_wtiles = 0;

@@ -41,7 +41,8 @@ using tkv::TokDesc;
 
 namespace {
 
-constexpr int kChunkBlocks = 16;  // longest key run of one shared item (256 tokens)
+constexpr int kChunkBlocks = 16;      // longest key run of a narrow shared item (256 tokens)
+constexpr int kChunkBlocksWide = 64;  // longest key run of a wide (128-row tile) shared item
 static_assert(kChunkBlocks <= tkv::kWaveBlocks, "a wave item holds its key blocks in one record");
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -190,6 +191,23 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         }
         st.n_segments = static_cast<int32_t>(segs.size());
 
+        // Segments read by more than kWaveMaxRows query rows go to the 128-row tile kernel -- but
+        // only if they make enough tile items to fill the chip by themselves (the tile kernel runs
+        // before the wave kernel, not beside it); otherwise everything with G <= 16 stays on the
+        // wave kernel.
+        int64_t wave_max_rows = tkv::kWaveMaxRows;
+        if (const char* env = std::getenv("TKV_WAVE_MAX_ROWS")) wave_max_rows = std::atoll(env);
+        if (G <= tkv::kWaveRows) {
+            int64_t wide_items = 0;
+            for (const Segment& sg : segs) {
+                int64_t seg_tok = 0;
+                for (int32_t r : sg.rows) seg_tok += L[r];
+                if (seg_tok * G <= wave_max_rows) continue;
+                const int64_t nb = static_cast<int64_t>(sg.nodes.size());
+                wide_items += (nb + kChunkBlocksWide - 1) / kChunkBlocksWide * ((seg_tok + tpt - 1) / tpt) * s.hkv;
+            }
+            if (wide_items < tkv::kTileMinItems) wave_max_rows = int64_t{1} << 40;
+        }
         std::vector<Chunk> chunks;
         std::vector<int32_t> cover(st.n_qtok, 0);
         for (const Segment& sg : segs) {
@@ -197,7 +215,12 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
             const int32_t nb = static_cast<int32_t>(sg.nodes.size());
             const int32_t seg_blk_off = static_cast<int32_t>(p->blks.size());
             for (int32_t nd : sg.nodes) p->blks.push_back(BlkDesc{nodes[nd].blk, nodes[nd].len});
-            tile_evenly(nb, kChunkBlocks, [&](int32_t a, int32_t e) {
+            // segments read by many query rows go to the 128-row tile kernel in long chunks; the
+            // rest to the wave kernel in chunks that fit its records
+            int64_t seg_rows = 0;
+            for (int32_t r : sg.rows) seg_rows += static_cast<int64_t>(L[r]) * G;
+            const bool wide = G > tkv::kWaveRows || seg_rows > wave_max_rows;
+            tile_evenly(nb, wide ? kChunkBlocksWide : kChunkBlocks, [&](int32_t a, int32_t e) {
                 Chunk c;
                 c.blk_off = seg_blk_off + a;
                 c.n_blk = e - a;
@@ -227,15 +250,13 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 if (cover[t.qtok] > 1) t.slot = slot_next[t.qtok]++;
         p->merge_slots.resize(p->n_slots);
         std::iota(p->merge_slots.begin(), p->merge_slots.end(), 0);
-        // Chunks of groups with G <= 16 go to the wave kernel: a wave contracts each K/V block
-        // against T column tiles of 16 rows (T = 1..3 as the chunk's rows need), so a chunk of
-        // up to 48 rows is read once.  Chunks wider than TKV_WAVE_MAX_ROWS (and groups with
-        // G > 16) use the workgroup kernel's 64-row tiles.
-        int64_t wave_max_rows = int64_t{1} << 40;
-        if (const char* env = std::getenv("TKV_WAVE_MAX_ROWS")) wave_max_rows = std::atoll(env);
+        // Chunks of groups with G <= 16 and at most kWaveMaxRows query rows go to the wave kernel:
+        // a wave contracts each K/V block against T column tiles of 16 rows (T = 1, 2 as the
+        // chunk's rows need).  Wider chunks (and groups with G > 16) use the workgroup kernel's
+        // 128-row tiles, which stage each K/V block once for 128 rows.
         for (const Chunk& c : chunks) {
             const int64_t rows = static_cast<int64_t>(c.toks.size()) * G;
-            const bool wave = G <= tkv::kWaveRows && rows <= wave_max_rows;
+            const bool wave = G <= tkv::kWaveRows && rows <= wave_max_rows && c.n_blk <= kChunkBlocks;
             const int32_t T = static_cast<int32_t>(std::min<int64_t>(tkv::kWaveMaxTiles, (rows + 15) / 16));
             const int32_t per_tile = wave ? tkv::kWaveRows * T / G : tpt;
             tile_evenly(static_cast<int32_t>(c.toks.size()), per_tile, [&](int32_t a, int32_t e) {
@@ -390,38 +411,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
             for (auto& v : xcd_waves) n_total += v.size();
             const size_t n_slots_w = (n_total + tkv::kWaveWG - 1) / tkv::kWaveWG * tkv::kWaveWG;
             std::vector<size_t> next(kXcds, 0);
-            p->wave_off.assign(1, 0);
-            auto emit = [&](const Wave* wv) {
-                if (wv) {
-                    for (int32_t i : wv->items) {
-                        const ItemDesc& it = p->wave_items[i];
-                        // widths 1 and 2 walk blocks in pairs: an odd key list gets an empty block
-                        const int32_t nb_run = it.pad <= 2 ? (it.n_blk + 1) & ~1 : it.n_blk;
-                        tkv::WaveDesc wd{};
-                        int32_t pos = it.pos0;
-                        for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
-                            const bool in = j < it.n_blk;
-                            const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
-                            wd.e[4 * j] = bd.blk;
-                            wd.e[4 * j + 1] = in ? bd.len : 0;
-                            wd.e[4 * j + 2] = pos;
-                            if (in) pos += bd.len;
-                        }
-                        wd.e[3] = it.kvh;
-                        wd.e[7] = it.n_tok;
-                        wd.e[11] = nb_run;
-                        for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
-                            const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
-                            wd.e[4 * (16 + t)] = td.qtok;
-                            wd.e[4 * (16 + t) + 1] = td.limit;
-                            wd.e[4 * (16 + t) + 2] = td.slot;
-                        }
-                        p->wave_desc.push_back(wd);
-                    }
-                }
-                p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
-                p->wave_tiles.push_back(wv ? wv->T : 1);
-            };
+            std::vector<const Wave*> slots(n_slots_w, nullptr);
             for (size_t slot = 0; slot < n_slots_w; ++slot) {
                 const int32_t x = static_cast<int32_t>((slot / tkv::kWaveWG) % kXcds);
                 int32_t src = x;
@@ -434,7 +424,45 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                             src = y;
                         }
                 }
-                emit(src >= 0 ? &xcd_waves[src][next[src]++] : nullptr);
+                if (src >= 0) slots[slot] = &xcd_waves[src][next[src]++];
+            }
+            auto record = [&](const ItemDesc& it) {
+                // widths 1 and 2 walk blocks in pairs: an odd key list gets an empty block
+                const int32_t nb_run = it.pad <= 2 ? (it.n_blk + 1) & ~1 : it.n_blk;
+                tkv::WaveDesc wd{};
+                int32_t pos = it.pos0;
+                for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
+                    const bool in = j < it.n_blk;
+                    const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
+                    wd.e[4 * j] = bd.blk;
+                    wd.e[4 * j + 1] = in ? bd.len : 0;
+                    wd.e[4 * j + 2] = pos;
+                    if (in) pos += bd.len;
+                }
+                wd.e[3] = it.kvh;
+                wd.e[7] = it.n_tok;
+                wd.e[11] = nb_run;
+                for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
+                    const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
+                    wd.e[4 * (16 + t)] = td.qtok;
+                    wd.e[4 * (16 + t) + 1] = td.limit;
+                    wd.e[4 * (16 + t) + 2] = td.slot;
+                }
+                return wd;
+            };
+            // Wave w's first item is record w (so the wave's first load depends on nothing); its
+            // other items follow all first records, as the range [wave_off[w], wave_off[w + 1]).
+            p->wave_desc.assign(n_slots_w, tkv::WaveDesc{});
+            for (size_t w = 0; w < n_slots_w; ++w)
+                if (slots[w] && !slots[w]->items.empty()) p->wave_desc[w] = record(p->wave_items[slots[w]->items[0]]);
+            p->wave_off.assign(1, static_cast<int32_t>(n_slots_w));
+            for (size_t w = 0; w < n_slots_w; ++w) {
+                const bool busy = slots[w] && !slots[w]->items.empty();
+                if (busy)
+                    for (size_t k = 1; k < slots[w]->items.size(); ++k)
+                        p->wave_desc.push_back(record(p->wave_items[slots[w]->items[k]]));
+                p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
+                p->wave_tiles.push_back(busy ? slots[w]->T : 0);
             }
         }
         st.n_items_wave = static_cast<int32_t>(p->wave_items.size());
