@@ -11,7 +11,8 @@
 //    tile and contracted against all of them.  Each (token, chunk) result is a partial (o, lse)
 //    that a log-sum-exp merge combines -- unless the chunk is the token's only one, in which case
 //    the item writes the final output.  With G <= 16 these items go to the wave kernel (tiles of
-//    up to 48 rows, per-wave work lists built here); otherwise to the workgroup kernel.
+//    up to 32 rows, per-wave work lists built here); segments read by many rows (and G > 16)
+//    go to the workgroup kernel's 128-row tiles.
 //  * row items, for rows whose own query tokens fill a tile (verify rows with q_len * G >=
 //    kTileRows).  A workgroup-kernel tile of one row's tokens (128 rows) walks the row's whole
 //    path, truncated at the tile's largest causal limit, and writes the final output; the shared
