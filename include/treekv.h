@@ -113,7 +113,7 @@ int tkv_bm_coalesce(const tkv_bm* bm, int32_t n_cand, const int32_t* seqs, const
 
 /* ======================================================================== attention
  * One attention layer over the paged cache for a batch of rows (Sec. 2.1 attention; decode of
- * every live candidate, Sec. 3.2.1; prefill-only step verification, Sec. 3.2.2).  For row r with
+ * every live candidate and single-pass step verification, Sec. 3.2).  For row r with
  * block table T, q_len L and kv_len N = sum of block_len over T, query token i (0 <= i < L) and
  * query head h (kv head h / (hq/hkv)) attend keys 0 .. N-L+i of the path (bottom-right causal;
  * decode is L = 1 and sees all N keys):
@@ -141,7 +141,11 @@ typedef struct tkv_plan tkv_plan;
  * The planner finds the blocks that several rows share (a trie over the tables) so that each
  * shared K/V block is contracted against all query rows that reference it, splits long runs,
  * and lays out descriptors for the device.  EINVAL: bad shape, q_len < 1, q_len > kv_len, a block
- * id out of range or with block_len outside [1, block_size], multiplicity < 1. */
+ * id out of range or with block_len outside [1, block_size], multiplicity < 1.
+ * Work placement can be tuned through the environment, read at each call (the results do not
+ * depend on it): TKV_WAVE_MAX_ROWS (widest shared chunk, in query rows, kept on the wave kernel;
+ * default 96), TKV_TILE_MIN_ITEMS (wider chunks go to 128-row tiles only if they make at least
+ * this many; default 256), TKV_WAVES (size of the wave grid; default 2048). */
 int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
                     const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
                     const int32_t* multiplicity, tkv_plan** out);

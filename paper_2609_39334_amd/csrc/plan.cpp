@@ -207,7 +207,9 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 const int64_t nb = static_cast<int64_t>(sg.nodes.size());
                 wide_items += (nb + kChunkBlocksWide - 1) / kChunkBlocksWide * ((seg_tok + tpt - 1) / tpt) * s.hkv;
             }
-            if (wide_items < tkv::kTileMinItems) wave_max_rows = int64_t{1} << 40;
+            int64_t min_items = tkv::kTileMinItems;
+            if (const char* env = std::getenv("TKV_TILE_MIN_ITEMS")) min_items = std::atoll(env);
+            if (wide_items < min_items) wave_max_rows = int64_t{1} << 40;
         }
         std::vector<Chunk> chunks;
         std::vector<int32_t> cover(st.n_qtok, 0);
@@ -303,8 +305,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         // dispatched round-robin over the 8 XCDs (each with its own L2), so wave w runs on XCD
         // (w / kWaveWG) % 8: all tiles of one (chunk, KV head), which read the same K/V blocks, go
         // to one XCD.  Groups are assigned to XCDs, and items to the XCD's waves, longest
-        // processing time first; each XCD's heaviest waves take its first workgroups, which the
-        // dispatcher starts first.
+        // processing time first.
         {
             constexpr int32_t kXcds = 8;
             const int32_t n_items = static_cast<int32_t>(p->wave_items.size());
@@ -352,11 +353,17 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                     if (frac[best] < 0.0 && per_xt[best] < cap) frac[best] = 0.0;
                 }
             }
+            // Each XCD's wave positions are shared out evenly among the widths (interleaved in
+            // launch order); items go to the waves of their width longest processing time first.
+            struct Slot {
+                int32_t T;
+                double key;
+            };
             std::vector<std::vector<Wave>> xcd_waves(kXcds);
+            std::vector<std::vector<std::vector<int32_t>>> xcd_items_t(kXcds, std::vector<std::vector<int32_t>>(tkv::kWaveMaxTiles + 1));
             for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
                 const std::vector<int32_t>& its = by_t[T];
                 if (its.empty()) continue;
-                const int32_t per_x = per_xt[T];
                 std::map<std::pair<int32_t, int32_t>, int32_t> gid;
                 std::vector<std::vector<int32_t>> groups;
                 std::vector<int64_t> gcost;
@@ -376,24 +383,36 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 using Load = std::pair<int64_t, int32_t>;
                 std::priority_queue<Load, std::vector<Load>, std::greater<Load>> xheap;
                 for (int32_t x = 0; x < kXcds; ++x) xheap.push({0, x});
-                std::vector<std::vector<int32_t>> xcd_items(kXcds);
                 for (int32_t g2 : gorder) {
                     Load l = xheap.top();
                     xheap.pop();
-                    xcd_items[l.second].insert(xcd_items[l.second].end(), groups[g2].begin(), groups[g2].end());
+                    auto& dst = xcd_items_t[l.second][T];
+                    dst.insert(dst.end(), groups[g2].begin(), groups[g2].end());
                     l.first += gcost[g2];
                     xheap.push(l);
                 }
-                for (int32_t x = 0; x < kXcds; ++x) {
-                    if (xcd_items[x].empty()) continue;
-                    std::stable_sort(xcd_items[x].begin(), xcd_items[x].end(), [&](int32_t a2, int32_t b2) {
+            }
+            for (int32_t x = 0; x < kXcds; ++x) {
+                // this XCD's waves of each width, their positions interleaved in launch order
+                std::vector<Slot> slots_x;
+                for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
+                    const int32_t nw = std::min<int32_t>(per_xt[T], static_cast<int32_t>(xcd_items_t[x][T].size()));
+                    for (int32_t k = 0; k < nw; ++k) slots_x.push_back(Slot{T, (k + 0.5) / nw});
+                }
+                std::stable_sort(slots_x.begin(), slots_x.end(), [](const Slot& a2, const Slot& b2) { return a2.key < b2.key; });
+                std::vector<Wave> ws(slots_x.size());
+                for (size_t j = 0; j < slots_x.size(); ++j) ws[j] = Wave{slots_x[j].T, 0, {}};
+                for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
+                    auto& items_t = xcd_items_t[x][T];
+                    if (items_t.empty()) continue;
+                    std::stable_sort(items_t.begin(), items_t.end(), [&](int32_t a2, int32_t b2) {
                         return p->wave_items[a2].n_blk > p->wave_items[b2].n_blk;
                     });
-                    const int32_t nw = std::min<int32_t>(per_x, static_cast<int32_t>(xcd_items[x].size()));
-                    std::vector<Wave> ws(nw, Wave{T, 0, {}});
+                    using Load = std::pair<int64_t, int32_t>;
                     std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-                    for (int32_t w = 0; w < nw; ++w) heap.push({0, w});
-                    for (int32_t i : xcd_items[x]) {
+                    for (size_t j = 0; j < ws.size(); ++j)
+                        if (ws[j].T == T) heap.push({0, static_cast<int32_t>(j)});
+                    for (int32_t i : items_t) {
                         Load l = heap.top();
                         heap.pop();
                         ws[l.second].items.push_back(i);
@@ -401,13 +420,11 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                         l.first += cost(p->wave_items[i]);
                         heap.push(l);
                     }
-                    xcd_waves[x].insert(xcd_waves[x].end(), ws.begin(), ws.end());
                 }
+                xcd_waves[x] = std::move(ws);
             }
-            // launch order: workgroup k holds kWaveWG waves of XCD k % 8, heaviest first; an XCD
+            // launch order: workgroup k holds kWaveWG waves of XCD k % 8, in position order; an XCD
             // whose list has run out lends its slots to the longest remaining list
-            for (auto& v : xcd_waves)
-                std::stable_sort(v.begin(), v.end(), [](const Wave& a2, const Wave& b2) { return a2.cost > b2.cost; });
             size_t n_total = 0;
             for (auto& v : xcd_waves) n_total += v.size();
             const size_t n_slots_w = (n_total + tkv::kWaveWG - 1) / tkv::kWaveWG * tkv::kWaveWG;

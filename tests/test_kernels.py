@@ -137,3 +137,36 @@ def test_mixed_serving_both_launches_sampled():
         rng = np.random.default_rng(2 + launch)
         rows = sorted(rng.choice(len(b.q_lens), 40, replace=False).tolist())
         compare(wl, launch, rows=rows, poison=False)
+
+
+@pytest.mark.parametrize("seed,hq,hkv,d", [(10, 8, 2, 64), (11, 12, 2, 128), (12, 16, 1, 128), (13, 6, 6, 64)])
+def test_shared_chunks_on_tile_kernel(seed, hq, hkv, d, monkeypatch):
+    # every shared chunk read by more than 8 query rows goes to the 128-row tile kernel (partials,
+    # merges and per-token causal limits included), the narrow rest to the wave kernel
+    monkeypatch.setenv("TKV_WAVE_MAX_ROWS", "8")
+    monkeypatch.setenv("TKV_TILE_MIN_ITEMS", "0")
+    wl = W.random_tree(seed, W.Shape(hq, hkv, d), n_roots=3, depth=3, max_branch=4, max_step=60)
+    b, st = compare(wl, 0)
+    assert st["n_items_shared"] - st["n_items_wave"] > 0     # shared chunks did run on the tile kernel
+
+
+@pytest.mark.parametrize("waves", ["8", "64"])
+def test_small_wave_grids(waves, monkeypatch):
+    # a wave grid much smaller than the item count: long per-wave lists, items crossing into the
+    # next item's first blocks many times per wave
+    monkeypatch.setenv("TKV_WAVES", waves)
+    wl = W.random_tree(20, W.Shape(12, 2, 128), n_roots=4, depth=3, max_branch=3, max_step=70)
+    b, st = compare(wl, 0)
+    assert 0 < st["n_waves"] < st["n_items_wave"]            # waves walk lists of several items
+
+
+def test_empty_plan_on_gpu():
+    import paper_2609_39334_amd as tkv
+    plan = tkv.Plan((8, 2, 64, 16, 4), [0], [0], [], [16, 3, 0, 0])
+    q = torch.zeros((1, 8, 64), dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros((4, 2, 16, 64), dtype=torch.bfloat16, device="cuda")
+    o = torch.full((1, 8, 64), 7.0, dtype=torch.bfloat16, device="cuda")
+    plan.decode(q, kv, kv, o, None)
+    plan.verify(q, kv, kv, o, None)
+    torch.cuda.synchronize()
+    assert (o.float() == 7.0).all()          # no row, nothing written
