@@ -22,6 +22,7 @@
 
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include "internal.h"
@@ -711,11 +712,11 @@ __global__ __launch_bounds__(64 * tkv::kWaveWG) __attribute__((amdgpu_waves_per_
 }
 
 // Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
-// are contiguous): every thread owns float4 columns of one head and folds the partials in with an
-// online softmax, eight partials' outputs and lse values in flight at a time -- one round of
-// memory latency per eight partials, no barriers.
+// are contiguous, sized to one thread per float4 column of the token's heads): every thread folds
+// the partials of its column in with an online softmax, eight partials' outputs and lse values in
+// flight at a time -- one round of memory latency per eight partials, no barriers.
 template <int D>
-__global__ __launch_bounds__(kThreads) void merge_partials(const tkv::MergeDesc* __restrict__ md,
+__global__ __launch_bounds__(1024) void merge_partials(const tkv::MergeDesc* __restrict__ md,
                                                            const float* __restrict__ po,
                                                            const float* __restrict__ plse,
                                                            uint16_t* __restrict__ o, float* __restrict__ lse, int hq) {
@@ -724,7 +725,7 @@ __global__ __launch_bounds__(kThreads) void merge_partials(const tkv::MergeDesc*
     const size_t s0 = static_cast<size_t>(m.slot_off);
     const int n = m.n_slots;
     const float4* po4 = reinterpret_cast<const float4*>(po);
-    for (int idx = threadIdx.x; idx < hq * C4; idx += kThreads) {
+    for (int idx = threadIdx.x; idx < hq * C4; idx += blockDim.x) {
         const int h = idx / C4;
         float mx = -INFINITY, sum = 0.f;
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -823,7 +824,9 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
     if (!p->merges.empty()) {
-        hipExtLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(kThreads), 0, st,
+        // one thread per float4 column of the token's heads (up to 1024 threads)
+        const int merge_threads = std::min(1024, (hq * (D / 4) + 63) / 64 * 64);
+        hipExtLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(merge_threads), 0, st,
                               ev ? ev[2] : nullptr, ev ? ev[3] : nullptr, 0, merges,
                               static_cast<const float*>(po), static_cast<const float*>(plse),
                               static_cast<uint16_t*>(o), lse, hq);
