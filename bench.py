@@ -158,8 +158,7 @@ def main():
             tr = json.load(f).get(a.workload)
         if tr and tr.get("sources_sha256") == kernel_sources_digest():
             traffic = tr.get("bytes_per_launch")
-    main_kernels = ([] if st["n_items"] == st["n_items_wave"] else ["attn_tile"]) + \
-                   (["attn_wave"] if st["n_items_wave"] else [])
+    main_kernels = ["attn_fwd"]  # tile items and the wave grid in one launch
     # the bound is the one the work's arithmetic intensity puts it under (ridge: peak flop/s over
     # peak bytes/s); decode is HBM-bound, multi-token verify of long steps is MFMA-bound
     mfma_bound = flops / b_uniq > MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)

@@ -1,20 +1,23 @@
 // Tree-shared paged attention kernels for gfx950 (MI355X).
 //
-// Every kernel contracts a tile of query rows -- query tokens x the G query heads of one KV head --
-// against an ordered list of 16-token K/V blocks on bf16 MFMA with fp32 accumulation, computing the
-// transposed products so that each lane keeps one query row throughout:
+// Every work item contracts a tile of query rows -- query tokens x the G query heads of one KV
+// head -- against an ordered list of 16-token K/V blocks on bf16 MFMA with fp32 accumulation,
+// computing the transposed products so that each lane keeps one query row throughout:
 //   S^T = K Q^T     v_mfma_f32_16x16x32_bf16 (A = 16 keys x 32 dims, B = Q^T held in registers),
-//   O^T += V^T P^T  v_mfma_f32_16x16x16_bf16 (A = V^T read transposed from LDS with
-//                   ds_read_b64_tr_b16, B = P^T exactly as the S^T result sits in the lanes),
-// with an online softmax in between (exp2 with the scale folded into one FMA; O rescaled only when
-// a row's running max moves).  Keys past a block's length are never loaded (row reads are clamped
-// to the block's last token and masked) and keys past a token's causal limit get -inf.
+//   O^T += V^T P^T  v_mfma_f32_16x16x32_bf16 over two blocks at a time (A = V^T of both blocks read
+//                   transposed from LDS with ds_read_b64_tr_b16, B = P^T exactly as the two S^T
+//                   results sit in the lanes),
+// with an online softmax in between (exp2 with the scale folded into one FMA; the exponent base of
+// a row moves only when its maximum grows by more than 2^8, so O is rarely rescaled).  Keys past a
+// block's length are never loaded (row reads are clamped to the block's last token and masked) and
+// keys past a token's causal limit get -inf.
 //
-// attn_wave:  decode-shaped work (G <= 16, chunks of at most kWaveMaxRows rows): every wave is an
+// attn_fwd runs two kinds of work items in one launch:
+// wave grid:  decode-shaped work (G <= 16, chunks of at most kWaveMaxRows rows): every wave is an
 //             independent worker walking its own list of items, each a tile of up to 32 rows over a
 //             chunk of <= 16 blocks, with the next two blocks always in flight; no LDS sharing
 //             between waves, no barriers.
-// attn_tile:  wide tiles (multi-token verify rows, wide shared chunks, G > 16): one workgroup of
+// tile items: wide tiles (multi-token verify rows, wide shared chunks, G > 16): one workgroup of
 //             four waves per item, 128 rows (32 per wave) against 64-key stages of K/V
 //             double-buffered through LDS.
 // merge_partials: log-sum-exp merge of the partial results of a query token's chunks:
@@ -492,7 +495,6 @@ __device__ __forceinline__ void wave_worker(int w, int wave, int lane, const int
 }
 
 // ============================================================================ tile kernel
-constexpr int kTileRowsWG = 128;  // query rows of an attn_tile item (4 waves x 2 column tiles x 16)
 
 // One 64-key stage (4 blocks) of K/V, each wave fetching one block: lane l reads 16 bytes of rows
 // 4i + l/16 (clamped to the block's last token), so each load instruction covers 1 KB of the
@@ -684,31 +686,29 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
 }
 
 
-// The two attention kernels, launched back to back on the caller's stream: one workgroup per tile
-// item, and the wave grid (kWaveWG independent waves per workgroup, workgroup k on XCD k % 8 as
-// the planner assumed).  Separate kernels keep each one's register allocation to its own path.
+// The attention kernel: workgroups [0, n_tile) take one tile item each (longest first, in the
+// planner's XCD order), workgroups [n_tile_pad, ...) hold kWaveWG waves of the wave grid each
+// (n_tile_pad, a multiple of 8, keeps the wave grid's workgroup-to-XCD assignment that the
+// planner assumed).  One launch covers both kinds of work, so neither waits for the other's tail.
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_tile(
-    const tkv::ItemDesc* __restrict__ items, const tkv::TokDesc* __restrict__ toks,
-    const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd(
+    const tkv::ItemDesc* __restrict__ items, int n_tile, int n_tile_pad, const tkv::TokDesc* __restrict__ toks,
+    const tkv::BlkDesc* __restrict__ blks, const int4* __restrict__ wdesc, const int32_t* __restrict__ woff,
+    const int32_t* __restrict__ wtiles, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
     const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
     float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[tile_smem_bytes<D>()];
-    const tkv::ItemDesc it = items[blockIdx.x];
-    tile_item<D>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, smem);
-}
-
-template <int D>
-__global__ __launch_bounds__(64 * tkv::kWaveWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_wave(
-    const int4* __restrict__ wdesc, const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse, int hq,
-    int hkv, int G, float sl2) {
-    __shared__ __attribute__((aligned(16))) uint8_t smem[tkv::kWaveWG * 32 * (2 * D + 32)];
+    const int b = blockIdx.x;
+    if (b < n_tile) {
+        const tkv::ItemDesc it = items[b];
+        tile_item<D>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, smem);
+        return;
+    }
+    if (b < n_tile_pad) return;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    wave_worker<D>(blockIdx.x * tkv::kWaveWG + wave, wave, lane, wdesc, woff, wtiles, q, kpool, vpool, o, lse, po,
-                   plse, hq, hkv, G, sl2, smem);
+    wave_worker<D>((b - n_tile_pad) * tkv::kWaveWG + wave, wave, lane, wdesc, woff, wtiles, q, kpool, vpool, o, lse,
+                   po, plse, hq, hkv, G, sl2, smem);
 }
 
 // Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
@@ -807,21 +807,15 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     if (p->prof_n < p->prof_max) ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 4 * p->prof_n++;
     const int n_tile = static_cast<int>(p->items.size());
     const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of kWaveWG
-    if (n_tile > 0)
-        hipExtLaunchKernelGGL(attn_tile<D>, dim3(static_cast<unsigned>(n_tile)), dim3(kThreads), 0, st,
-                              ev ? ev[0] : nullptr, n_wave > 0 || !ev ? nullptr : ev[1], 0, items, toks, blks,
-                              static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+    const int n_tile_pad = (n_tile + 7) / 8 * 8;
+    const int grid = n_tile_pad + (n_wave > 0 ? n_wave / kWaveWG : 0);
+    if (grid > 0)
+        hipExtLaunchKernelGGL(attn_fwd<D>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, st,
+                              ev ? ev[0] : nullptr, ev ? ev[1] : nullptr, 0, items, n_tile, n_tile_pad, toks, blks,
+                              wdesc, woff, wtiles, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                               static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
                               p->group, sl2);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
-    if (n_wave > 0)
-        hipExtLaunchKernelGGL(attn_wave<D>, dim3(static_cast<unsigned>(n_wave / kWaveWG)), dim3(64 * kWaveWG), 0,
-                              st, n_tile > 0 || !ev ? nullptr : ev[0], ev ? ev[1] : nullptr, 0, wdesc, woff, wtiles,
-                              static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                              static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
-                              p->group, sl2);
-    e = hipGetLastError();
     if (e != hipSuccess) return set_error(TKV_EHIP, "attention launch: %s", hipGetErrorString(e));
     if (!p->merges.empty()) {
         // one thread per float4 column of the token's heads (up to 1024 threads)
