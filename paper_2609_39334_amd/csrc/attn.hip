@@ -247,6 +247,29 @@ __device__ __forceinline__ void softmax_pair_lazy(WaveAcc<D, T>& A, f32x4_t (&sa
     }
 }
 
+// The lazily moved exponent base for a whole 64-key stage (four blocks of already-masked scores):
+// a row's base moves only when the stage's maximum exceeds it by more than 2^8 in probability
+// scale (then O and l are rescaled), as in softmax_pair_lazy.
+template <int D, int T>
+__device__ __forceinline__ void stage_base(WaveAcc<D, T>& A, const f32x4_t (&sc)[4][T], float sl2) {
+    constexpr float kSlack = 8.f;
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mx = fmaxf(mx, fmaxf(fmaxf(sc[j][tt][0], sc[j][tt][1]), fmaxf(sc[j][tt][2], sc[j][tt][3])));
+        mx = rowmax4(mx);
+        if (__builtin_amdgcn_ballot_w64(mx != -INFINITY && (A.m[tt] == -INFINITY || (mx - A.m[tt]) * sl2 > kSlack)) != 0) {
+            const float m_new = fmaxf(A.m[tt], mx);
+            const float alpha = A.m[tt] == m_new ? 1.f : __builtin_amdgcn_exp2f((A.m[tt] - m_new) * sl2);
+            A.l[tt] *= alpha;
+#pragma unroll
+            for (int c = 0; c < D / 16; ++c) A.acc[tt][c] *= alpha;
+            A.m[tt] = m_new;
+        }
+    }
+}
+
 // Normalise one column tile's rows and write them: the final bf16 output and lse (slot < 0) or an
 // fp32 partial and its lse.  Lane holds columns 16ct + 4kg + r of its row; l is summed over the
 // four lanes of the row.
@@ -541,9 +564,18 @@ __device__ __forceinline__ void lds_barrier() {
 // registers while stage s is contracted from LDS; one barrier per stage (the two LDS buffers
 // alternate, so a buffer is rewritten only after every wave has passed the barrier that follows
 // its last use).
+// K row stride in LDS (elements) and V row stride (bytes) of a tile item's stage buffers.
+template <int D>
+constexpr int tile_kstr() {
+    return D + 16;
+}
+template <int D>
+constexpr int tile_vrow() {
+    return 2 * D + 32;
+}
 template <int D>
 constexpr int tile_smem_bytes() {
-    return 2 * 64 * (D + 8) * 2 + 2 * 64 * (2 * D + 32);
+    return 2 * 64 * tile_kstr<D>() * 2 + 2 * 64 * tile_vrow<D>();
 }
 
 template <int D>
@@ -553,8 +585,8 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
                                           uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
                                           float* __restrict__ plse, int hq, int hkv, int G, float sl2, uint8_t* smem) {
     constexpr int T = 2;
-    constexpr int KSTR = D + 8;       // K row stride (elements): 16-byte reads of 16 rows hit distinct banks
-    constexpr int VROW = 2 * D + 32;  // V row stride (bytes): transposed 8-byte reads spread over the banks
+    constexpr int KSTR = tile_kstr<D>();  // K row stride (elements): 16-byte reads of 16 rows spread over banks
+    constexpr int VROW = tile_vrow<D>();  // V row stride (bytes): transposed 8-byte reads spread over the banks
     // two stage buffers: K [2][64][KSTR] bf16, then V [2][64][VROW] bytes
     uint16_t* const ks_base = reinterpret_cast<uint16_t*>(smem);
     uint8_t* const vs_base = smem + 2 * 64 * KSTR * 2;
@@ -653,13 +685,32 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
                         if (4 * kg + x >= vlen) sc[j][tt][x] = -INFINITY;
                 }
         }
+        // the exponent base: one row-max and lazy-move decision per stage and tile, so that the
+        // exponentials and PV MFMAs of both pairs below form one branch-free block the scheduler can
+        // interleave (a stage past every causal limit of the wave is all -inf and adds nothing)
+        stage_base<D, T>(A, sc, sl2);
+        float msc[T];
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt) msc[tt] = A.m[tt] == -INFINITY ? 0.f : A.m[tt] * sl2;
 #pragma unroll
         for (int jp = 0; jp < 2; ++jp) {
             const int ja = 2 * jp, jb = 2 * jp + 1;
-            // skip a pair that no row of this wave may see (past every causal limit, or absent)
-            if (len[ja] == 0 || __builtin_amdgcn_ballot_w64(limit[0] >= bpos[ja] || limit[1] >= bpos[ja]) == 0) continue;
             bf16x8_t pb[T];
-            softmax_pair_lazy<D, T>(A, sc[ja], sc[jb], sl2, pb);
+#pragma unroll
+            for (int tt = 0; tt < T; ++tt) {
+                float psum = 0.f;
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    sc[ja][tt][x] = __builtin_amdgcn_exp2f(fmaf(sc[ja][tt][x], sl2, -msc[tt]));
+                    sc[jb][tt][x] = __builtin_amdgcn_exp2f(fmaf(sc[jb][tt][x], sl2, -msc[tt]));
+                    psum += sc[ja][tt][x] + sc[jb][tt][x];
+                }
+                A.l[tt] += psum;
+                pb[tt] = __builtin_bit_cast(bf16x8_t, uint4{pack_bf16x2(sc[ja][tt][0], sc[ja][tt][1]),
+                                                            pack_bf16x2(sc[ja][tt][2], sc[ja][tt][3]),
+                                                            pack_bf16x2(sc[jb][tt][0], sc[jb][tt][1]),
+                                                            pack_bf16x2(sc[jb][tt][2], sc[jb][tt][3])});
+            }
             const uint8_t* vra = vs + (16 * ja + 4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
             const uint8_t* vrb = vra + 16 * VROW;
 #pragma unroll
