@@ -255,11 +255,14 @@ __device__ __forceinline__ void stage_base(WaveAcc<D, T>& A, const f32x4_t (&sc)
     constexpr float kSlack = 8.f;
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) {
+        // each lane tests its own 16 scores against the base; the row maximum over the four lanes
+        // of a row is taken only when some lane needs the base moved (the four lanes of a row hold
+        // the same base, so a row needs a move exactly when one of its lanes does)
         float mx = -INFINITY;
 #pragma unroll
         for (int j = 0; j < 4; ++j) mx = fmaxf(mx, fmaxf(fmaxf(sc[j][tt][0], sc[j][tt][1]), fmaxf(sc[j][tt][2], sc[j][tt][3])));
-        mx = rowmax4(mx);
         if (__builtin_amdgcn_ballot_w64(mx != -INFINITY && (A.m[tt] == -INFINITY || (mx - A.m[tt]) * sl2 > kSlack)) != 0) {
+            mx = rowmax4(mx);
             const float m_new = fmaxf(A.m[tt], mx);
             const float alpha = A.m[tt] == m_new ? 1.f : __builtin_amdgcn_exp2f((A.m[tt] - m_new) * sl2);
             A.l[tt] *= alpha;
