@@ -145,7 +145,8 @@ typedef struct tkv_plan tkv_plan;
  * Work placement can be tuned through the environment, read at each call (the results do not
  * depend on it): TKV_WAVE_MAX_ROWS (widest shared chunk, in query rows, kept on the wave kernel;
  * default 96), TKV_TILE_MIN_ITEMS (wider chunks go to 128-row tiles only if they make at least
- * this many; default 256), TKV_WAVES (size of the wave grid; default 2048). */
+ * this many; default 0), TKV_WAVES (size of the wave grid; default 2048, less the 4 waves of
+ * each workgroup slot that the 128-row tiles take when they are fewer than the 512 slots). */
 int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
                     const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
                     const int32_t* multiplicity, tkv_plan** out);

@@ -27,7 +27,7 @@ constexpr int kItemWave = 2;    // tile of <= 16 T rows over one segment chunk (
 constexpr int kWaveRows = 16;   // query rows of one MFMA column tile of the wave kernel
 constexpr int kWaveMaxTiles = 2;  // column tiles a wave contracts against each K/V block
 constexpr int kWaveMaxRows = 96;  // widest chunk (query rows) the wave kernel takes; wider ones use 128-row tiles
-constexpr int kTileMinItems = 256;  // wide chunks go to the tile kernel only if they make this many items
+constexpr int kTileMinItems = 0;  // wide chunks go to the tile kernel only if they make this many items
 constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
 constexpr int kWaveToks = 48;   // token slots of a wave-kernel record (>= 16 kWaveMaxTiles / G)
 constexpr int kWaveWorkers = 2048;  // waves of the wave kernel: 2 workgroups of kWaveWG on each of 256 CUs

@@ -192,10 +192,11 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         }
         st.n_segments = static_cast<int32_t>(segs.size());
 
-        // Segments read by more than kWaveMaxRows query rows go to the 128-row tile kernel -- but
-        // only if they make enough tile items to fill the chip by themselves (the tile kernel runs
-        // before the wave kernel, not beside it); otherwise everything with G <= 16 stays on the
-        // wave kernel.
+        // Segments read by more than kWaveMaxRows query rows go to 128-row tile items, which read
+        // each K/V block once for all of those rows -- if they make at least kTileMinItems items
+        // (none by default: tile items and the wave grid share one launch, and the wave grid
+        // gives up the workgroup slots the tile items take); otherwise everything with G <= 16
+        // stays on the wave grid.
         int64_t wave_max_rows = tkv::kWaveMaxRows;
         if (const char* env = std::getenv("TKV_WAVE_MAX_ROWS")) wave_max_rows = std::atoll(env);
         if (G <= tkv::kWaveRows) {
@@ -309,7 +310,13 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         {
             constexpr int32_t kXcds = 8;
             const int32_t n_items = static_cast<int32_t>(p->wave_items.size());
+            // The tile items share the launch with the wave grid and hold a workgroup slot each
+            // (two per CU); when they are fewer than the slots, the wave grid takes the slots they
+            // leave (at least half), so that no wave workgroup waits for a tile item to finish.
+            const int32_t wg_slots = tkv::kWaveWorkers / tkv::kWaveWG;
+            const int32_t n_tile = static_cast<int32_t>(p->items.size());
             int32_t target = tkv::kWaveWorkers;
+            if (n_tile < wg_slots) target = std::max(wg_slots / 2, wg_slots - n_tile) / kXcds * kXcds * tkv::kWaveWG;
             if (const char* env = std::getenv("TKV_WAVES")) target = std::max(kXcds, std::atoi(env));
             auto cost = [](const ItemDesc& it) { return static_cast<int64_t>(it.n_blk) * (3 + it.pad) + 4; };
             std::vector<std::vector<int32_t>> by_t(tkv::kWaveMaxTiles + 1);

@@ -150,6 +150,16 @@ def test_shared_chunks_on_tile_kernel(seed, hq, hkv, d, monkeypatch):
     assert st["n_items_shared"] - st["n_items_wave"] > 0     # shared chunks did run on the tile kernel
 
 
+@pytest.mark.parametrize("seed,hq,hkv,d", [(17, 12, 2, 128), (20, 8, 1, 64)])
+def test_wide_chunks_on_wave_kernel(seed, hq, hkv, d, monkeypatch):
+    # chunks read by more than 96 query rows stay on the wave kernel, split into many 32-row tiles
+    # over the same blocks (by default they go to 128-row tile items)
+    monkeypatch.setenv("TKV_TILE_MIN_ITEMS", "1000000")
+    wl = W.random_tree(seed, W.Shape(hq, hkv, d), n_roots=2, depth=3, max_branch=5, max_step=40)
+    b, st = compare(wl, 0)
+    assert st["n_items_shared"] == st["n_items_wave"]        # no shared chunk on the tile kernel
+
+
 @pytest.mark.parametrize("waves", ["8", "64"])
 def test_small_wave_grids(waves, monkeypatch):
     # a wave grid much smaller than the item count: long per-wave lists, items crossing into the

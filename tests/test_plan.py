@@ -140,6 +140,10 @@ def test_plan_covers_each_path_exactly_once(name):
         assert st["n_items_row"] == st["n_items"] and st["n_merge"] == 0
     if name == "beam_decode":
         assert st["n_items_shared"] == st["n_items"] and st["n_shared_segments"] > 0
+        # the 16 prompts, each read by 32 live beams x 6 query heads, go to 128-row tile items; the
+        # wave grid keeps clear of the workgroup slots (2 per CU, 4 waves each) those take
+        n_tile = st["n_items"] - st["n_items_wave"]
+        assert 0 < n_tile < 512 and 4 * n_tile + st["n_waves"] <= 2048
 
 
 def test_plan_rejects_bad_input():
