@@ -503,17 +503,15 @@ __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, co
 // Wave-kernel worker: wave w of the wave grid walks its own list of items with no barrier; its tile
 // width T (1 or 2 column tiles of 16 query rows) is fixed per wave by the planner.
 template <int D>
-__device__ __forceinline__ void wave_worker(int w, int wave, int lane, const int4* __restrict__ wdesc,
+__device__ __forceinline__ void wave_worker(int w, int lane, const int4* __restrict__ wdesc,
                                             const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
                                             const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
                                             const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
                                             float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse,
-                                            int hq, int hkv, int G, float sl2, uint8_t* smem) {
-    constexpr int VROW = 2 * D + 32;
+                                            int hq, int hkv, int G, float sl2, uint8_t* vs) {
     const int T = wtiles[w];
     if (T == 0) return;
     const WaveList L{w, woff[w], woff[w + 1] - woff[w] + 1};
-    uint8_t* vs = smem + wave * (32 * VROW);
     if (T == 1)
         wave_run_pair<D, 1>(wdesc, L, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, vs, lane);
     else
@@ -522,41 +520,49 @@ __device__ __forceinline__ void wave_worker(int w, int wave, int lane, const int
 
 // ============================================================================ tile kernel
 
-// One 64-key stage (4 blocks) of K/V, each wave fetching one block: lane l reads 16 bytes of rows
-// 4i + l/16 (clamped to the block's last token), so each load instruction covers 1 KB of the
-// block contiguously.
+// Stage buffers of a tile item: K and V of one 64-key stage (4 blocks), 64 rows of D bf16 each,
+// unpadded.  The 16-byte chunks of row r are XOR-swizzled -- chunk c sits at chunk position
+// c ^ tile_swz(r) -- so that both read patterns hit distinct LDS banks: the MFMA-operand reads of
+// K (16 rows, one chunk each, per 16 lanes) and the transposed 8-byte reads of V (8 rows, 32
+// contiguous bytes each, per 32 lanes).  The swizzle depends on r mod 16 only, so a block's rows
+// carry the same pattern wherever the block sits in the stage.
 template <int D>
-struct StageRegs {
-    u32x4_t k[D / 32], v[D / 32];
-};
+__device__ __forceinline__ int tile_swz(int r) {
+    // D = 128: 16 chunks per row, one row per 256-byte bank line; D = 64: 8 chunks, two rows per line
+    return D == 128 ? (2 * (r & 7)) ^ ((r >> 3) & 1) : (2 * ((r >> 1) & 3)) ^ ((r >> 3) & 1);
+}
+template <int D>
+constexpr int tile_buf_bytes() {
+    return 64 * D * 2;
+}
 
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+
+// Fetch one block of a stage straight from global memory into LDS (global_load_lds_dwordx4: lane l
+// of an instruction writes the l-th 16 bytes of a contiguous 1-KB run at the wave-uniform
+// destination), each lane fetching the global chunk that the swizzle puts at its slot.  Rows past
+// the block's length read its last row (masked later); a block past the item's end has len 0 and
+// reads row 0 of a valid block.  kdst / vdst: the block's rows in the stage buffers (uniform).
 template <int D>
-__device__ __forceinline__ void stage_load(StageRegs<D>& r, const uint16_t* __restrict__ kpool,
-                                           const uint16_t* __restrict__ vpool, size_t boff, int len, int lane) {
-    constexpr int RPI = 64 * 8 / D;  // rows per load instruction (16 bytes per lane)
+__device__ __forceinline__ void stage_fetch(const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
+                                            size_t boff, int len, int lane, uint8_t* kdst, uint8_t* vdst) {
+    constexpr int CPR = D / 8;     // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;  // rows per 1-KB instruction
     const int last = max(len - 1, 0);
 #pragma unroll
-    for (int i = 0; i < D / 32; ++i) {
-        const int row = min(i * RPI + lane / (D / 8), last);
-        const size_t off = boff + static_cast<size_t>(row) * D + (lane % (D / 8)) * 8;
-        r.k[i] = *reinterpret_cast<const u32x4_t*>(kpool + off);
-        r.v[i] = *reinterpret_cast<const u32x4_t*>(vpool + off);
+    for (int i = 0; i < 16 / RPI; ++i) {
+        const int r = i * RPI + lane / CPR;
+        const int c = (lane % CPR) ^ tile_swz<D>(r);
+        const size_t off = boff + static_cast<size_t>(min(r, last)) * D + c * 8;
+        __builtin_amdgcn_global_load_lds(kpool + off, (lds_void_ptr)(kdst + i * 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(vpool + off, (lds_void_ptr)(vdst + i * 1024), 16, 0, 0);
     }
 }
 
-template <int D, int KSTR, int VROW>
-__device__ __forceinline__ void stage_store(const StageRegs<D>& r, uint16_t* ks, uint8_t* vs, int wave, int lane) {
-    constexpr int RPI = 64 * 8 / D;
-#pragma unroll
-    for (int i = 0; i < D / 32; ++i) {
-        const int row = 16 * wave + i * RPI + lane / (D / 8);
-        const int col = (lane % (D / 8)) * 8;
-        *reinterpret_cast<u32x4_t*>(ks + row * KSTR + col) = r.k[i];
-        *reinterpret_cast<u32x4_t*>(vs + row * VROW + col * 2) = r.v[i];
-    }
-}
-
-__device__ __forceinline__ void lds_barrier() {
+// Wait for this wave's stage fetches, then for every wave's (and for every wave to be done reading
+// the buffer that the next fetch overwrites).
+__device__ __forceinline__ void stage_barrier() {
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
@@ -564,35 +570,19 @@ __device__ __forceinline__ void lds_barrier() {
 
 // One workgroup per tile item: a tile of up to 128 query rows (wave w owns rows 32w .. 32w+31 as two
 // column tiles) against the item's key blocks, four blocks per stage.  Stage s+1 is fetched into
-// registers while stage s is contracted from LDS; one barrier per stage (the two LDS buffers
-// alternate, so a buffer is rewritten only after every wave has passed the barrier that follows
-// its last use).
-// K row stride in LDS (elements) and V row stride (bytes) of a tile item's stage buffers.
-template <int D>
-constexpr int tile_kstr() {
-    return D + 16;
-}
-template <int D>
-constexpr int tile_vrow() {
-    return 2 * D + 32;
-}
-template <int D>
-constexpr int tile_smem_bytes() {
-    return 2 * 64 * tile_kstr<D>() * 2 + 2 * 64 * tile_vrow<D>();
-}
-
+// the other pair of LDS buffers while stage s is contracted; one barrier per stage (a buffer is
+// rewritten only after every wave has passed the barrier that follows its last use).  The stage
+// loop is unrolled by two so that each stage names its buffers statically: the compiler then knows
+// that the reads of one buffer do not depend on the fetch into the other.
 template <int D>
 __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::TokDesc* __restrict__ toks,
                                           const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q,
                                           const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
                                           uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
-                                          float* __restrict__ plse, int hq, int hkv, int G, float sl2, uint8_t* smem) {
+                                          float* __restrict__ plse, int hq, int hkv, int G, float sl2, uint8_t* k0,
+                                          uint8_t* v0, uint8_t* k1, uint8_t* v1) {
     constexpr int T = 2;
-    constexpr int KSTR = tile_kstr<D>();  // K row stride (elements): 16-byte reads of 16 rows spread over banks
-    constexpr int VROW = tile_vrow<D>();  // V row stride (bytes): transposed 8-byte reads spread over the banks
-    // two stage buffers: K [2][64][KSTR] bf16, then V [2][64][VROW] bytes
-    uint16_t* const ks_base = reinterpret_cast<uint16_t*>(smem);
-    uint8_t* const vs_base = smem + 2 * 64 * KSTR * 2;
+    constexpr int RB = 2 * D;  // bytes per K/V row in the stage buffers
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, kg = lane >> 4;
@@ -618,35 +608,40 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
     }
     const bool wave_active = __builtin_amdgcn_ballot_w64(limit[0] >= 0 || limit[1] >= 0) != 0;
 
+    // Swizzled read offsets within a block (bytes).  K, S^T A operand: lane (col, kg) reads row col,
+    // chunk 4kk + kg, i.e. koff ^ 64kk.  V, transposed reads: lane (col, kg) reads row
+    // 4kg + col/4, bytes 8(col & 3) .. +7 of the 32-byte column run of output tile ct, i.e.
+    // voff ^ 32ct.  (The XORs touch only the chunk-index bits of the offsets.)
+    const int koff = col * RB + 16 * (kg ^ tile_swz<D>(col));
+    const int vrow = 4 * kg + (col >> 2);
+    const int voff = vrow * RB + 16 * (((col & 3) >> 1) ^ tile_swz<D>(vrow)) + 8 * (col & 1);
+
     // block descriptors of a stage: lane l holds block 4s + (l & 3) (the item's last block past its end)
     auto stage_desc = [&](int st) { return bd[min(4 * st + (lane & 3), nb - 1)]; };
     int2 dcur = stage_desc(0), dnxt = stage_desc(1);
-    StageRegs<D> r;
+    const int wblk = wave * 16 * RB;  // this wave's block within a stage buffer
     {
-        const int len = 4 * 0 + wave < nb ? __builtin_amdgcn_readlane(dcur.y, wave) : 0;
-        stage_load<D>(r, kpool, vpool, static_cast<size_t>(__builtin_amdgcn_readlane(dcur.x, wave)) * blk_stride + kvh_off,
-                      len, lane);
+        const int len = wave < nb ? __builtin_amdgcn_readlane(dcur.y, wave) : 0;
+        stage_fetch<D>(kpool, vpool, static_cast<size_t>(__builtin_amdgcn_readlane(dcur.x, wave)) * blk_stride + kvh_off,
+                       len, lane, k0 + wblk, v0 + wblk);
     }
     WaveAcc<D, T> A;
     A.reset();
     int pos = it.pos0;
-    for (int st = 0; st < n_stages; ++st) {
-        const int buf = st & 1;
-        uint16_t* ks = ks_base + buf * (64 * KSTR);
-        uint8_t* vs = vs_base + buf * (64 * VROW);
-        stage_store<D, KSTR, VROW>(r, ks, vs, wave, lane);
-        lds_barrier();
+    auto stage = [&](int st, const uint8_t* ks, const uint8_t* vs, uint8_t* kn, uint8_t* vn) {
+        stage_barrier();
         // fetch the next stage while this one is contracted
-        {
+        if (st + 1 < n_stages) {
             const int bn = 4 * (st + 1) + wave;
             const int len = bn < nb ? __builtin_amdgcn_readlane(dnxt.y, wave) : 0;
-            stage_load<D>(r, kpool, vpool,
-                          static_cast<size_t>(__builtin_amdgcn_readlane(dnxt.x, wave)) * blk_stride + kvh_off, len, lane);
+            stage_fetch<D>(kpool, vpool,
+                           static_cast<size_t>(__builtin_amdgcn_readlane(dnxt.x, wave)) * blk_stride + kvh_off, len,
+                           lane, kn + wblk, vn + wblk);
         }
         const int2 dthis = dcur;
         dcur = dnxt;
         dnxt = stage_desc(st + 2);
-        if (!wave_active) continue;
+        if (!wave_active) return;
         int len[4], bpos[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -666,7 +661,7 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
             bf16x8_t kf[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                kf[j] = *reinterpret_cast<const bf16x8_t*>(ks + (16 * j + col) * KSTR + 32 * kk + 8 * kg);
+                kf[j] = *reinterpret_cast<const bf16x8_t*>(ks + 16 * j * RB + (koff ^ (64 * kk)));
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -714,19 +709,24 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
                                                             pack_bf16x2(sc[jb][tt][0], sc[jb][tt][1]),
                                                             pack_bf16x2(sc[jb][tt][2], sc[jb][tt][3])});
             }
-            const uint8_t* vra = vs + (16 * ja + 4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
-            const uint8_t* vrb = vra + 16 * VROW;
+            const uint8_t* vra = vs + 16 * ja * RB;
+            const uint8_t* vrb = vra + 16 * RB;
 #pragma unroll
             for (int ct = 0; ct < D / 16; ++ct) {
+                const int off = voff ^ (32 * ct);
                 const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vra + ct * 32)));
+                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vra + off)));
                 const s16x4_t vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vrb + ct * 32)));
+                    (__attribute__((address_space(3))) s16x4_t*)(const_cast<uint8_t*>(vrb + off)));
                 const bf16x8_t vab = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
                 for (int tt = 0; tt < T; ++tt) A.acc[tt][ct] = mfma_16x16x32(vab, pb[tt], A.acc[tt][ct]);
             }
         }
+    };
+    for (int st = 0; st < n_stages; st += 2) {
+        stage(st, k0, v0, k1, v1);
+        if (st + 1 < n_stages) stage(st + 1, k1, v1, k0, v0);
     }
     if (!wave_active) return;
 #pragma unroll
@@ -751,18 +751,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int32_t* __restrict__ wtiles, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
     const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
     float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
-    __shared__ __attribute__((aligned(16))) uint8_t smem[tile_smem_bytes<D>()];
+    // the tile path's two stage buffers of K and V; the wave grid gives one of the four to each wave
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[tile_buf_bytes<D>()];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[tile_buf_bytes<D>()];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[tile_buf_bytes<D>()];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[tile_buf_bytes<D>()];
+    static_assert(32 * (2 * D + 32) <= tile_buf_bytes<D>(), "a wave-grid wave stages two V blocks in one buffer");
     const int b = blockIdx.x;
     if (b < n_tile) {
         const tkv::ItemDesc it = items[b];
-        tile_item<D>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, smem);
+        tile_item<D>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, lds_k0, lds_v0, lds_k1, lds_v1);
         return;
     }
     if (b < n_tile_pad) return;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    wave_worker<D>((b - n_tile_pad) * tkv::kWaveWG + wave, wave, lane, wdesc, woff, wtiles, q, kpool, vpool, o, lse,
-                   po, plse, hq, hkv, G, sl2, smem);
+    uint8_t* vs = wave == 0 ? lds_k0 : wave == 1 ? lds_v0 : wave == 2 ? lds_k1 : lds_v1;
+    wave_worker<D>((b - n_tile_pad) * tkv::kWaveWG + wave, lane, wdesc, woff, wtiles, q, kpool, vpool, o, lse, po,
+                   plse, hq, hkv, G, sl2, vs);
 }
 
 // Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
