@@ -538,24 +538,30 @@ constexpr int tile_buf_bytes() {
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 
-// Fetch one block of a stage straight from global memory into LDS (global_load_lds_dwordx4: lane l
-// of an instruction writes the l-th 16 bytes of a contiguous 1-KB run at the wave-uniform
-// destination), each lane fetching the global chunk that the swizzle puts at its slot.  Rows past
-// the block's length read its last row (masked later); a block past the item's end has len 0 and
-// reads row 0 of a valid block.  kdst / vdst: the block's rows in the stage buffers (uniform).
+// Fetch one block of a stage straight from global memory into LDS (buffer_load_dwordx4 ... lds:
+// lane l of an instruction writes the l-th 16 bytes of a contiguous 1-KB run at the wave-uniform
+// destination), each lane fetching the global chunk that the swizzle puts at its slot.  The buffer
+// descriptor spans the one block, so the offsets stay small for pools of any size.  (The buffer
+// form rather than global_load_lds: the latter also counts as an LDS access of unknown order,
+// which forces every later LDS read to wait for all earlier ones.)  Rows past the block's length
+// read its last row (masked later); a block past the item's end has len 0 and reads row 0 of a
+// valid block.  kdst / vdst: the block's rows in the stage buffers (uniform).
 template <int D>
 __device__ __forceinline__ void stage_fetch(const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
                                             size_t boff, int len, int lane, uint8_t* kdst, uint8_t* vdst) {
     constexpr int CPR = D / 8;     // 16-byte chunks per row
     constexpr int RPI = 64 / CPR;  // rows per 1-KB instruction
+    constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kpool + boff), 0, 32 * D, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(vpool + boff), 0, 32 * D, kRsrcWord3);
     const int last = max(len - 1, 0);
 #pragma unroll
     for (int i = 0; i < 16 / RPI; ++i) {
         const int r = i * RPI + lane / CPR;
         const int c = (lane % CPR) ^ tile_swz<D>(r);
-        const size_t off = boff + static_cast<size_t>(min(r, last)) * D + c * 8;
-        __builtin_amdgcn_global_load_lds(kpool + off, (lds_void_ptr)(kdst + i * 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(vpool + off, (lds_void_ptr)(vdst + i * 1024), 16, 0, 0);
+        const int off = (min(r, last) * D + c * 8) * 2;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_ptr)(kdst + i * 1024), 16, off, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void_ptr)(vdst + i * 1024), 16, off, 0, 0, 0);
     }
 }
 
@@ -656,17 +662,26 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
         for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int tt = 0; tt < T; ++tt) sc[j][tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        bf16x8_t kf[D / 32][4];
 #pragma unroll
-        for (int kk = 0; kk < D / 32; ++kk) {
-            bf16x8_t kf[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                kf[j] = *reinterpret_cast<const bf16x8_t*>(ks + 16 * j * RB + (koff ^ (64 * kk)));
+        for (int kk = 0; kk < D / 32; ++kk)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
+                kf[kk][j] = *reinterpret_cast<const bf16x8_t*>(ks + 16 * j * RB + (koff ^ (64 * kk)));
 #pragma unroll
-                for (int tt = 0; tt < T; ++tt) sc[j][tt] = mfma_16x16x32(kf[j], qf[tt][kk], sc[j][tt]);
+        for (int kk = 0; kk < D / 32; ++kk)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int tt = 0; tt < T; ++tt) sc[j][tt] = mfma_16x16x32(kf[kk][j], qf[tt][kk], sc[j][tt]);
+        // K reads two k-steps ahead of the MFMAs that use them
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+        for (int kk = 0; kk < D / 32 - 2; ++kk) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
         }
+        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
         // one uniform decision per stage: mask only if a block is partial or absent, or some row's
         // causal limit falls inside the stage
         const int stage_end = pos;  // one past the last key position of the stage
