@@ -522,14 +522,19 @@ __device__ __forceinline__ void wave_worker(int w, int lane, const int4* __restr
 
 // Stage buffers of a tile item: K and V of one 64-key stage (4 blocks), 64 rows of D bf16 each,
 // unpadded.  The 16-byte chunks of row r are XOR-swizzled -- chunk c sits at chunk position
-// c ^ tile_swz(r) -- so that both read patterns hit distinct LDS banks: the MFMA-operand reads of
-// K (16 rows, one chunk each, per 16 lanes) and the transposed 8-byte reads of V (8 rows, 32
-// contiguous bytes each, per 32 lanes).  The swizzle depends on r mod 16 only, so a block's rows
-// carry the same pattern wherever the block sits in the stage.
+// c ^ swz(r) -- so that the reads hit distinct LDS banks: the MFMA-operand reads of K
+// (ds_read_b128, 16 rows of one chunk each) and the transposed 8-byte reads of V
+// (ds_read_b64_tr_b16, 8 rows of 32 contiguous bytes each per 32 lanes).  K and V take different
+// swizzles: the ones below measured zero bank-conflict cycles (SQ_LDS_BANK_CONFLICT) for their own
+// read pattern, whereas one swizzle for both cost 4 cycles per K read (or 2 per V read).  Both depend
+// on r mod 16 only, so a block's rows carry the same pattern wherever the block sits in the stage.
 template <int D>
-__device__ __forceinline__ int tile_swz(int r) {
-    // D = 128: 16 chunks per row, one row per 256-byte bank line; D = 64: 8 chunks, two rows per line
-    return D == 128 ? (2 * (r & 7)) ^ ((r >> 3) & 1) : (2 * ((r >> 1) & 3)) ^ ((r >> 3) & 1);
+__device__ __forceinline__ int tile_swz_k(int r) {
+    return D == 128 ? r & 15 : r & 7;
+}
+template <int D>
+__device__ __forceinline__ int tile_swz_v(int r) {
+    return D == 128 ? (2 * (r & 7)) ^ ((r >> 3) & 1) : r & 7;
 }
 template <int D>
 constexpr int tile_buf_bytes() {
@@ -558,10 +563,11 @@ __device__ __forceinline__ void stage_fetch(const uint16_t* __restrict__ kpool, 
 #pragma unroll
     for (int i = 0; i < 16 / RPI; ++i) {
         const int r = i * RPI + lane / CPR;
-        const int c = (lane % CPR) ^ tile_swz<D>(r);
-        const int off = (min(r, last) * D + c * 8) * 2;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_ptr)(kdst + i * 1024), 16, off, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void_ptr)(vdst + i * 1024), 16, off, 0, 0, 0);
+        const int row_off = min(r, last) * D * 2;
+        const int koff = row_off + (((lane % CPR) ^ tile_swz_k<D>(r)) * 16);
+        const int voff = row_off + (((lane % CPR) ^ tile_swz_v<D>(r)) * 16);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_ptr)(kdst + i * 1024), 16, koff, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void_ptr)(vdst + i * 1024), 16, voff, 0, 0, 0);
     }
 }
 
@@ -618,9 +624,9 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
     // chunk 4kk + kg, i.e. koff ^ 64kk.  V, transposed reads: lane (col, kg) reads row
     // 4kg + col/4, bytes 8(col & 3) .. +7 of the 32-byte column run of output tile ct, i.e.
     // voff ^ 32ct.  (The XORs touch only the chunk-index bits of the offsets.)
-    const int koff = col * RB + 16 * (kg ^ tile_swz<D>(col));
+    const int koff = col * RB + 16 * (kg ^ tile_swz_k<D>(col));
     const int vrow = 4 * kg + (col >> 2);
-    const int voff = vrow * RB + 16 * (((col & 3) >> 1) ^ tile_swz<D>(vrow)) + 8 * (col & 1);
+    const int voff = vrow * RB + 16 * (((col & 3) >> 1) ^ tile_swz_v<D>(vrow)) + 8 * (col & 1);
 
     // block descriptors of a stage: lane l holds block 4s + (l & 3) (the item's last block past its end)
     auto stage_desc = [&](int st) { return bd[min(4 * st + (lane & 3), nb - 1)]; };
