@@ -225,7 +225,7 @@ __device__ __forceinline__ void softmax_pair_lazy(WaveAcc<D, T>& A, f32x4_t (&sa
     for (int tt = 0; tt < T; ++tt) {
         const float mx = rowmax4(fmaxf(fmaxf(fmaxf(sa[tt][0], sa[tt][1]), fmaxf(sa[tt][2], sa[tt][3])),
                                        fmaxf(fmaxf(sb[tt][0], sb[tt][1]), fmaxf(sb[tt][2], sb[tt][3]))));
-        if (__builtin_amdgcn_ballot_w64(mx != -INFINITY && (A.m[tt] == -INFINITY || (mx - A.m[tt]) * sl2 > kSlack)) != 0) {
+        if (__builtin_amdgcn_ballot_w64(mx > A.m[tt] + kSlack / sl2) != 0) {  // false for mx = -inf; true for m = -inf < mx
             const float m_new = fmaxf(A.m[tt], mx);
             const float alpha = A.m[tt] == m_new ? 1.f : __builtin_amdgcn_exp2f((A.m[tt] - m_new) * sl2);
             A.l[tt] *= alpha;
@@ -261,7 +261,7 @@ __device__ __forceinline__ void stage_base(WaveAcc<D, T>& A, const f32x4_t (&sc)
         float mx = -INFINITY;
 #pragma unroll
         for (int j = 0; j < 4; ++j) mx = fmaxf(mx, fmaxf(fmaxf(sc[j][tt][0], sc[j][tt][1]), fmaxf(sc[j][tt][2], sc[j][tt][3])));
-        if (__builtin_amdgcn_ballot_w64(mx != -INFINITY && (A.m[tt] == -INFINITY || (mx - A.m[tt]) * sl2 > kSlack)) != 0) {
+        if (__builtin_amdgcn_ballot_w64(mx > A.m[tt] + kSlack / sl2) != 0) {  // false for mx = -inf; true for m = -inf < mx
             mx = rowmax4(mx);
             const float m_new = fmaxf(A.m[tt], mx);
             const float alpha = A.m[tt] == m_new ? 1.f : __builtin_amdgcn_exp2f((A.m[tt] - m_new) * sl2);
@@ -657,7 +657,8 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
         int len[4], bpos[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            len[j] = 4 * st + j < nb ? __builtin_amdgcn_readlane(dthis.y, j) : 0;
+            const int lj = __builtin_amdgcn_readlane(dthis.y, j);
+            len[j] = 4 * st + j < nb ? lj : 0;
             bpos[j] = pos;
             pos += len[j];
         }
