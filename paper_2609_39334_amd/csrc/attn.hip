@@ -50,6 +50,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
+// acc + lo + hi of a packed bf16 pair, in fp32 (v_dot2_f32_bf16 against the pair (1, 1)).
+__device__ __forceinline__ float sum_bf16x2(uint32_t p, float acc) {
+    const bf16x2_t one{static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, p), one, acc, false);
+}
+
 constexpr int kThreads = 256;
 
 // ============================================================================ wave-private kernel
@@ -580,20 +586,19 @@ __device__ __forceinline__ void stage_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// One workgroup per tile item: a tile of up to 128 query rows (wave w owns rows 32w .. 32w+31 as two
-// column tiles) against the item's key blocks, four blocks per stage.  Stage s+1 is fetched into
+// One workgroup per tile item: a tile of up to 64T query rows (wave w owns rows 16Tw .. 16Tw+16T-1
+// as T column tiles) against the item's key blocks, four blocks per stage.  Stage s+1 is fetched into
 // the other pair of LDS buffers while stage s is contracted; one barrier per stage (a buffer is
 // rewritten only after every wave has passed the barrier that follows its last use).  The stage
 // loop is unrolled by two so that each stage names its buffers statically: the compiler then knows
 // that the reads of one buffer do not depend on the fetch into the other.
-template <int D>
+template <int D, int T>
 __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::TokDesc* __restrict__ toks,
                                           const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q,
                                           const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
                                           uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
                                           float* __restrict__ plse, int hq, int hkv, int G, float sl2, uint8_t* k0,
                                           uint8_t* v0, uint8_t* k1, uint8_t* v1) {
-    constexpr int T = 2;
     constexpr int RB = 2 * D;  // bytes per K/V row in the stage buffers
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -610,7 +615,7 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
     int limit[T];
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) {
-        const int row = 32 * wave + 16 * tt + col;
+        const int row = 16 * T * wave + 16 * tt + col;
         const int t = row / G;
         const tkv::TokDesc td = toks[it.tok_off + min(t, it.n_tok - 1)];
         limit[tt] = t < it.n_tok ? td.limit : -1;
@@ -618,7 +623,10 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
 #pragma unroll
         for (int ks = 0; ks < D / 32; ++ks) qf[tt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
     }
-    const bool wave_active = __builtin_amdgcn_ballot_w64(limit[0] >= 0 || limit[1] >= 0) != 0;
+    bool any_row = false;
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) any_row = any_row || limit[tt] >= 0;
+    const bool wave_active = __builtin_amdgcn_ballot_w64(any_row) != 0;
 
     // Swizzled read offsets within a block (bytes).  K, S^T A operand: lane (col, kg) reads row col,
     // chunk 4kk + kg, i.e. koff ^ 64kk.  V, transposed reads: lane (col, kg) reads row
@@ -685,16 +693,17 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
         __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
 #pragma unroll
         for (int kk = 0; kk < D / 32 - 2; ++kk) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 4 * T, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 8 * T, 0);
         // one uniform decision per stage: mask only if a block is partial or absent, or some row's
         // causal limit falls inside the stage
         const int stage_end = pos;  // one past the last key position of the stage
-        if (len[3] != 16 || len[0] + len[1] + len[2] != 48 ||
-            __builtin_amdgcn_ballot_w64((limit[0] >= 0 && limit[0] < stage_end - 1) ||
-                                        (limit[1] >= 0 && limit[1] < stage_end - 1)) != 0) {
+        bool cut = false;
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt) cut = cut || (limit[tt] >= 0 && limit[tt] < stage_end - 1);
+        if (len[3] != 16 || len[0] + len[1] + len[2] != 48 || __builtin_amdgcn_ballot_w64(cut) != 0) {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -718,18 +727,16 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
             bf16x8_t pb[T];
 #pragma unroll
             for (int tt = 0; tt < T; ++tt) {
-                float psum = 0.f;
 #pragma unroll
                 for (int x = 0; x < 4; ++x) {
                     sc[ja][tt][x] = __builtin_amdgcn_exp2f(fmaf(sc[ja][tt][x], sl2, -msc[tt]));
                     sc[jb][tt][x] = __builtin_amdgcn_exp2f(fmaf(sc[jb][tt][x], sl2, -msc[tt]));
-                    psum += sc[ja][tt][x] + sc[jb][tt][x];
                 }
-                A.l[tt] += psum;
-                pb[tt] = __builtin_bit_cast(bf16x8_t, uint4{pack_bf16x2(sc[ja][tt][0], sc[ja][tt][1]),
-                                                            pack_bf16x2(sc[ja][tt][2], sc[ja][tt][3]),
-                                                            pack_bf16x2(sc[jb][tt][0], sc[jb][tt][1]),
-                                                            pack_bf16x2(sc[jb][tt][2], sc[jb][tt][3])});
+                const uint4 pk{pack_bf16x2(sc[ja][tt][0], sc[ja][tt][1]), pack_bf16x2(sc[ja][tt][2], sc[ja][tt][3]),
+                               pack_bf16x2(sc[jb][tt][0], sc[jb][tt][1]), pack_bf16x2(sc[jb][tt][2], sc[jb][tt][3])};
+                // the row sum over the bf16-rounded P that the PV product uses, two keys per v_dot2
+                A.l[tt] = sum_bf16x2(pk.x, sum_bf16x2(pk.y, sum_bf16x2(pk.z, sum_bf16x2(pk.w, A.l[tt]))));
+                pb[tt] = __builtin_bit_cast(bf16x8_t, pk);
             }
             const uint8_t* vra = vs + 16 * ja * RB;
             const uint8_t* vrb = vra + 16 * RB;
@@ -753,7 +760,7 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
     if (!wave_active) return;
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) {
-        const int row = 32 * wave + 16 * tt + col;
+        const int row = 16 * T * wave + 16 * tt + col;
         const int t = row / G;
         const tkv::TokDesc td = toks[it.tok_off + min(t, it.n_tok - 1)];
         write_rows<D>(A.acc[tt], A.m[tt], A.l[tt], t < it.n_tok, td.qtok, it.kvh * G + (row - t * G), td.slot, kg, o,
@@ -782,7 +789,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int b = blockIdx.x;
     if (b < n_tile) {
         const tkv::ItemDesc it = items[b];
-        tile_item<D>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, lds_k0, lds_v0, lds_k1, lds_v1);
+        tile_item<D, 2>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, lds_k0, lds_v0, lds_k1,
+                        lds_v1);
         return;
     }
     if (b < n_tile_pad) return;
