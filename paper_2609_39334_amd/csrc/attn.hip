@@ -769,13 +769,17 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
 }
 
 
-// The attention kernel: workgroups [0, n_tile) take one tile item each (longest first, in the
-// planner's XCD order), workgroups [n_tile_pad, ...) hold kWaveWG waves of the wave grid each
-// (n_tile_pad, a multiple of 8, keeps the wave grid's workgroup-to-XCD assignment that the
-// planner assumed).  One launch covers both kinds of work, so neither waits for the other's tail.
+// The attention kernel runs tile items (one workgroup each, longest first, in the planner's XCD
+// order) and the wave grid (kWaveWG waves per workgroup) in one launch, so neither waits for the
+// other's tail.  Workgroups are dispatched in index order, workgroup b on XCD b % 8.  The first
+// `runs` pairs of runs of eight alternate -- eight tile items, eight wave-grid workgroups, ... --
+// so that MFMA-bound tiles and HBM-bound waves share the CUs from the start when the grid does
+// not fit on the chip at once; then come the remaining tile items, then the remaining wave-grid
+// workgroups.  Either way tile item i and wave workgroup j run on XCDs i % 8 and j % 8, as the
+// planner assumed.
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd(
-    const tkv::ItemDesc* __restrict__ items, int n_tile, int n_tile_pad, const tkv::TokDesc* __restrict__ toks,
+    const tkv::ItemDesc* __restrict__ items, int n_tile, int n_wave_wg, int runs, const tkv::TokDesc* __restrict__ toks,
     const tkv::BlkDesc* __restrict__ blks, const int4* __restrict__ wdesc, const int32_t* __restrict__ woff,
     const int32_t* __restrict__ wtiles, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
     const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
@@ -787,17 +791,28 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[tile_buf_bytes<D>()];
     static_assert(32 * (2 * D + 32) <= tile_buf_bytes<D>(), "a wave-grid wave stages two V blocks in one buffer");
     const int b = blockIdx.x;
-    if (b < n_tile) {
-        const tkv::ItemDesc it = items[b];
+    int tile = -1, wg = -1;
+    if (b < 16 * runs) {
+        ((b & 8) ? wg : tile) = 8 * (b >> 4) + (b & 7);
+    } else {
+        const int r = b - 16 * runs, tiles_left = (n_tile + 7) / 8 * 8 - 8 * runs;
+        if (r < tiles_left)
+            tile = 8 * runs + r;
+        else
+            wg = 8 * runs + (r - tiles_left);
+    }
+    if (tile >= 0) {
+        if (tile >= n_tile) return;
+        const tkv::ItemDesc it = items[tile];
         tile_item<D, 2>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, lds_k0, lds_v0, lds_k1,
                         lds_v1);
         return;
     }
-    if (b < n_tile_pad) return;
+    if (wg >= n_wave_wg) return;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     uint8_t* vs = wave == 0 ? lds_k0 : wave == 1 ? lds_v0 : wave == 2 ? lds_k1 : lds_v1;
-    wave_worker<D>((b - n_tile_pad) * tkv::kWaveWG + wave, lane, wdesc, woff, wtiles, q, kpool, vpool, o, lse, po,
+    wave_worker<D>(wg * tkv::kWaveWG + wave, lane, wdesc, woff, wtiles, q, kpool, vpool, o, lse, po,
                    plse, hq, hkv, G, sl2, vs);
 }
 
@@ -896,12 +911,14 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     hipEvent_t* ev = nullptr;
     if (p->prof_n < p->prof_max) ev = reinterpret_cast<hipEvent_t*>(p->prof_events.data()) + 4 * p->prof_n++;
     const int n_tile = static_cast<int>(p->items.size());
-    const int n_wave = static_cast<int>(p->wave_off.size()) - 1;  // a multiple of kWaveWG
-    const int n_tile_pad = (n_tile + 7) / 8 * 8;
-    const int grid = n_tile_pad + (n_wave > 0 ? n_wave / kWaveWG : 0);
+    const int n_wave_wg = std::max(0, static_cast<int>(p->wave_off.size()) - 1) / kWaveWG;  // waves: a multiple of kWaveWG
+    // runs of eight of each kind (the last run of each padded with workgroups that return at once),
+    // interleaved when the grid exceeds the workgroup slots of the chip (two per CU)
+    const int grid = (n_tile + 7) / 8 * 8 + (n_wave_wg + 7) / 8 * 8;
+    const int runs = n_tile + n_wave_wg > kWaveWorkers / kWaveWG ? std::min((n_tile + 7) / 8, (n_wave_wg + 7) / 8) : 0;
     if (grid > 0)
         hipExtLaunchKernelGGL(attn_fwd<D>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, st,
-                              ev ? ev[0] : nullptr, ev ? ev[1] : nullptr, 0, items, n_tile, n_tile_pad, toks, blks,
+                              ev ? ev[0] : nullptr, ev ? ev[1] : nullptr, 0, items, n_tile, n_wave_wg, runs, toks, blks,
                               wdesc, woff, wtiles, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                               static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
                               p->group, sl2);

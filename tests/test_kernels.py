@@ -180,3 +180,35 @@ def test_empty_plan_on_gpu():
     plan.verify(q, kv, kv, o, None)
     torch.cuda.synchronize()
     assert (o.float() == 7.0).all()          # no row, nothing written
+
+
+@pytest.mark.parametrize("seed,hq,hkv,d,tile_rows", [(30, 12, 2, 128, None), (31, 8, 2, 64, None), (32, 12, 2, 128, "8")])
+def test_consecutive_calls_new_queries(seed, hq, hkv, d, tile_rows, monkeypatch):
+    # a plan's partial slots are reused by every call on it: the second and third calls, with new
+    # queries, must not see an earlier call's partials (tile_rows "8": shared chunks on the 128-row
+    # tiles)
+    import paper_2609_39334_amd as tkv
+    if tile_rows:
+        monkeypatch.setenv("TKV_WAVE_MAX_ROWS", tile_rows)
+        monkeypatch.setenv("TKV_TILE_MIN_ITEMS", "0")
+    wl = W.random_tree(seed, W.Shape(hq, hkv, d), n_roots=3, depth=3, max_branch=4, max_step=60)
+    b = realize_native(wl)[0]
+    ob = realize_oracle(wl)[0]
+    s = wl.shape
+    k, v = wl.kv_values()
+    qi, ki, kb = b.arrays()
+    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, b.block_len, b.mult)
+    assert plan.stats["n_merge"] > 0
+    kd, vd = _dev(k), _dev(v)
+    for call in range(3):
+        q = wl.q_values(10 + call, b.n_qtok)                 # new queries each call
+        o = torch.full((b.n_qtok, s.hq, s.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((b.n_qtok, s.hq), float("nan"), dtype=torch.float32, device="cuda")
+        (plan.decode if b.decode else plan.verify)(_dev(q), kd, vd, o, lse)
+        torch.cuda.synchronize()
+        o_ref, l_ref = oracle.attention(_f64(q), W.bf16_bits_to_f32(k), W.bf16_bits_to_f32(v), ob.tables,
+                                        ob.block_len, ob.q_lens)
+        err = np.abs(o.float().cpu().numpy() - o_ref)
+        lerr = np.abs(lse.cpu().numpy() - l_ref)
+        _log(f"    call {call}: max {err.max():.2e} mean {err.mean():.2e} lse max {lerr.max():.2e}")
+        assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS and lerr.max() <= LSE_ABS
