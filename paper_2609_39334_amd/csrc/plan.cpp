@@ -499,7 +499,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         // i % 8.  Items that read the same keys -- the same first block and KV head (a row's path
         // root, or a shared chunk) -- go to one XCD so that their repeated reads hit its L2.  Groups
         // are assigned to XCDs longest processing time first (cost = key blocks x active waves);
-        // each XCD's list runs longest first and the lists are interleaved into the launch order.
+        // each XCD's list runs group by group and the lists are interleaved into the launch order.
         {
             constexpr int32_t kXcds = 8;
             auto cost = [&](const ItemDesc& it) {
@@ -532,8 +532,18 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 l.first += gcost[g2];
                 xheap.push(l);
             }
+            // group-major: a group's items run together (so that the XCD's L2 holds the keys they
+            // share), groups in the order assigned, each group's items longest first
+            std::vector<int32_t> group_of(p->items.size());
+            for (size_t g2 = 0; g2 < groups.size(); ++g2)
+                for (int32_t i : groups[g2]) group_of[i] = static_cast<int32_t>(g2);
+            std::vector<int32_t> rank(groups.size());
+            for (size_t k2 = 0; k2 < gorder.size(); ++k2) rank[gorder[k2]] = static_cast<int32_t>(k2);
             for (auto& v : xl)
-                std::stable_sort(v.begin(), v.end(), [&](int32_t a2, int32_t b2) { return cost(p->items[a2]) > cost(p->items[b2]); });
+                std::stable_sort(v.begin(), v.end(), [&](int32_t a2, int32_t b2) {
+                    if (group_of[a2] != group_of[b2]) return rank[group_of[a2]] < rank[group_of[b2]];
+                    return cost(p->items[a2]) > cost(p->items[b2]);
+                });
             std::vector<ItemDesc> ordered;
             ordered.reserve(p->items.size());
             std::vector<size_t> next(kXcds, 0);
