@@ -56,6 +56,9 @@ const char* tkv_last_error(void);
  *     the lowest free block id (miss).  Unsealed chunks never hit and are never indexed.
  *   - refcount(b) = number of live sequences whose table holds b; a block is freed and unindexed
  *     when it reaches 0.  New sequence ids are the lowest free id.
+ *   - A sequence's open (unsealed) step is private to it: its blocks have refcount 1, are not
+ *     indexed, and no sequence can be extended from it.  A decode loop grows it token by token
+ *     (tkv_bm_append) and completes it (tkv_bm_seal), when its blocks are deduplicated.
  * Host-only; no device memory is touched.
  */
 typedef struct tkv_bm tkv_bm;
@@ -75,6 +78,30 @@ void tkv_bm_destroy(tkv_bm* bm);
  * (cap < ceil(n/block_size); *n_blk_out = that size).  On error nothing changes. */
 int tkv_bm_extend(tkv_bm* bm, int32_t parent, const int32_t* tokens, int32_t n, int32_t seal,
                   int32_t* child_out, int32_t* blk_out, uint8_t* hit_out, int32_t cap, int32_t* n_blk_out);
+
+/* Grow a live sequence in place by tokens[0..n) (one decode step appends one token per
+ * candidate).  A sealed sequence starts a new open step in a fresh block; an open step fills its
+ * last block first, then takes the lowest free block ids one at a time.  dst_out[0..n) = each
+ * token's pool slot, block * block_size + slot within the block: where the token's K and V go
+ * (tkv_kv_append).  cap = capacity of dst_out.  Errors: EINVAL (n < 0, NULL pointers), ENOSEQ,
+ * ENOMEM (too few free blocks), ECAP (cap < n).  On error nothing changes. */
+int tkv_bm_append(tkv_bm* bm, int32_t seq, const int32_t* tokens, int32_t n, int32_t* dst_out, int32_t cap);
+
+/* Complete the open step of a live sequence.  Its blocks are taken in path order with the dedup
+ * key of the extension rules (the predecessor being the block the path holds after the earlier
+ * ones were settled): a hit replaces the sequence's own block with the live sealed block of the same
+ * key (refcount +1) and frees its own; a miss indexes the block.  replaced_out[2i], [2i+1] = the
+ * i-th (own block, sealed block) pair, i < *n_replaced_out; cap = capacity in pairs, at least the
+ * open step's block count (ECAP otherwise, *n_replaced_out = that count, nothing changes).
+ * EINVAL if the sequence is already sealed or a pointer is NULL; ENOSEQ. */
+int tkv_bm_seal(tkv_bm* bm, int32_t seq, int32_t* replaced_out, int32_t cap, int32_t* n_replaced_out);
+
+/* Pool slots of a new step's tokens for tkv_kv_append, from tkv_bm_extend's outputs: token t of n_tok
+ * goes to block blk[t / block_size] at slot t % block_size, or nowhere (-1) where that block was a
+ * deduplication hit -- the block already holds the same tokens' K/V, so the write is skipped.
+ * n_blk must be ceil(n_tok / block_size).  dst_out[0..n_tok).  EINVAL.  Host-only. */
+int tkv_extend_slots(const int32_t* blk, const uint8_t* hit, int32_t n_blk, int32_t n_tok, int32_t block_size,
+                     int32_t* dst_out);
 
 /* Release a sequence (early pruning, Sec. 4.1): refcounts of its table drop by one in table order;
  * blocks reaching 0 are freed and written to freed_out[0..*n_freed_out) in that order.  cap =
@@ -97,7 +124,7 @@ int tkv_bm_block_len(const tkv_bm* bm, int32_t* len_out);
 /* Whole state as int32 words, for bit-exact comparison in tests:
  *   num_blocks, block_size, max_seqs, n_live,
  *   refcount[num_blocks], block_len[num_blocks], indexed[num_blocks] (0/1),
- *   then per live sequence in ascending id: seq, sealed, n, table[n].
+ *   then per live sequence in ascending id: seq, sealed, open step's block count, n, table[n].
  * *used = bytes needed; ECAP if cap < *used (buf may be NULL to query the size). */
 int tkv_bm_snapshot(const tkv_bm* bm, void* buf, size_t cap, size_t* used);
 

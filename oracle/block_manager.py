@@ -18,6 +18,18 @@ rules, so the following reading is used and is exact (no hashing decides anythin
   is freed at once and leaves the index (no cached-but-free pool).
 * New sequence id = lowest free id.  Extending an unsealed sequence is an error; so is a root with no
   tokens.  Errors leave the state unchanged.
+
+Growing a path token by token (a decode loop) and completing a step:
+
+* append(seq, tokens) grows the sequence in place.  Its open (unsealed) step is private to it -- no
+  sequence can be extended from an unsealed one -- so the tokens fill the open step's last block and
+  then take the lowest free ids, one block at a time.  A sealed sequence starts a new open step in a
+  fresh block (step-aligned, as for extensions).  Open blocks are never indexed.
+* seal(seq) completes the open step: its blocks, in path order, are looked up with the dedup key
+  above (the predecessor being the block the path now holds there).  A hit replaces the sequence's
+  own block with the live sealed block of the same key (whose refcount rises; the own block, held
+  by this sequence only, is freed); a miss indexes the block.  As in an extension, once a block
+  misses every later one misses (a block that was just indexed precedes nothing in the index).
 """
 from __future__ import annotations
 
@@ -48,7 +60,9 @@ class BlockManager:
         self.index: Dict[tuple, int] = {}
         self.free_blocks = list(range(num_blocks))              # a heap: lowest id first
         self.free_seqs = list(range(max_seqs))
-        self.seqs: Dict[int, dict] = {}                          # seq -> {table, sealed}
+        self.seqs: Dict[int, dict] = {}                          # seq -> {table, sealed, open}
+        # "open": tokens of the open (unsealed) step, which fill the last ceil(len / block_size)
+        # blocks of the table (empty for a sealed sequence)
 
     # ------------------------------------------------------------------ operations
     def extend(self, parent: int, tokens, seal: bool) -> Tuple[int, List[int], List[int]]:
@@ -102,8 +116,67 @@ class BlockManager:
             table.append(b)
             new_ids.append(b)
             pred = b
-        self.seqs[seq] = {"table": table, "sealed": bool(seal)}
+        self.seqs[seq] = {"table": table, "sealed": bool(seal), "open": [] if seal else list(toks)}
         return seq, new_ids, hits
+
+    def append(self, seq: int, tokens) -> List[int]:
+        """Grow `seq` in place by `tokens`; returns each token's pool slot, block * block_size + slot."""
+        toks = [int(t) for t in np.asarray(tokens).reshape(-1)]
+        if seq not in self.seqs:
+            raise BMError(ENOSEQ, f"unknown sequence {seq}")
+        sq = self.seqs[seq]
+        bs = self.block_size
+        open_toks = [] if sq["sealed"] else sq["open"]
+        room = (-len(open_toks)) % bs            # free slots in the open step's last block
+        need = -(-max(0, len(toks) - room) // bs)
+        if need > len(self.free_blocks):
+            raise BMError(ENOMEM, f"pool exhausted: need {need} blocks, {len(self.free_blocks)} free")
+        if sq["sealed"]:
+            sq["sealed"] = False
+            sq["open"] = open_toks = []
+        dst = []
+        for t in toks:
+            if len(open_toks) % bs == 0:          # the open step's last block is full (or there is none)
+                b = heapq.heappop(self.free_blocks)
+                self.refcount[b] = 1
+                sq["table"].append(b)
+            b = sq["table"][-1]
+            dst.append(b * bs + self.block_len[b])
+            self.block_len[b] += 1
+            open_toks.append(t)
+        return dst
+
+    def seal(self, seq: int) -> List[Tuple[int, int]]:
+        """Complete the open step of `seq`; returns the (own block, live sealed block) replacements."""
+        if seq not in self.seqs:
+            raise BMError(ENOSEQ, f"unknown sequence {seq}")
+        sq = self.seqs[seq]
+        if sq["sealed"]:
+            raise BMError(EINVAL, f"sequence {seq} is already sealed")
+        bs = self.block_size
+        table, open_toks = sq["table"], sq["open"]
+        n_open = -(-len(open_toks) // bs)
+        first = len(table) - n_open
+        replaced = []
+        for j in range(n_open):
+            i = first + j
+            pred = table[i - 1] if i > 0 else -1
+            key = (pred, tuple(open_toks[j * bs:(j + 1) * bs]))
+            own = table[i]
+            hit = self.index.get(key)
+            if hit is not None:
+                table[i] = hit
+                self.refcount[hit] += 1
+                self.refcount[own] = 0
+                self.block_len[own] = 0
+                heapq.heappush(self.free_blocks, own)
+                replaced.append((own, hit))
+            else:
+                self.key[own] = key
+                self.index[key] = own
+        sq["sealed"] = True
+        sq["open"] = []
+        return replaced
 
     def prune(self, seq: int) -> List[int]:
         """Release a sequence; returns the block ids freed, in table order."""
@@ -138,5 +211,6 @@ class BlockManager:
             "refcount": np.array(self.refcount, dtype=np.int32),
             "block_len": np.array(self.block_len, dtype=np.int32),
             "indexed": np.array([k is not None for k in self.key], dtype=np.int32),
-            "seqs": {s: (tuple(v["table"]), int(v["sealed"])) for s, v in sorted(self.seqs.items())},
+            "seqs": {s: (tuple(v["table"]), int(v["sealed"]), -(-len(v["open"]) // self.block_size))
+                     for s, v in sorted(self.seqs.items())},
         }

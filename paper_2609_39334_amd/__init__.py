@@ -54,6 +54,9 @@ _SIG = {
     "tkv_bm_destroy": (None, [_P]),
     "tkv_bm_extend": (ctypes.c_int, [_P, _I32, _PI32, _I32, _I32, _PI32, _PI32, _PU8, _I32, _PI32]),
     "tkv_prune": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32]),
+    "tkv_bm_append": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32, _I32]),
+    "tkv_bm_seal": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32]),
+    "tkv_extend_slots": (ctypes.c_int, [_PI32, _PU8, _I32, _I32, _I32, _PI32]),
     "tkv_bm_table": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32, _PI32]),
     "tkv_bm_refcount": (ctypes.c_int, [_P, _I32, _PI32]),
     "tkv_bm_block_len": (ctypes.c_int, [_P, _PI32]),
@@ -150,6 +153,36 @@ def tkv_prune(bm: int, seq: int, cap: int = None) -> np.ndarray:
     return out[:n.value].copy()
 
 
+def tkv_bm_append(bm: int, seq: int, tokens) -> np.ndarray:
+    """Grows a sequence in place; returns each token's pool slot (block * block_size + slot)."""
+    t = _i32(tokens)
+    dst = np.zeros(max(1, len(t)), dtype=np.int32)
+    _check(lib().tkv_bm_append(bm, seq, _ptr(t), len(t), _ptr(dst), len(t)))
+    return dst[:len(t)].copy()
+
+
+def tkv_bm_seal(bm: int, seq: int):
+    """Completes the open step of a sequence; returns the (own block, sealed block) replacements."""
+    n = _I32()
+    rc = lib().tkv_bm_seal(bm, seq, None, 0, ctypes.byref(n))
+    if rc == TKV_OK:
+        return []
+    if rc != TKV_ECAP:
+        _check(rc)
+    out = np.zeros(2 * n.value, dtype=np.int32)
+    _check(lib().tkv_bm_seal(bm, seq, _ptr(out), n.value, ctypes.byref(n)))
+    return [(int(out[2 * i]), int(out[2 * i + 1])) for i in range(n.value)]
+
+
+def tkv_extend_slots(blk, hit, n_tok: int, block_size: int = 16) -> np.ndarray:
+    """Pool slots of a new step's tokens (-1 where the block was a deduplication hit)."""
+    b = _i32(blk)
+    h = np.ascontiguousarray(np.asarray(hit, dtype=np.uint8).reshape(-1))
+    dst = np.zeros(max(1, n_tok), dtype=np.int32)
+    _check(lib().tkv_extend_slots(_ptr(b), h.ctypes.data_as(_PU8), len(b), n_tok, block_size, _ptr(dst)))
+    return dst[:n_tok].copy()
+
+
 def _table_len(bm: int, seq: int):
     n, kv = _I32(), _I32()
     rc = lib().tkv_bm_table(bm, seq, None, 0, ctypes.byref(n), ctypes.byref(kv))
@@ -191,9 +224,9 @@ def tkv_bm_snapshot(bm: int, seqs: bool = True) -> dict:
             "indexed": buf[w + 2 * nb:w + 3 * nb].copy(), "seqs": {}}
     w += 3 * nb
     for _ in range(nlive if seqs else 0):
-        s, sealed, n = (int(x) for x in buf[w:w + 3])
-        snap["seqs"][s] = (tuple(int(b) for b in buf[w + 3:w + 3 + n]), sealed)
-        w += 3 + n
+        s, sealed, n_open, n = (int(x) for x in buf[w:w + 4])
+        snap["seqs"][s] = (tuple(int(b) for b in buf[w + 4:w + 4 + n]), sealed, n_open)
+        w += 4 + n
     return snap
 
 
@@ -300,6 +333,12 @@ class BlockManager:
 
     def prune(self, seq):
         return tkv_prune(self.h, seq)
+
+    def append(self, seq, tokens):
+        return tkv_bm_append(self.h, seq, tokens)
+
+    def seal(self, seq):
+        return tkv_bm_seal(self.h, seq)
 
     def table(self, seq):
         return tkv_bm_table(self.h, seq)[0]

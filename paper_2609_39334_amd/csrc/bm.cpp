@@ -7,6 +7,10 @@
 // sealed block with the same (predecessor block, exact tokens) key; misses take the lowest free id;
 // refcount = live sequences holding the block; freed and unindexed at zero; lowest free sequence id.
 // A 64-bit FNV-1a hash only selects a bucket -- keys are compared exactly.
+// A decode loop grows a path in place (append: the open, unsealed step is private to its sequence,
+// so its last block fills up before the lowest free id is taken) and completes a step (seal: each
+// open block is looked up with the same key; a hit swaps in the live sealed block and frees the
+// sequence's own, a miss indexes the block).
 #include <algorithm>
 #include <cstring>
 #include <functional>
@@ -45,6 +49,7 @@ struct Seq {
     bool live = false;
     bool sealed = false;
     std::vector<int32_t> table;
+    std::vector<int32_t> open;  // tokens of the open step: the last ceil(size / block_size) blocks
 };
 
 }  // namespace
@@ -178,9 +183,104 @@ TKV_EXPORT int tkv_bm_extend(tkv_bm* bm, int32_t parent, const int32_t* tokens, 
     }
     sq.live = true;
     sq.sealed = seal != 0;
+    if (seal)
+        sq.open.clear();
+    else
+        sq.open.assign(tokens, tokens + n);
     bm->n_live += 1;
     *child_out = s;
     *n_blk_out = n_chunks;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_bm_append(tkv_bm* bm, int32_t seq, const int32_t* tokens, int32_t n, int32_t* dst_out,
+                             int32_t cap) {
+    tkv::clear_error();
+    if (!bm || (n > 0 && (!tokens || !dst_out))) return set_error(TKV_EINVAL, "tkv_bm_append: NULL argument");
+    if (n < 0) return set_error(TKV_EINVAL, "tkv_bm_append: n = %d < 0", n);
+    if (!seq_live(bm, seq)) return set_error(TKV_ENOSEQ, "tkv_bm_append: sequence %d is not live", seq);
+    if (cap < n) return set_error(TKV_ECAP, "tkv_bm_append: output capacity %d < %d tokens", cap, n);
+    Seq& sq = bm->seqs[seq];
+    const int32_t bs = bm->block_size;
+    const int64_t open = sq.sealed ? 0 : static_cast<int64_t>(sq.open.size());
+    const int64_t room = (bs - open % bs) % bs;  // free slots in the open step's last block
+    const int64_t need = (std::max<int64_t>(0, n - room) + bs - 1) / bs;
+    if (static_cast<size_t>(need) > bm->free_blocks.size())
+        return set_error(TKV_ENOMEM, "tkv_bm_append: pool exhausted (need %lld blocks, %zu free)",
+                         static_cast<long long>(need), bm->free_blocks.size());
+    if (sq.sealed) {  // a new step, in a fresh block
+        sq.sealed = false;
+        sq.open.clear();
+    }
+    for (int32_t i = 0; i < n; ++i) {
+        if (sq.open.size() % bs == 0) {
+            const int32_t b = bm->free_blocks.top();
+            bm->free_blocks.pop();
+            bm->refcount[b] = 1;
+            sq.table.push_back(b);
+        }
+        const int32_t b = sq.table.back();
+        dst_out[i] = b * bs + bm->block_len[b];
+        bm->block_len[b] += 1;
+        sq.open.push_back(tokens[i]);
+    }
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_bm_seal(tkv_bm* bm, int32_t seq, int32_t* replaced_out, int32_t cap, int32_t* n_replaced_out) {
+    tkv::clear_error();
+    if (!bm || !n_replaced_out) return set_error(TKV_EINVAL, "tkv_bm_seal: NULL argument");
+    if (!seq_live(bm, seq)) return set_error(TKV_ENOSEQ, "tkv_bm_seal: sequence %d is not live", seq);
+    Seq& sq = bm->seqs[seq];
+    if (sq.sealed) return set_error(TKV_EINVAL, "tkv_bm_seal: sequence %d is already sealed", seq);
+    const int32_t bs = bm->block_size;
+    const int32_t n_open = static_cast<int32_t>((sq.open.size() + bs - 1) / bs);
+    if (cap < n_open || (n_open > 0 && !replaced_out)) {
+        *n_replaced_out = n_open;
+        return set_error(TKV_ECAP, "tkv_bm_seal: capacity %d < %d open blocks", cap, n_open);
+    }
+    const int32_t first = static_cast<int32_t>(sq.table.size()) - n_open;
+    int32_t nr = 0;
+    for (int32_t j = 0; j < n_open; ++j) {
+        const int32_t i = first + j;
+        const size_t a = static_cast<size_t>(j) * bs, e = std::min(sq.open.size(), a + bs);
+        ChunkKey k{i > 0 ? sq.table[i - 1] : -1, std::vector<int32_t>(sq.open.begin() + a, sq.open.begin() + e)};
+        const int32_t own = sq.table[i];
+        auto it = bm->index.find(k);
+        if (it != bm->index.end()) {
+            const int32_t hit = it->second;
+            sq.table[i] = hit;
+            bm->refcount[hit] += 1;
+            bm->refcount[own] = 0;
+            bm->block_len[own] = 0;
+            bm->free_blocks.push(own);
+            replaced_out[2 * nr] = own;
+            replaced_out[2 * nr + 1] = hit;
+            ++nr;
+        } else {
+            bm->index.emplace(k, own);
+            bm->key[own] = std::move(k);
+            bm->indexed[own] = 1;
+        }
+    }
+    sq.sealed = true;
+    sq.open.clear();
+    *n_replaced_out = nr;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_extend_slots(const int32_t* blk, const uint8_t* hit, int32_t n_blk, int32_t n_tok,
+                                int32_t block_size, int32_t* dst_out) {
+    tkv::clear_error();
+    if (n_blk < 0 || n_tok < 0 || block_size < 1 || (n_blk > 0 && (!blk || !hit)) || (n_tok > 0 && !dst_out))
+        return set_error(TKV_EINVAL, "tkv_extend_slots: bad argument");
+    if (n_blk != (static_cast<int64_t>(n_tok) + block_size - 1) / block_size)
+        return set_error(TKV_EINVAL, "tkv_extend_slots: %d tokens take %lld blocks of %d, not %d", n_tok,
+                         static_cast<long long>((static_cast<int64_t>(n_tok) + block_size - 1) / block_size), block_size, n_blk);
+    for (int32_t t = 0; t < n_tok; ++t) {
+        const int32_t c = t / block_size;
+        dst_out[t] = hit[c] ? -1 : blk[c] * block_size + (t - c * block_size);
+    }
     return TKV_OK;
 }
 
@@ -208,6 +308,7 @@ TKV_EXPORT int tkv_prune(tkv_bm* bm, int32_t seq, int32_t* freed_out, int32_t ca
         }
     }
     sq.table.clear();
+    sq.open.clear();
     sq.live = false;
     sq.sealed = false;
     bm->free_seqs.push(seq);
@@ -255,7 +356,7 @@ TKV_EXPORT int tkv_bm_snapshot(const tkv_bm* bm, void* buf, size_t cap, size_t* 
     if (!bm || !used) return set_error(TKV_EINVAL, "tkv_bm_snapshot: NULL argument");
     size_t words = 4 + 3 * static_cast<size_t>(bm->num_blocks);
     for (const Seq& s : bm->seqs)
-        if (s.live) words += 3 + s.table.size();
+        if (s.live) words += 4 + s.table.size();
     *used = words * sizeof(int32_t);
     if (!buf || cap < *used) return set_error(TKV_ECAP, "tkv_bm_snapshot: capacity %zu < %zu bytes", cap, *used);
     int32_t* w = static_cast<int32_t*>(buf);
@@ -271,6 +372,7 @@ TKV_EXPORT int tkv_bm_snapshot(const tkv_bm* bm, void* buf, size_t cap, size_t* 
         if (!q.live) continue;
         *w++ = s;
         *w++ = q.sealed ? 1 : 0;
+        *w++ = static_cast<int32_t>((q.open.size() + bm->block_size - 1) / bm->block_size);
         *w++ = static_cast<int32_t>(q.table.size());
         for (int32_t b : q.table) *w++ = b;
     }

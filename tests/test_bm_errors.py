@@ -117,3 +117,44 @@ def test_coalesce_rejects_dead_sequences_and_bad_q_len():
     with pytest.raises(tkv.TkvError) as e:
         bm.coalesce([p], [0])
     assert e.value.code == tkv.TKV_EINVAL
+
+
+def test_append_errors_leave_state_unchanged():
+    bm, p, c = _bm()                                       # c: open step of 2 tokens in block 2; 7 blocks free
+    before = bm.snapshot()
+    with pytest.raises(tkv.TkvError) as e:
+        bm.append(c, list(range(31)))                      # 2 slots left, then 29 tokens = 8 blocks > 7
+    assert e.value.code == tkv.TKV_ENOMEM
+    _same(before, bm.snapshot())
+    for s in (3, -1, 99):
+        with pytest.raises(tkv.TkvError) as e:
+            bm.append(s, [1])
+        assert e.value.code == tkv.TKV_ENOSEQ
+    _same(before, bm.snapshot())
+    L = tkv.lib()
+    toks = np.arange(5, dtype=np.int32)
+    dst = np.zeros(5, dtype=np.int32)
+    rc = L.tkv_bm_append(bm.h, c, toks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 5,
+                         dst.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 4)
+    assert rc == tkv.TKV_ECAP
+    _same(before, bm.snapshot())
+    assert bm.append(c, list(range(30))).tolist()[:2] == [2 * 4 + 2, 2 * 4 + 3]   # 30 tokens fit
+
+
+def test_seal_errors_leave_state_unchanged():
+    bm, p, c = _bm()
+    bm.append(c, [8, 9, 10])                               # open step: blocks 2 (full) and 3
+    before = bm.snapshot()
+    with pytest.raises(tkv.TkvError) as e:
+        bm.seal(p)                                         # already sealed
+    assert e.value.code == tkv.TKV_EINVAL
+    L = tkv.lib()
+    n = ctypes.c_int32()
+    out = np.zeros(2, dtype=np.int32)
+    rc = L.tkv_bm_seal(bm.h, c, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 1, ctypes.byref(n))
+    assert rc == tkv.TKV_ECAP and n.value == 2             # two open blocks need room for two pairs
+    _same(before, bm.snapshot())
+    assert bm.seal(c) == [] and bm.snapshot()["seqs"][c][1:] == (1, 0)
+    with pytest.raises(tkv.TkvError) as e:
+        bm.seal(c)
+    assert e.value.code == tkv.TKV_EINVAL

@@ -69,6 +69,46 @@ class _Pair:
         self.ops += 1
         return fo
 
+    def append(self, seq, tokens):
+        err_o = err_c = None
+        try:
+            do = self.o.append(seq, tokens)
+        except oracle.BMError as e:
+            err_o = e.code
+        try:
+            dc = self.c.append(seq, tokens)
+        except tkv.TkvError as e:
+            err_c = e.code
+        assert err_o == err_c
+        if err_o is not None:
+            raise oracle.BMError(err_o, "both failed")
+        assert list(do) == [int(x) for x in dc]
+        table = self.o.table(seq)
+        assert tuple(table) == tuple(int(x) for x in self.c.table(seq))
+        self._cmp_arrays(table)
+        self.ops += 1
+        return do
+
+    def seal(self, seq):
+        err_o = err_c = None
+        try:
+            ro = self.o.seal(seq)
+        except oracle.BMError as e:
+            err_o = e.code
+        try:
+            rc = self.c.seal(seq)
+        except tkv.TkvError as e:
+            err_c = e.code
+        assert err_o == err_c
+        if err_o is not None:
+            raise oracle.BMError(err_o, "both failed")
+        assert ro == rc
+        table = self.o.table(seq)
+        assert tuple(table) == tuple(int(x) for x in self.c.table(seq))
+        self._cmp_arrays(list(table) + [own for own, _ in ro])
+        self.ops += 1
+        return ro
+
     def full_compare(self):
         so, sc = self.o.snapshot(), self.c.snapshot()
         _arrays_equal(so, sc)
@@ -90,6 +130,10 @@ def test_golden_cases_lockstep(case):
         try:
             if op["op"] == "extend":
                 p.extend(op["parent"], _tokens(op["tokens"]), bool(op["seal"]))
+            elif op["op"] == "append":
+                p.append(op["seq"], _tokens(op["tokens"]))
+            elif op["op"] == "seal":
+                p.seal(op["seq"])
             else:
                 try:
                     p.prune(op["seq"])
@@ -134,6 +178,63 @@ def test_random_scripts_lockstep(seed):
         if p.ops % 25 == 0:
             p.full_compare()
     p.full_compare()
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_decode_loop_scripts_lockstep(seed):
+    # extensions, token-by-token appends (decode steps), seals and prunes in random order, with small
+    # vocabularies so that sealed steps often find identical blocks
+    rng = np.random.default_rng(2000 + seed)
+    p = _Pair(64, 4, 16)
+    live, open_ = [], set()
+    for _ in range(300):
+        r = rng.random()
+        vocab = 2 if rng.random() < 0.6 else 40
+        try:
+            if live and r < 0.15:
+                s = live.pop(int(rng.integers(0, len(live))))
+                p.prune(s)
+                open_.discard(s)
+            elif live and r < 0.55:
+                s = live[int(rng.integers(0, len(live)))]
+                p.append(s, rng.integers(0, vocab, size=int(rng.integers(0, 7))).tolist())
+                open_.add(s)
+            elif live and r < 0.7:
+                s = live[int(rng.integers(0, len(live)))]
+                if s in open_:
+                    p.seal(s)
+                    open_.discard(s)
+                else:
+                    with pytest.raises(oracle.BMError):          # sealing a sealed sequence fails on both
+                        p.seal(s)
+            else:
+                cands = [s for s in live if s not in open_]
+                parent = -1 if not cands or rng.random() < 0.2 else cands[int(rng.integers(0, len(cands)))]
+                toks = rng.integers(0, vocab, size=int(rng.integers(1 if parent == -1 else 0, 9))).tolist()
+                seal = bool(rng.random() < 0.5)
+                s, _, _ = p.extend(parent, toks, seal)
+                live.append(s)
+                if not seal:
+                    open_.add(s)
+        except oracle.BMError:
+            continue
+        if p.ops % 25 == 0:
+            p.full_compare()
+    p.full_compare()
+
+
+def test_extend_slots_skip_hit_blocks():
+    # the pool slots of a sealed step's tokens: consecutive within each block, none for a hit block
+    p = _Pair(20, 4, 8)
+    root, _, _ = p.extend(-1, [1, 2, 3, 4, 5], True)
+    a, blk, hit = p.extend(root, [7, 8, 9, 10, 11, 12], True)
+    b, blk2, hit2 = p.extend(root, [7, 8, 9, 10, 13], True)      # first block a hit, second a miss
+    assert list(hit2) == [1, 0]
+    dst = tkv.tkv_extend_slots(blk2, hit2, 5, 4)
+    assert dst.tolist() == [-1, -1, -1, -1, blk2[1] * 4]
+    assert tkv.tkv_extend_slots(blk, hit, 6, 4).tolist() == [blk[0] * 4 + i for i in range(4)] + [blk[1] * 4, blk[1] * 4 + 1]
+    with pytest.raises(tkv.TkvError):
+        tkv.tkv_extend_slots(blk, hit, 9, 4)                       # 9 tokens need 3 blocks
 
 
 @pytest.mark.parametrize("name", list(W.CONFIGS))

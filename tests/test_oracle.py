@@ -298,6 +298,10 @@ def test_bm_golden_cases(case):
             if op["op"] == "extend":
                 seq, blocks, hits = bm.extend(op["parent"], _tokens(op["tokens"]), bool(op["seal"]))
                 got = {"seq": seq, "blocks": blocks, "hits": hits}
+            elif op["op"] == "append":
+                got = {"dst": bm.append(op["seq"], _tokens(op["tokens"]))}
+            elif op["op"] == "seal":
+                got = {"replaced": [list(r) for r in bm.seal(op["seq"])]}
             else:
                 got = {"freed": bm.prune(op["seq"])}
         except BMError as e:
@@ -314,7 +318,7 @@ def test_bm_golden_cases(case):
     np.testing.assert_array_equal(snap["block_len"], _expand(fin["block_len"], nb))
     if "indexed" in fin:
         np.testing.assert_array_equal(snap["indexed"], _expand(fin["indexed"], nb))
-    assert {str(s): list(t) for s, (t, _) in snap["seqs"].items()} == fin["tables"]
+    assert {str(s): list(t) for s, (t, _, _) in snap["seqs"].items()} == fin["tables"]
     for s, n in fin["kv_len"].items():
         assert bm.kv_len(int(s)) == n
 
@@ -374,7 +378,7 @@ def _check_bm_against_brute(bm, tracker, used_before, new_ids):
     live = snap["seqs"]
     ref = np.zeros(bm.num_blocks, dtype=np.int64)
     owner = {}
-    for s, (table, _) in live.items():
+    for s, (table, _, _) in live.items():
         ids = tracker.ident[s]
         assert len(ids) == len(table)
         for b, idn in zip(table, ids):
@@ -425,3 +429,114 @@ def test_bm_random_scripts_match_brute_force(seed):
         fresh = [b for b, h in zip(new_blocks, hits) if not h]
         assert all(h == 0 for h in hits[len(new_blocks) - len(fresh):])   # misses never precede hits
         _check_bm_against_brute(bm, tr, used, fresh)
+
+
+class _StepTracker(_BruteTracker):
+    """The brute-force model of deduplication extended to steps grown token by token: a chunk of an
+    open step is private (identity: the step and the chunk's place in it), and sealing gives each of
+    its chunks the identity a sealed extension would -- its tokens and its predecessor's identity."""
+
+    def __init__(self, bs):
+        super().__init__(bs)
+        self.open = {}         # seq -> (step id, tokens of the open step)
+
+    def extend_seq(self, s, parent, toks, seal, op_id):
+        self.ident[s] = self.extend(parent, toks, seal, op_id)
+        if not seal:
+            self.open[s] = (op_id, list(toks))
+
+    def append(self, s, toks, op_id):
+        if s not in self.open:                          # a sealed sequence starts a new step
+            self.open[s] = (op_id, [])
+        sid, ot = self.open[s]
+        before = -(-len(ot) // self.bs)
+        ot.extend(toks)
+        self.ident[s] += [("U", sid, ci) for ci in range(before, -(-len(ot) // self.bs))]
+
+    def seal(self, s):
+        _, ot = self.open.pop(s)
+        chunks = [tuple(ot[i:i + self.bs]) for i in range(0, len(ot), self.bs)]
+        base = self.ident[s][:len(self.ident[s]) - len(chunks)]
+        for c in chunks:
+            base.append(("S", base[-1] if base else ("root",), c))
+        self.ident[s] = base
+
+    def drop(self, s):
+        del self.ident[s]
+        self.open.pop(s, None)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_bm_decode_steps_match_brute_force(seed):
+    # extensions, token-by-token appends, seals and prunes in random order: after every operation
+    # equal chunk histories share a block, different ones do not, refcounts count holders, and fresh
+    # blocks are the lowest free ids
+    rng = np.random.default_rng(100 + seed)
+    bs = 4
+    bm = oracle.BlockManager(96, bs, 24)
+    tr = _StepTracker(bs)
+    live = []
+    for op_id in range(250):
+        used = set(int(b) for b in np.nonzero(np.array(bm.refcount))[0])
+        r = rng.random()
+        vocab = 2 if rng.random() < 0.6 else 50            # tiny vocab -> frequent identical steps
+        if live and r < 0.15:
+            s = live.pop(int(rng.integers(0, len(live))))
+            bm.prune(s)
+            tr.drop(s)
+            _check_bm_against_brute(bm, tr, used, [])
+        elif live and r < 0.55:
+            s = live[int(rng.integers(0, len(live)))]
+            toks = rng.integers(0, vocab, size=int(rng.integers(0, 7))).tolist()
+            table_before = bm.table(s)
+            try:
+                dst = bm.append(s, toks)
+            except BMError as e:
+                assert e.code == -2
+                continue
+            tr.append(s, toks, op_id)
+            table = bm.table(s)
+            fresh = table[len(table_before):]
+            # the tokens fill the path's last blocks in order: consecutive slots, block after block
+            runs = [d // bs for i, d in enumerate(dst) if i == 0 or d // bs != dst[i - 1] // bs]
+            assert runs == table[len(table) - len(runs):]
+            assert all(dst[i] + 1 == dst[i + 1] for i in range(len(dst) - 1) if dst[i] // bs == dst[i + 1] // bs)
+            assert all(d % bs == 0 for i, d in enumerate(dst) if i > 0 and d // bs != dst[i - 1] // bs)
+            _check_bm_against_brute(bm, tr, used, fresh)
+        elif live and r < 0.7:
+            uns = [s for s in live if s in tr.open]
+            if not uns:
+                continue
+            s = uns[int(rng.integers(0, len(uns)))]
+            bm.seal(s)
+            tr.seal(s)
+            _check_bm_against_brute(bm, tr, used, [])
+        else:
+            cands = [s for s in live if s not in tr.open]
+            parent = -1 if not cands or rng.random() < 0.2 else cands[int(rng.integers(0, len(cands)))]
+            toks = rng.integers(0, vocab, size=int(rng.integers(1 if parent == -1 else 0, 9))).tolist()
+            seal = bool(rng.random() < 0.5)
+            try:
+                s, new_blocks, hits = bm.extend(parent, toks, seal)
+            except BMError as e:
+                assert e.code == -2
+                continue
+            tr.extend_seq(s, parent, toks, seal, op_id)
+            live.append(s)
+            _check_bm_against_brute(bm, tr, used, [b for b, h in zip(new_blocks, hits) if not h])
+
+
+def test_append_then_seal_equals_sealed_extension():
+    # a step decoded token by token and sealed ends on the same blocks as the same step extended
+    # sealed in one go (here the sealed copy exists first, so every block is a hit)
+    bm = oracle.BlockManager(40, 4, 8)
+    root, _, _ = bm.extend(-1, [5, 6, 7, 8, 9], True)
+    toks = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11]
+    twin, _, _ = bm.extend(root, toks, True)
+    cand, _, _ = bm.extend(root, [], False)
+    for t in toks:
+        bm.append(cand, [t])
+    repl = bm.seal(cand)
+    assert bm.table(cand) == bm.table(twin) and len(repl) == 3
+    assert all(bm.refcount[b] == 2 for b in bm.table(twin)[2:])
+    assert bm.kv_len(cand) == 5 + len(toks)
