@@ -2,6 +2,9 @@
 
     python bench.py [--steps K] [--warmup W] [--workload beam_decode] [--gpus 1] [--no-cpu]
 
+(--workload kv_append times the K/V append kernel instead: all K/V writes of the spec_explosion
+tree, deduplicated blocks skipped.)
+
 A step is one tkv_decode (or tkv_verify) call over the whole batch: the shared-segment and
 private-suffix contractions of every row and the log-sum-exp merge.  The block manager has built
 the tree, rows are coalesced and the plan is built and uploaded before timing (host times are
@@ -57,6 +60,87 @@ def _args():
     return ap.parse_args()
 
 
+def bench_kv_append(a):
+    """The K/V writes of a whole tree in one tkv_kv_append launch: every token of every extension of
+    the spec_explosion script goes to the slot the block manager gave it, tokens of deduplicated
+    blocks are skipped.  HBM-bound: each written token moves hkv * d bf16 of K and of V in and out."""
+    import torch
+    import paper_2609_39334_amd as tkv
+    import workloads as W
+    dev = torch.device("cuda:0")
+    wl = W.spec_explosion(a.seed)
+    s = wl.shape
+    bm = tkv.BlockManager(wl.num_blocks, s.block_size, wl.max_seqs)
+    dsts = []
+    t0 = time.perf_counter()
+    seq_of = []
+    for e in wl.events:                   # replay the script, keeping each extension's slots
+        if isinstance(e, W.Extend):
+            parent = -1 if e.parent < 0 else seq_of[e.parent]
+            seq, blk, hit = bm.extend(parent, e.tokens, e.seal)
+            seq_of.append(seq)
+            if len(e.tokens):
+                dsts.append(tkv.tkv_extend_slots(blk, hit, len(e.tokens), s.block_size))
+        elif isinstance(e, W.Prune):
+            bm.prune(seq_of[e.handle])
+    t_host = time.perf_counter() - t0
+    dst = np.concatenate(dsts).astype(np.int32)
+    n_tok, n_written = len(dst), int((dst >= 0).sum())
+    rng = np.random.default_rng([a.seed, 5])
+    new_bits = W.f32_to_bf16_bits(rng.standard_normal((2, n_tok, s.hkv, s.d), dtype=np.float32))
+
+    def to_dev(x):
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    k_new, v_new = to_dev(new_bits[0]), to_dev(new_bits[1])
+    d_dst = torch.from_numpy(dst).to(dev)
+    k = torch.zeros((wl.num_blocks, s.hkv, s.block_size, s.d), dtype=torch.bfloat16, device=dev)
+    v = torch.zeros_like(k)
+    stream = torch.cuda.current_stream()
+    for _ in range(a.warmup):
+        tkv.tkv_kv_append(d_dst, k_new, v_new, k, v, stream)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(a.steps):
+        tkv.tkv_kv_append(d_dst, k_new, v_new, k, v, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / a.steps
+    row = s.hkv * s.d * 2
+    b_alg = n_written * row * 2 * 2 + n_tok * 4      # K and V read and written, plus the slots
+    gbs = b_alg / (ms_step / 1e3) / 1e9
+    cpu = None
+    if not a.no_cpu:
+        import oracle
+        kh = np.zeros((wl.num_blocks, s.hkv, s.block_size, s.d), dtype=np.uint16)
+        vh = np.zeros_like(kh)
+        done, t_cpu = 0, 0.0
+        while t_cpu < a.cpu_seconds and done < n_tok:
+            e = min(n_tok, done + 20000)
+            t0 = time.perf_counter()
+            oracle.kv_append(kh, vh, dst[done:e], new_bits[0][done:e], new_bits[1][done:e])
+            t_cpu += time.perf_counter() - t0
+            done = e
+        cpu = {"value": round(done / t_cpu, 1), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+               "sample": f"the first {done} of {n_tok} tokens, NumPy row scatter, {t_cpu:.1f} s"}
+    out = {
+        "metric": "kv-append tokens/s and % HBM roofline, tree K/V writes with deduplicated blocks skipped",
+        "value": round(n_tok / (ms_step / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (spec_explosion tree, N(0,1) bf16 rows)",
+        "config": {"workload": "kv_append", "tree": "spec_explosion", "hkv": s.hkv, "head_dim": s.d,
+                   "block_size": s.block_size, "tokens": n_tok, "written_tokens": n_written,
+                   "skipped_tokens": n_tok - n_written},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "kv_append",
+                     "algorithmic_bytes": b_alg, "kernel_us": round(ms_step * 1e3, 2)},
+        "cpu_baseline": cpu,
+        "host_ms": {"block_manager_and_slots": round(t_host * 1e3, 2)},
+    }
+    print(json.dumps(out))
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -70,6 +154,8 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU"}))
         sys.exit(1)
+    if a.workload == "kv_append":
+        return bench_kv_append(a)
     dev = torch.device("cuda:0")
     wl = W.CONFIGS[a.workload](a.seed)
     s = wl.shape

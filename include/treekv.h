@@ -228,6 +228,20 @@ int tkv_decode(const tkv_plan* plan, const void* q, const void* k, const void* v
 int tkv_verify(const tkv_plan* plan, const void* q, const void* k, const void* v, void* o,
                float* lse, void* hip_stream);
 
+/* Write the K and V of n_tok new tokens into the paged pool: the step before attention in a decode
+ * loop.  Token t's rows go to pool slot d_dst[t] = block * block_size + position (tkv_bm_append for
+ * tokens decoded one at a time, tkv_extend_slots for a completed step).  A slot of -1 -- a token of a
+ * block that was a deduplication hit, which already holds the same tokens' K/V (Sec. 4.2) -- is not
+ * written; so is any slot outside [0, num_blocks * block_size).
+ *   d_dst          [n_tok] int32, device
+ *   k_new, v_new   [n_tok][hkv][d] bf16, device
+ *   k, v           the pool, [num_blocks][hkv][block_size][d] bf16, device (written in place)
+ * shape: hkv, d, block_size and num_blocks are used (block_size 16, d in {64, 128}).  Enqueued on
+ * hip_stream; tokens with the same slot race (the block manager never gives one slot twice).
+ * EINVAL (shape, n_tok < 0, NULL pointers when n_tok > 0), EHIP (launch failure). */
+int tkv_kv_append(const tkv_shape* shape, const int32_t* d_dst, int32_t n_tok, const void* k_new, const void* v_new,
+                  void* k, void* v, void* hip_stream);
+
 /* Instrumentation.  tkv_plan_profile(plan, max_calls) makes the next max_calls attention calls on
  * this plan record HIP events taken from the kernel dispatches' own start and end timestamps: the
  * main attention phase (start of its first kernel to end of its last) and the merge kernel

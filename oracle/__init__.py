@@ -8,6 +8,7 @@ Contents
   block_manager  prefix-tree KV block manager (dedup key, refcounts, lowest-free allocation, prune)
   attention      fp64 gather attention: each row's full KV by block table, no sharing
   coalesce       computation-deduplication row coalescing (identical candidates submitted once)
+  kv_append      new tokens' K/V rows written to their pool slots (deduplicated blocks skipped)
 
 Pins: every function here is checked in tests/test_oracle.py against values that do not come from
 this package (brute force in pure Python, closed forms, invariants, hand-worked fixtures under
@@ -16,5 +17,6 @@ tests/golden/).
 from .attention import attention, gather_kv
 from .block_manager import BlockManager, BMError
 from .coalesce import coalesce
+from .kv_append import kv_append
 
-__all__ = ["attention", "gather_kv", "BlockManager", "BMError", "coalesce"]
+__all__ = ["attention", "gather_kv", "BlockManager", "BMError", "coalesce", "kv_append"]

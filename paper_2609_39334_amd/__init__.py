@@ -71,6 +71,7 @@ _SIG = {
     "tkv_plan_get_view": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_view)]),
     "tkv_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_verify": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
+    "tkv_kv_append": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _P, _I32, _P, _P, _P, _P, _P]),
     "tkv_plan_profile": (ctypes.c_int, [_P, _I32]),
     "tkv_plan_profile_read": (ctypes.c_int, [_P, _PI32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
 }
@@ -301,6 +302,24 @@ def tkv_decode(plan: int, q, k, v, o, lse=None, stream=None) -> None:
 
 def tkv_verify(plan: int, q, k, v, o, lse=None, stream=None) -> None:
     _attn(lib().tkv_verify, plan, q, k, v, o, lse, stream)
+
+
+def tkv_kv_append(dst: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                  stream=None) -> None:
+    """Writes new tokens' K/V rows into the paged pool at their slots (dst int32, -1 = skip).
+    k_new, v_new: [n_tok, hkv, d] bf16; k, v: [num_blocks, hkv, block_size, d] bf16 (all on the GPU)."""
+    nb, hkv, bs, d = k.shape
+    n = int(dst.numel())
+    for t, shp in ((k_new, (n, hkv, d)), (v_new, (n, hkv, d)), (v, tuple(k.shape))):
+        if tuple(t.shape) != shp or t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"tkv_kv_append: expected a contiguous bf16 GPU tensor of shape {shp}, got {tuple(t.shape)}")
+    if k.dtype != torch.bfloat16 or not k.is_contiguous() or not k.is_cuda:
+        raise ValueError("tkv_kv_append: the pool must be a contiguous bf16 GPU tensor")
+    if dst.dtype != torch.int32 or not dst.is_cuda or not dst.is_contiguous():
+        raise ValueError("tkv_kv_append: dst must be a contiguous int32 GPU tensor")
+    shape = tkv_shape(0, hkv, d, bs, nb)
+    _check(lib().tkv_kv_append(ctypes.byref(shape), dst.data_ptr(), n, k_new.data_ptr(), v_new.data_ptr(),
+                               k.data_ptr(), v.data_ptr(), _stream(stream)))
 
 
 def tkv_plan_profile(plan: int, max_calls: int) -> None:

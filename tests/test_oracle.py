@@ -540,3 +540,99 @@ def test_append_then_seal_equals_sealed_extension():
     assert bm.table(cand) == bm.table(twin) and len(repl) == 3
     assert all(bm.refcount[b] == 2 for b in bm.table(twin)[2:])
     assert bm.kv_len(cand) == 5 + len(toks)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_kv_append_rows_follow_paths(seed):
+    # A decode loop writes each new token's K row with oracle.kv_append at the slot the block manager
+    # gave it (append: its own slots; a sealed extension: its blocks' slots, none for a hit block).
+    # Independently, every path's rows are modelled position by position: a token appended or
+    # extended brings its own row, except in a chunk that deduplicated, which shows the rows of the
+    # chunk's first writer.  Gathering every live path from the pool must give the modelled rows.
+    rng = np.random.default_rng(300 + seed)
+    bs, hkv, d = 4, 2, 3
+    bm = oracle.BlockManager(80, bs, 16)
+    tr = _StepTracker(bs)
+    pool = np.full((80, hkv, bs, d), np.nan)
+    vpool = np.full((80, hkv, bs, d), np.nan)
+    first_rows = {}                  # sealed chunk identity -> rows of its first writer
+    open_rows = {}                   # seq -> rows of its open step
+    rows = {}                        # seq -> modelled rows, one [hkv, d] array per path position
+    live = []
+
+    def fresh(n):
+        return rng.standard_normal((n, hkv, d))
+
+    def settle(s):
+        # positions of sealed chunks show their first writer's rows
+        out, pos = [], 0
+        for ci, idn in enumerate(tr.ident[s]):
+            n_in = bm.block_len[bm.table(s)[ci]]
+            if idn[0] == "S":
+                out += list(first_rows[idn])
+            else:
+                out += list(rows[s][pos:pos + n_in])
+            pos += n_in
+        rows[s] = out
+
+    for op_id in range(160):
+        r = rng.random()
+        vocab = 2 if rng.random() < 0.6 else 40
+        if live and r < 0.15:
+            s = live.pop(int(rng.integers(0, len(live))))
+            bm.prune(s)
+            tr.drop(s)
+            del rows[s]
+            continue
+        if live and r < 0.55:
+            s = live[int(rng.integers(0, len(live)))]
+            toks = rng.integers(0, vocab, size=int(rng.integers(0, 6))).tolist()
+            try:
+                dst = bm.append(s, toks)
+            except BMError:
+                continue
+            tr.append(s, toks, op_id)
+            new = fresh(len(toks))
+            oracle.kv_append(pool, vpool, dst, new, new)
+            rows[s] = rows[s] + list(new)
+        elif live and r < 0.7:
+            s = live[int(rng.integers(0, len(live)))]
+            if s not in tr.open:
+                continue
+            n_open = -(-len(tr.open[s][1]) // bs)
+            base = len(tr.ident[s]) - n_open
+            blens = [bm.block_len[b] for b in bm.table(s)]
+            start = sum(blens[:base])
+            bm.seal(s)
+            tr.seal(s)
+            pos = start
+            for ci in range(base, len(tr.ident[s])):
+                n_in = bm.block_len[bm.table(s)[ci]]
+                first_rows.setdefault(tr.ident[s][ci], rows[s][pos:pos + n_in])
+                pos += n_in
+            settle(s)
+        else:
+            cands = [s for s in live if s not in tr.open]
+            parent = -1 if not cands or rng.random() < 0.2 else cands[int(rng.integers(0, len(cands)))]
+            toks = rng.integers(0, vocab, size=int(rng.integers(1 if parent == -1 else 0, 9))).tolist()
+            seal = bool(rng.random() < 0.5)
+            try:
+                s, blk, hit = bm.extend(parent, toks, seal)
+            except BMError:
+                continue
+            tr.extend_seq(s, parent, toks, seal, op_id)
+            live.append(s)
+            dst = [-1 if hit[t // bs] else blk[t // bs] * bs + t % bs for t in range(len(toks))]
+            new = fresh(len(toks))
+            oracle.kv_append(pool, vpool, dst, new, new)
+            rows[s] = (list(rows[parent]) if parent >= 0 else []) + list(new)
+            if seal:
+                base = len(tr.ident[s]) - len(blk)
+                for j in range(len(blk)):
+                    a = j * bs
+                    first_rows.setdefault(tr.ident[s][base + j], list(new[a:a + bs]))
+            settle(s)
+        for s in live:
+            got = oracle.gather_kv(pool, bm.table(s), bm.block_len)       # [hkv, N, d]
+            want = np.stack(rows[s], axis=1) if rows[s] else np.zeros((hkv, 0, d))
+            np.testing.assert_array_equal(got, want)
