@@ -60,6 +60,14 @@ def _args():
     return ap.parse_args()
 
 
+def calibration_copy(torch, dev):
+    """One plain 256 MiB device-to-device copy: a kernel of known size for the PMC byte counters."""
+    src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 def bench_kv_append(a):
     """The K/V writes of a whole tree in one tkv_kv_append launch: every token of every extension of
     the spec_explosion script goes to the slot the block manager gave it, tokens of deduplicated
@@ -97,6 +105,8 @@ def bench_kv_append(a):
     k = torch.zeros((wl.num_blocks, s.hkv, s.block_size, s.d), dtype=torch.bfloat16, device=dev)
     v = torch.zeros_like(k)
     stream = torch.cuda.current_stream()
+    if a.calib_copy:
+        calibration_copy(torch, dev)
     for _ in range(a.warmup):
         tkv.tkv_kv_append(d_dst, k_new, v_new, k, v, stream)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -204,12 +214,8 @@ def main():
     stream = torch.cuda.current_stream()
     call = plan.decode if L.decode else plan.verify
 
-    if a.calib_copy:                         # a copy kernel of known size for the PMC byte counters
-        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    if a.calib_copy:
+        calibration_copy(torch, dev)
     for i in range(a.warmup):
         call(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
     ev0 = torch.cuda.Event(enable_timing=True)
