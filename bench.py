@@ -3,7 +3,8 @@
     python bench.py [--steps K] [--warmup W] [--workload beam_decode] [--gpus 1] [--no-cpu]
 
 (--workload kv_append times the K/V append kernel instead: all K/V writes of the spec_explosion
-tree, deduplicated blocks skipped.)
+tree, deduplicated blocks skipped.  --workload cd_sample times one CD branching step of the
+spec_explosion decode batch.)
 
 A step is one tkv_decode (or tkv_verify) call over the whole batch: the shared-segment and
 private-suffix contractions of every row and the log-sum-exp merge.  The block manager has built
@@ -151,6 +152,77 @@ def bench_kv_append(a):
     print(json.dumps(out))
 
 
+def bench_cd_sample(a):
+    """One CD branching step: the spec_explosion decode batch's distinct rows, each with its
+    multiplicity as potential size, draw from synthetic logits over a 151,936-token vocabulary (the
+    Qwen2.5 generators' vocabulary size) and group their draws.  HBM-bound on reading the logits."""
+    import torch
+    import paper_2609_39334_amd as tkv
+    import workloads as W
+    dev = torch.device("cuda:0")
+    wl = W.spec_explosion(a.seed)
+    bm = tkv.BlockManager(wl.num_blocks, wl.shape.block_size, wl.max_seqs)
+    got = {}
+    W.drive(wl, bm, on_launch=lambda i, l, c: got.setdefault("c", c))
+    seqs = [x for x, _ in got["c"]]
+    _, first, mult = bm.coalesce(seqs, [1] * len(seqs))
+    n_rows, vocab, temperature = len(first), 151936, 0.8
+    potential = np.asarray(mult, dtype=np.int64)
+    off = np.concatenate([[0], np.cumsum(potential)]).astype(np.int32)
+    rng = np.random.default_rng([a.seed, 6])
+    logits = torch.empty((n_rows, vocab), dtype=torch.float32, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(a.seed)
+    logits.normal_(0.0, 2.0, generator=gen)
+    u = torch.from_numpy(rng.random(int(off[-1]), dtype=np.float32)).to(dev)
+    d_off = torch.from_numpy(off).to(dev)
+    mp = int(potential.max())
+    stream = torch.cuda.current_stream()
+    if a.calib_copy:
+        calibration_copy(torch, dev)
+    for _ in range(a.warmup):
+        tkv.tkv_cd_sample(logits, temperature, d_off, u, mp, stream)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(a.steps):
+        tkv.tkv_cd_sample(logits, temperature, d_off, u, mp, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / a.steps
+    tok, cnt, ng = tkv.tkv_cd_sample(logits, temperature, d_off, u, mp, stream)
+    torch.cuda.synchronize()
+    n_groups = int(ng.sum().item())
+    b_alg = n_rows * vocab * 4 + int(off[-1]) * (4 + 8) + (n_rows + 1) * 4 + n_rows * 4
+    gbs = b_alg / (ms_step / 1e3) / 1e9
+    cpu = None
+    if not a.no_cpu:
+        import oracle
+        lg = logits.cpu().numpy()
+        uh = u.cpu().numpy()
+        done, t_cpu = 0, 0.0
+        while t_cpu < a.cpu_seconds and done < n_rows:
+            t0 = time.perf_counter()
+            oracle.cd_sample.cd_sample(lg[done:done + 1], temperature, potential[done:done + 1], uh[off[done]:off[done + 1]])
+            t_cpu += time.perf_counter() - t0
+            done += 1
+        cpu = {"value": round(done / t_cpu, 1), "unit": "rows/s", "cores": 1, "kind": "oracle",
+               "sample": f"the first {done} of {n_rows} rows, NumPy float64 softmax and inverse CDF, {t_cpu:.1f} s"}
+    out = {
+        "metric": "CD branching rows/s and % HBM roofline (logits read once), one sampling step",
+        "value": round(n_rows / (ms_step / 1e3), 1), "unit": "rows/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp32", "data": "synthetic (N(0, 2) fp32 logits, spec_explosion potentials)",
+        "config": {"workload": "cd_sample", "rows": n_rows, "draws": int(off[-1]), "vocab": vocab,
+                   "temperature": temperature, "max_potential": mp, "groups": n_groups},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "cd_sample",
+                     "algorithmic_bytes": b_alg, "kernel_us": round(ms_step * 1e3, 2)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -166,6 +238,8 @@ def main():
         sys.exit(1)
     if a.workload == "kv_append":
         return bench_kv_append(a)
+    if a.workload == "cd_sample":
+        return bench_cd_sample(a)
     dev = torch.device("cuda:0")
     wl = W.CONFIGS[a.workload](a.seed)
     s = wl.shape

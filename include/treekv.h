@@ -96,6 +96,16 @@ int tkv_bm_append(tkv_bm* bm, int32_t seq, const int32_t* tokens, int32_t n, int
  * EINVAL if the sequence is already sealed or a pointer is NULL; ENOSEQ. */
 int tkv_bm_seal(tkv_bm* bm, int32_t seq, int32_t* replaced_out, int32_t cap, int32_t* n_replaced_out);
 
+/* Branch a live sequence where its candidates' next tokens differ (on-demand branching of
+ * computation deduplication, Sec. 4.2: one child per distinct sampled token, e.g. from
+ * tkv_cd_sample).  The open step, if any, is sealed first (tkv_bm_seal) -- the point of divergence
+ * becomes a step boundary, so the children share every block before it -- then token i starts
+ * child_out[i], a new sequence whose open step holds that token (children take the lowest free ids in
+ * token order).  The parent stays live; release it with tkv_prune when it is no longer a candidate.
+ * A single distinct token needs no branch: append it instead.  Errors: EINVAL (n < 0, NULL),
+ * ENOSEQ, ENOMEM (fewer than n free blocks or sequence slots), ECAP (cap < n); nothing changes. */
+int tkv_bm_fork(tkv_bm* bm, int32_t seq, const int32_t* tokens, int32_t n, int32_t* child_out, int32_t cap);
+
 /* Pool slots of a new step's tokens for tkv_kv_append, from tkv_bm_extend's outputs: token t of n_tok
  * goes to block blk[t / block_size] at slot t % block_size, or nowhere (-1) where that block was a
  * deduplication hit -- the block already holds the same tokens' K/V, so the write is skipped.
@@ -241,6 +251,29 @@ int tkv_verify(const tkv_plan* plan, const void* q, const void* k, const void* v
  * EINVAL (shape, n_tok < 0, NULL pointers when n_tok > 0), EHIP (launch failure). */
 int tkv_kv_append(const tkv_shape* shape, const int32_t* d_dst, int32_t n_tok, const void* k_new, const void* v_new,
                   void* k, void* v, void* hip_stream);
+
+/* ======================================================================== CD branching sampler
+ * On-demand branching of computation deduplication (Sec. 4.2): a sequence with potential size n
+ * stands for n identical candidates; its one row of logits gives n independent draws from the
+ * temperature softmax p_j = exp(l_j / T) / sum_i exp(l_i / T) (Sec. 2.1), grouped by token: one child
+ * per distinct token (tkv_bm_fork), whose potential is the group's size.  Rows of any potential run
+ * in one launch.
+ * Draw k of row r is the inverse CDF at uniform u = d_uniform[d_draw_off[r] + k]: the first token j
+ * (in token order) whose cumulative weight exceeds u times the total, the weights and their sums in
+ * fp32 (exp2 of the scaled logit minus the row maximum); a token with logit -inf is never drawn.
+ *   d_logits    [n_rows][vocab] fp32 (finite or -inf, no NaN), device
+ *   d_draw_off  [n_rows + 1] int32, device: row r draws potential_r = off[r + 1] - off[r] tokens,
+ *               0 <= potential_r <= max_potential <= 1024
+ *   d_uniform   [off[n_rows]] fp32 in [0, 1), device (the caller's random numbers)
+ *   d_token, d_count  [off[n_rows]] int32, device: row r's groups at [off[r], off[r] + d_n_groups[r]),
+ *               tokens ascending, counts summing to potential_r
+ *   d_n_groups  [n_rows] int32, device: distinct tokens of the row (-1: no finite logit, or a
+ *               potential above 1024)
+ * Enqueued on hip_stream.  EINVAL (n_rows < 0, vocab < 1, temperature not positive and finite,
+ * max_potential outside [0, 1024], NULL pointers), EHIP. */
+int tkv_cd_sample(int32_t n_rows, int32_t vocab, float temperature, int32_t max_potential, const float* d_logits,
+                  const float* d_uniform, const int32_t* d_draw_off, int32_t* d_token, int32_t* d_count,
+                  int32_t* d_n_groups, void* hip_stream);
 
 /* Instrumentation.  tkv_plan_profile(plan, max_calls) makes the next max_calls attention calls on
  * this plan record HIP events taken from the kernel dispatches' own start and end timestamps: the

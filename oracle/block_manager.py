@@ -30,6 +30,11 @@ Growing a path token by token (a decode loop) and completing a step:
   own block with the live sealed block of the same key (whose refcount rises; the own block, held
   by this sequence only, is freed); a miss indexes the block.  As in an extension, once a block
   misses every later one misses (a block that was just indexed precedes nothing in the index).
+* fork(seq, tokens) branches a sequence where its candidates' next tokens differ (the on-demand
+  branching of Sec. 4.2): the open step, if any, is sealed there -- the point of divergence becomes a
+  step boundary, so the children share every block before it -- and each token starts one child, a
+  new sequence whose open step holds that token.  The children take the lowest free sequence ids in
+  token order.  Nothing changes unless every child gets its block and sequence slot.
 """
 from __future__ import annotations
 
@@ -145,6 +150,18 @@ class BlockManager:
             self.block_len[b] += 1
             open_toks.append(t)
         return dst
+
+    def fork(self, seq: int, tokens) -> List[int]:
+        """Branch `seq`: seal its open step, then one open child per token.  Returns the children."""
+        toks = [int(t) for t in np.asarray(tokens).reshape(-1)]
+        if seq not in self.seqs:
+            raise BMError(ENOSEQ, f"unknown sequence {seq}")
+        if len(toks) > len(self.free_blocks) or len(toks) > len(self.free_seqs):
+            raise BMError(ENOMEM, f"fork into {len(toks)} children: {len(self.free_blocks)} blocks, "
+                                  f"{len(self.free_seqs)} sequence slots free")
+        if not self.seqs[seq]["sealed"]:
+            self.seal(seq)
+        return [self.extend(seq, [t], False)[0] for t in toks]
 
     def seal(self, seq: int) -> List[Tuple[int, int]]:
         """Complete the open step of `seq`; returns the (own block, live sealed block) replacements."""

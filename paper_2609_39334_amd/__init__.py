@@ -56,6 +56,7 @@ _SIG = {
     "tkv_prune": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32]),
     "tkv_bm_append": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32, _I32]),
     "tkv_bm_seal": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32]),
+    "tkv_bm_fork": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32, _I32]),
     "tkv_extend_slots": (ctypes.c_int, [_PI32, _PU8, _I32, _I32, _I32, _PI32]),
     "tkv_bm_table": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32, _PI32]),
     "tkv_bm_refcount": (ctypes.c_int, [_P, _I32, _PI32]),
@@ -72,6 +73,7 @@ _SIG = {
     "tkv_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_verify": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_kv_append": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _P, _I32, _P, _P, _P, _P, _P]),
+    "tkv_cd_sample": (ctypes.c_int, [_I32, _I32, ctypes.c_float, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "tkv_plan_profile": (ctypes.c_int, [_P, _I32]),
     "tkv_plan_profile_read": (ctypes.c_int, [_P, _PI32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
 }
@@ -173,6 +175,14 @@ def tkv_bm_seal(bm: int, seq: int):
     out = np.zeros(2 * n.value, dtype=np.int32)
     _check(lib().tkv_bm_seal(bm, seq, _ptr(out), n.value, ctypes.byref(n)))
     return [(int(out[2 * i]), int(out[2 * i + 1])) for i in range(n.value)]
+
+
+def tkv_bm_fork(bm: int, seq: int, tokens) -> list:
+    """Branches a sequence: seals its open step, then one open child per token; returns the children."""
+    t = _i32(tokens)
+    out = np.zeros(max(1, len(t)), dtype=np.int32)
+    _check(lib().tkv_bm_fork(bm, seq, _ptr(t), len(t), _ptr(out), len(t)))
+    return [int(x) for x in out[:len(t)]]
 
 
 def tkv_extend_slots(blk, hit, n_tok: int, block_size: int = 16) -> np.ndarray:
@@ -322,6 +332,27 @@ def tkv_kv_append(dst: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, k
                                k.data_ptr(), v.data_ptr(), _stream(stream)))
 
 
+def tkv_cd_sample(logits: torch.Tensor, temperature: float, draw_off: torch.Tensor, uniform: torch.Tensor,
+                  max_potential: int, stream=None):
+    """Draws each row's potential-many tokens and groups them; returns device tensors
+    (tokens, counts, n_groups): row r's groups at [draw_off[r], draw_off[r] + n_groups[r])."""
+    if logits.dim() != 2 or logits.dtype != torch.float32 or not logits.is_cuda or not logits.is_contiguous():
+        raise ValueError("tkv_cd_sample: logits must be a contiguous float32 GPU tensor [n_rows, vocab]")
+    n_rows, vocab = logits.shape
+    if draw_off.dtype != torch.int32 or draw_off.numel() != n_rows + 1 or not draw_off.is_cuda:
+        raise ValueError("tkv_cd_sample: draw_off must be an int32 GPU tensor of n_rows + 1 entries")
+    if uniform.dtype != torch.float32 or not uniform.is_cuda or not uniform.is_contiguous():
+        raise ValueError("tkv_cd_sample: uniform must be a contiguous float32 GPU tensor")
+    n = max(1, int(uniform.numel()))
+    tok = torch.empty(n, dtype=torch.int32, device=logits.device)
+    cnt = torch.empty(n, dtype=torch.int32, device=logits.device)
+    ng = torch.empty(max(1, n_rows), dtype=torch.int32, device=logits.device)
+    _check(lib().tkv_cd_sample(n_rows, vocab, float(temperature), int(max_potential), logits.data_ptr(),
+                               uniform.data_ptr(), draw_off.data_ptr(), tok.data_ptr(), cnt.data_ptr(), ng.data_ptr(),
+                               _stream(stream)))
+    return tok, cnt, ng[:n_rows]
+
+
 def tkv_plan_profile(plan: int, max_calls: int) -> None:
     _check(lib().tkv_plan_profile(plan, max_calls))
 
@@ -358,6 +389,9 @@ class BlockManager:
 
     def seal(self, seq):
         return tkv_bm_seal(self.h, seq)
+
+    def fork(self, seq, tokens):
+        return tkv_bm_fork(self.h, seq, tokens)
 
     def table(self, seq):
         return tkv_bm_table(self.h, seq)[0]

@@ -18,7 +18,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
 HOST_SOURCES = ["capi.cpp", "bm.cpp", "plan.cpp"]
-HIP_SOURCES = ["attn.hip", "kv_append.hip"]
+HIP_SOURCES = ["attn.hip", "kv_append.hip", "cd_sample.hip"]
 
 HOST_FLAGS = ["-std=c++17", "-O2", "-fPIC", "-fvisibility=hidden", "-Wall", "-Wextra", "-Wno-unused-parameter"]
 HIP_FLAGS = [

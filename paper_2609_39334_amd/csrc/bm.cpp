@@ -269,6 +269,33 @@ TKV_EXPORT int tkv_bm_seal(tkv_bm* bm, int32_t seq, int32_t* replaced_out, int32
     return TKV_OK;
 }
 
+TKV_EXPORT int tkv_bm_fork(tkv_bm* bm, int32_t seq, const int32_t* tokens, int32_t n, int32_t* child_out,
+                           int32_t cap) {
+    tkv::clear_error();
+    if (!bm || (n > 0 && (!tokens || !child_out))) return set_error(TKV_EINVAL, "tkv_bm_fork: NULL argument");
+    if (n < 0) return set_error(TKV_EINVAL, "tkv_bm_fork: n = %d < 0", n);
+    if (!seq_live(bm, seq)) return set_error(TKV_ENOSEQ, "tkv_bm_fork: sequence %d is not live", seq);
+    if (cap < n) return set_error(TKV_ECAP, "tkv_bm_fork: output capacity %d < %d children", cap, n);
+    if (static_cast<size_t>(n) > bm->free_blocks.size() || static_cast<size_t>(n) > bm->free_seqs.size())
+        return set_error(TKV_ENOMEM, "tkv_bm_fork: %d children need as many blocks and sequence slots (%zu, %zu free)", n,
+                         bm->free_blocks.size(), bm->free_seqs.size());
+    // the point of divergence becomes a step boundary: seal the open step, then one open child per token
+    if (!bm->seqs[seq].sealed) {
+        const size_t n_open = (bm->seqs[seq].open.size() + bm->block_size - 1) / bm->block_size;
+        std::vector<int32_t> replaced(2 * std::max<size_t>(1, n_open));
+        int32_t nr = 0;
+        const int rc = tkv_bm_seal(bm, seq, replaced.data(), static_cast<int32_t>(n_open), &nr);
+        if (rc != TKV_OK) return rc;
+    }
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t blk = 0, nb = 0;
+        uint8_t hit = 0;
+        const int rc = tkv_bm_extend(bm, seq, tokens + i, 1, 0, child_out + i, &blk, &hit, 1, &nb);
+        if (rc != TKV_OK) return rc;  // cannot happen: blocks and slots were checked above
+    }
+    return TKV_OK;
+}
+
 TKV_EXPORT int tkv_extend_slots(const int32_t* blk, const uint8_t* hit, int32_t n_blk, int32_t n_tok,
                                 int32_t block_size, int32_t* dst_out) {
     tkv::clear_error();

@@ -158,3 +158,19 @@ def test_seal_errors_leave_state_unchanged():
     with pytest.raises(tkv.TkvError) as e:
         bm.seal(c)
     assert e.value.code == tkv.TKV_EINVAL
+
+
+def test_fork_errors_leave_state_unchanged():
+    bm, p, c = _bm()                                       # 7 blocks and 2 sequence slots free
+    before = bm.snapshot()
+    with pytest.raises(tkv.TkvError) as e:
+        bm.fork(c, [1, 2, 3])                              # 3 children, 2 sequence slots
+    assert e.value.code == tkv.TKV_ENOMEM
+    _same(before, bm.snapshot())                           # the open step was not sealed either
+    with pytest.raises(tkv.TkvError) as e:
+        bm.fork(9, [1])
+    assert e.value.code == tkv.TKV_ENOSEQ
+    _same(before, bm.snapshot())
+    kids = bm.fork(c, [5, 6])
+    snap = bm.snapshot()["seqs"]
+    assert snap[c][1] == 1 and all(snap[k][1:] == (0, 1) for k in kids)

@@ -109,6 +109,28 @@ class _Pair:
         self.ops += 1
         return ro
 
+    def fork(self, seq, tokens):
+        err_o = err_c = None
+        try:
+            ko = self.o.fork(seq, tokens)
+        except oracle.BMError as e:
+            err_o = e.code
+        try:
+            kc = self.c.fork(seq, tokens)
+        except tkv.TkvError as e:
+            err_c = e.code
+        assert err_o == err_c
+        if err_o is not None:
+            raise oracle.BMError(err_o, "both failed")
+        assert ko == kc
+        touched = list(self.o.table(seq))
+        for k in ko:
+            assert tuple(self.o.table(k)) == tuple(int(x) for x in self.c.table(k))
+            touched += self.o.table(k)
+        self._cmp_arrays(touched)
+        self.ops += 1
+        return ko
+
     def full_compare(self):
         so, sc = self.o.snapshot(), self.c.snapshot()
         _arrays_equal(so, sc)
@@ -207,6 +229,12 @@ def test_decode_loop_scripts_lockstep(seed):
                 else:
                     with pytest.raises(oracle.BMError):          # sealing a sealed sequence fails on both
                         p.seal(s)
+            elif live and r < 0.78:                              # on-demand branching into 2-4 children
+                s = live[int(rng.integers(0, len(live)))]
+                kids = p.fork(s, rng.integers(0, vocab, size=int(rng.integers(2, 5))).tolist())
+                open_.discard(s)
+                live += kids
+                open_.update(kids)
             else:
                 cands = [s for s in live if s not in open_]
                 parent = -1 if not cands or rng.random() < 0.2 else cands[int(rng.integers(0, len(cands)))]

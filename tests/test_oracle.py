@@ -7,6 +7,7 @@ causal verify == decode over truncated prefixes, padding never read).
 Block manager: hand-worked fixtures, the paper's computation-deduplication example, and a
 brute-force characterisation of deduplication checked after every operation of random scripts.
 """
+import itertools
 import json
 import math
 import os
@@ -636,3 +637,65 @@ def test_kv_append_rows_follow_paths(seed):
             got = oracle.gather_kv(pool, bm.table(s), bm.block_len)       # [hkv, N, d]
             want = np.stack(rows[s], axis=1) if rows[s] else np.zeros((hkv, 0, d))
             np.testing.assert_array_equal(got, want)
+
+
+def _softmax_py(logits, temperature):
+    # plain Python (math module), independent of the oracle's NumPy
+    m = max(logits)
+    e = [math.exp((x - m) / temperature) if x != -math.inf else 0.0 for x in logits]
+    z = sum(e)
+    return [x / z for x in e]
+
+
+def test_cd_sample_paper_example():
+    g = _load("cd_sample_of_that.json")
+    p = _softmax_py(g["logits"], g["temperature"])
+    cdf = list(itertools.accumulate(p))
+    for tok, (a, b) in g["expect"]["cdf_intervals"].items():      # the hand-worked intervals
+        t = int(tok)
+        assert abs(cdf[t - 1] - a) < 1e-5 and abs(cdf[t] - b) < 1e-5
+    draws = oracle.cd_sample.draw(np.array(g["logits"]), g["temperature"], g["uniforms"])
+    assert draws == g["expect"]["draws"]
+    toks, counts = oracle.cd_sample.group(draws)
+    assert toks == g["expect"]["tokens"] and counts == g["expect"]["counts"]
+    assert [g["vocab_words"][t] for t in toks] == ["of", "that"]
+    # the branch: the parent's open step is sealed, one open child per distinct token
+    bm = oracle.BlockManager(16, g["block_size"], 8)
+    root, _, _ = bm.extend(-1, g["prefix"], True)
+    parent, _, _ = bm.extend(root, g["open_step"], False)
+    kids = bm.fork(parent, toks)
+    assert kids == g["expect_fork"]["children"]
+    assert [bm.table(k) for k in kids] == g["expect_fork"]["child_tables"]
+    assert bm.snapshot()["seqs"][parent][1] == g["expect_fork"]["parent_sealed"]
+
+
+def test_cd_sample_matches_the_distribution():
+    # 40,000 independent draws from a 60-token distribution against its probabilities (chi-square)
+    from scipy.stats import chi2
+    rng = np.random.default_rng(7)
+    logits = (rng.standard_normal(60) * 1.5).tolist()
+    logits[5] = -math.inf                                          # a masked token is never drawn
+    p = np.array(_softmax_py(logits, 0.8))
+    u = rng.random(40000)
+    draws = oracle.cd_sample.draw(np.array(logits), 0.8, u)
+    counts = np.bincount(draws, minlength=60)
+    assert counts[5] == 0
+    keep = p * len(u) >= 5
+    stat = float((((counts - p * len(u)) ** 2) / np.where(keep, p * len(u), 1))[keep].sum())
+    assert chi2.sf(stat, int(keep.sum()) - 1) > 1e-4
+    toks, cnt = oracle.cd_sample.group(draws)
+    assert sum(cnt) == len(u) and toks == sorted(set(draws))
+
+
+def test_cd_sample_closed_forms():
+    V = 37
+    u = (np.arange(200) + 0.5) / 200                               # no uniform on a boundary j / V
+    assert oracle.cd_sample.draw(np.zeros(V), 1.3, u) == [int(x * V) for x in u]   # equal logits: floor(u V)
+    logits = np.random.default_rng(3).standard_normal(50)
+    top = int(np.argmax(logits))
+    assert set(oracle.cd_sample.draw(logits, 1e-3, u)) == {top}    # temperature -> 0: the argmax
+    # scaling logits and temperature together changes nothing
+    assert oracle.cd_sample.draw(logits, 0.7, u) == oracle.cd_sample.draw(2 * logits, 1.4, u)
+    # rows take consecutive slices of the uniforms
+    rows = oracle.cd_sample.cd_sample(np.stack([np.zeros(V), logits[:V]]), 1.0, [3, 2], u[:5])
+    assert rows[0][2] == [int(x * V) for x in u[:3]] and len(rows[1][2]) == 2
