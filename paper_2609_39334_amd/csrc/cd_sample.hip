@@ -101,11 +101,15 @@ __global__ __launch_bounds__(kSampleThreads) void cd_sample(const float* __restr
         return;
     }
 
-    // one pass over the row: per tile its maximum and its total over that base
-    float x[kPerThread];
+    // one pass over the row: per tile its maximum and its total over that base (the next tile's
+    // loads in flight while one is reduced)
+    float x[kPerThread], xn[kPerThread];
     float mx = -INFINITY;
+    load16<VEC>(row, vocab, 0, t, xn);
     for (int i = 0; i < n_tiles; ++i) {
-        load16<VEC>(row, vocab, i, t, x);
+#pragma unroll
+        for (int k = 0; k < kPerThread; ++k) x[k] = xn[k];
+        if (i + 1 < n_tiles) load16<VEC>(row, vocab, i + 1, t, xn);
         float m = x[0];
 #pragma unroll
         for (int k = 1; k < kPerThread; ++k) m = fmaxf(m, x[k]);
