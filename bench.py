@@ -32,14 +32,29 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 MALL_BYTES = 256 << 20
 
 
-def kernel_sources_digest():
-    """sha256 over the sources that decide what the attention kernels do (kernels, planner)."""
+ATTN_SOURCES = ("attn.hip", "plan.cpp", "internal.h")
+
+
+def kernel_sources_digest(files=ATTN_SOURCES):
+    """sha256 over the sources that decide what a kernel does (for attention: kernels and planner)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("attn.hip", "plan.cpp", "internal.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2609_39334_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+def measured_traffic(a, key, files):
+    """HBM bytes per launch from the committed PMC summary, or None when the kernel's sources have
+    changed since the counters were taken."""
+    if not (a.traffic and os.path.exists(a.traffic)):
+        return None
+    with open(a.traffic) as f:
+        tr = json.load(f).get(key)
+    if tr and tr.get("sources_sha256") == kernel_sources_digest(files):
+        return tr.get("bytes_per_launch")
+    return None
 
 
 def _args():
@@ -144,7 +159,8 @@ def bench_kv_append(a):
                    "block_size": s.block_size, "tokens": n_tok, "written_tokens": n_written,
                    "skipped_tokens": n_tok - n_written},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "kv_append",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(a, "kv_append", ("kv_append.hip", "internal.h")), "kernel": "kv_append",
                      "algorithmic_bytes": b_alg, "kernel_us": round(ms_step * 1e3, 2)},
         "cpu_baseline": cpu,
         "host_ms": {"block_manager_and_slots": round(t_host * 1e3, 2)},
@@ -216,7 +232,8 @@ def bench_cd_sample(a):
         "config": {"workload": "cd_sample", "rows": n_rows, "draws": int(off[-1]), "vocab": vocab,
                    "temperature": temperature, "max_potential": mp, "groups": n_groups},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "cd_sample",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(a, "cd_sample", ("cd_sample.hip", "internal.h")), "kernel": "cd_sample",
                      "algorithmic_bytes": b_alg, "kernel_us": round(ms_step * 1e3, 2)},
         "cpu_baseline": cpu,
     }
@@ -318,12 +335,7 @@ def main():
     flops = st["flops"]
     cand_tok_s = n_qtok / (ms_step / 1e3)
     achieved_gbs = b_uniq / t_main / 1e9
-    traffic = None
-    if a.traffic and os.path.exists(a.traffic):
-        with open(a.traffic) as f:
-            tr = json.load(f).get(a.workload)
-        if tr and tr.get("sources_sha256") == kernel_sources_digest():
-            traffic = tr.get("bytes_per_launch")
+    traffic = measured_traffic(a, a.workload, ATTN_SOURCES)
     main_kernels = ["attn_fwd"]  # tile items and the wave grid in one launch
     # the bound is the one the work's arithmetic intensity puts it under (ridge: peak flop/s over
     # peak bytes/s); decode is HBM-bound, multi-token verify of long steps is MFMA-bound
