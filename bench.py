@@ -240,6 +240,140 @@ def bench_cd_sample(a):
     print(json.dumps(out))
 
 
+def bench_verify_sweep(a):
+    """Verification throughput against batch size, the shape of the paper's verify-throughput
+    microbenchmark (Sec. 4.3, from which it takes its 2,048-token flush threshold), for the attention
+    layer of a 28/4/128 verifier (the head layout of a 7B reward model).  A batch is candidate steps
+    U{32..256} in sibling groups of 4 under parent steps U{64..256} of a 1,024-token prompt, as lazy
+    verification flushes them, filled up to T query tokens; each T is one tkv_verify call."""
+    import torch
+    import paper_2609_39334_amd as tkv
+    import workloads as W
+    dev = torch.device("cuda:0")
+    hq, hkv, d, bs = 28, 4, 128, 16
+    sizes = [256, 512, 1024, 2048, 4096, 8192, 16384]
+    rng = np.random.default_rng([a.seed, 8])
+    steps, total = [], 0
+    while total < sizes[-1]:                      # the largest batch; each smaller one is a prefix of it
+        parent = int(rng.integers(64, 257))
+        for _ in range(4):
+            if total == sizes[-1]:
+                break
+            edge = min(x for x in sizes if x > total)       # a step ends on every batch size
+            n = min(int(rng.integers(32, 257)), edge - total)
+            steps.append((len(steps) // 4, parent, n))
+            total += n
+    prompt = 1024
+    nb = -(-prompt // bs) + sum(-(-p // bs) for p in {g: p for g, p, _ in steps}.values()) + \
+        sum(-(-n // bs) for _, _, n in steps)
+    bm = tkv.BlockManager(nb, bs, len(steps) + 64)
+    root = bm.extend(-1, rng.integers(0, 1000, size=prompt).tolist(), True)[0]
+    parents, seqs = {}, []
+    for g, p, n in steps:
+        if g not in parents:
+            parents[g] = bm.extend(root, rng.integers(0, 1000, size=p).tolist(), True)[0]
+        seqs.append(bm.extend(parents[g], rng.integers(0, 1000, size=n).tolist(), True)[0])
+    bl = bm.block_len()
+    kbits = W.f32_to_bf16_bits(rng.standard_normal((nb, hkv, bs, d), dtype=np.float32))
+    vbits = W.f32_to_bf16_bits(rng.standard_normal((nb, hkv, bs, d), dtype=np.float32))
+
+    def to_dev(x):
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    k0, v0 = to_dev(kbits), to_dev(vbits)
+    n_copies = a.kv_copies or max(2, math.ceil(4 * MALL_BYTES / (4 * k0.numel())) + 1)
+    ks = [k0] + [k0.clone() for _ in range(n_copies - 1)]
+    vs = [v0] + [v0.clone() for _ in range(n_copies - 1)]
+    stream = torch.cuda.current_stream()
+    sweep, at_threshold = [], None
+    for T in sizes:
+        rows, acc = [], 0
+        for i, (_, _, n) in enumerate(steps):
+            if acc == T:
+                break
+            rows.append((seqs[i], n))
+            acc += n
+        assert acc == T
+        tables = [bm.table(x) for x, _ in rows]
+        q_lens = [n for _, n in rows]
+        qi = np.concatenate([[0], np.cumsum(q_lens)]).astype(np.int32)
+        ki = np.concatenate([[0], np.cumsum([len(t) for t in tables])]).astype(np.int32)
+        plan = tkv.Plan((hq, hkv, d, bs, nb), qi, ki, np.concatenate(tables).astype(np.int32), bl, None, device=dev)
+        st = plan.stats
+        n_qtok = int(qi[-1])
+        q = to_dev(W.f32_to_bf16_bits(rng.standard_normal((n_qtok, hq, d), dtype=np.float32)))
+        o = torch.empty((n_qtok, hq, d), dtype=torch.bfloat16, device=dev)
+        lse = torch.empty((n_qtok, hq), dtype=torch.float32, device=dev)
+        reps = max(20, a.steps // 4)
+        for i in range(a.warmup):
+            plan.verify(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for i in range(reps):
+            plan.verify(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / reps
+        tkv.tkv_plan_profile(plan.h, reps)
+        for i in range(reps):
+            plan.verify(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
+        torch.cuda.synchronize()
+        n_rec, ms_main, ms_merge = tkv.tkv_plan_profile_read(plan.h)
+        tkv.tkv_plan_profile(plan.h, 0)
+        t_main = ms_main / max(1, n_rec) / 1e3
+        b_uniq = st["uniq_kv_tokens"] * hkv * d * 2 * 2
+        entry = {"tokens": n_qtok, "rows": len(rows), "us": round(ms * 1e3, 2), "tokens_per_s": round(n_qtok / (ms / 1e3), 1),
+                 "attn_fwd_us": round(t_main * 1e6, 2), "tflops": round(st["flops"] / t_main / 1e12, 1),
+                 "flops": st["flops"], "unique_kv_bytes": b_uniq}
+        sweep.append(entry)
+        if T == 2048:
+            at_threshold = (entry, st, tables, q_lens, q, plan)
+    best = max(e["tokens_per_s"] for e in sweep)
+    saturation = next(e["tokens"] for e in sweep if e["tokens_per_s"] >= 0.9 * best)
+    e, st, tables, q_lens, q, _ = at_threshold
+    t_main = e["attn_fwd_us"] / 1e6
+    mfma_bound = e["flops"] / e["unique_kv_bytes"] > MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if mfma_bound:
+        ach = e["flops"] / t_main / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": "attn_fwd",
+                "algorithmic_flops": e["flops"], "kernel_us": e["attn_fwd_us"]}
+    else:
+        ach = e["unique_kv_bytes"] / t_main / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "attn_fwd",
+                "algorithmic_bytes": e["unique_kv_bytes"], "kernel_us": e["attn_fwd_us"]}
+    cpu = None
+    if not a.no_cpu:
+        import oracle
+        kf, vf = W.bf16_bits_to_f32(kbits), W.bf16_bits_to_f32(vbits)
+        qf = W.bf16_bits_to_f32(q.view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+        done_tok, t_cpu, r = 0, 0.0, 0
+        while t_cpu < a.cpu_seconds and r < len(tables):
+            t0 = time.perf_counter()
+            oracle.attention(qf, kf, vf, tables, bl, q_lens, rows=[r])
+            t_cpu += time.perf_counter() - t0
+            done_tok += q_lens[r]
+            r += 1
+        cpu = {"value": round(done_tok / t_cpu, 2), "unit": "tokens/s", "cores": len(os.sched_getaffinity(0)),
+               "kind": "oracle", "sample": f"the first {r} of {len(tables)} rows of the 2,048-token batch "
+                                           f"({done_tok} query tokens), fp64 NumPy gather attention, {t_cpu:.1f} s"}
+    out = {
+        "metric": "verify tokens/s against batch tokens, attention layer (shape of the verify-throughput microbenchmark)",
+        "value": e["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": max(20, a.steps // 4),
+        "warmup": a.warmup, "ms_per_step": round(e["us"] / 1e3, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (sibling groups of candidate steps, N(0,1) bf16)",
+        "config": {"workload": "verify_sweep", "hq": hq, "hkv": hkv, "head_dim": d, "batch_tokens": 2048,
+                   "prompt": prompt, "kv_pool_copies_rotated": n_copies},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "sweep": sweep,
+        "saturation_tokens": saturation,
+    }
+    print(json.dumps(out))
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -257,6 +391,8 @@ def main():
         return bench_kv_append(a)
     if a.workload == "cd_sample":
         return bench_cd_sample(a)
+    if a.workload == "verify_sweep":
+        return bench_verify_sweep(a)
     dev = torch.device("cuda:0")
     wl = W.CONFIGS[a.workload](a.seed)
     s = wl.shape

@@ -275,6 +275,94 @@ int tkv_cd_sample(int32_t n_rows, int32_t vocab, float temperature, int32_t max_
                   const float* d_uniform, const int32_t* d_draw_off, int32_t* d_token, int32_t* d_count,
                   int32_t* d_n_groups, void* hip_stream);
 
+/* ======================================================================== search controller
+ * Early pruning (Sec. 4.1) and lazy verification (Sec. 4.3) of a speculative beam search whose
+ * rounds keep the top k candidates by verifier score (k = beam size / beam width, Sec. 2.2).
+ * Candidates (nodes) are numbered in creation order; the caller maps them to block-manager
+ * sequences, verifies flushed batches (tkv_verify) and releases pruned ones (tkv_prune).
+ *   - Rounds.  Round d's members are the children of round d-1's selected candidates (the roots for
+ *     d = 0).  A candidate expands once it has a score, possibly before its round is decided
+ *     (speculation); until then its children are speculative, and their sibling group is all that
+ *     is sure to share their round.
+ *   - Rule 1 (rank).  A scored candidate is pruned once at least k unpruned, scored candidates that
+ *     surely share its round have strictly higher scores.
+ *   - Rule 2 (perfect score 1.0).  Once k candidates that surely share a round are perfect, the first
+ *     k of them in score arrival order are kept and every other such candidate is pruned; for the
+ *     round's members this decides the round with those k selected.
+ *   - A round is otherwise decided when every selected parent has expanded and every unpruned member
+ *     has a score: the top k by (score descending, arrival ascending) are selected.  Deciding a round
+ *     prunes its other candidates.  Pruning a candidate prunes its subtree and drops it from the
+ *     queue.
+ *   - Lazy verification.  A completed step is queued.  Flush is advised while the queue is not empty
+ *     and: the queued tokens exceed token_threshold (policy 1), or the sibling group of a queued
+ *     candidate has no candidate still generating (policy 2), or a queued candidate has been deferred
+ *     max_deferrals times (policy 3).  A deferral is a tick that passes without a flush advice.
+ * Host-only; not thread-safe. */
+typedef struct tkv_search tkv_search;
+
+enum {
+    TKV_CAND_GENERATING = 0, /* decoding its step */
+    TKV_CAND_QUEUED = 1,     /* step complete, waiting in the verification queue */
+    TKV_CAND_VERIFYING = 2,  /* flushed in a batch, score not yet reported */
+    TKV_CAND_VERIFIED = 3,   /* scored; its round is undecided */
+    TKV_CAND_SELECTED = 4,   /* kept by its decided round */
+    TKV_CAND_PRUNED = 5      /* pruned (or not selected): its sequence can be released */
+};
+
+/* k >= 1 candidates kept per round; max_nodes >= 1 candidates in all; token_threshold >= 0 (the paper
+ * profiles 2,048); max_deferrals >= 0 (the paper uses 6).  EINVAL, ENOMEM. */
+int tkv_search_create(int32_t k, int32_t max_nodes, int32_t token_threshold, int32_t max_deferrals,
+                      tkv_search** out);
+void tkv_search_destroy(tkv_search* s);
+
+/* Create n >= 0 children of `parent` with consecutive ids from *first_out; parent = -1 creates the
+ * roots (once).  The parent must have a score and not be expanded yet; n = 0 marks a candidate that
+ * does not continue (it counts as expanded).  Expanding can decide a round (the caller then drains
+ * tkv_search_pruned).  EINVAL (no score yet, already expanded, roots exist, n < 0), ENOSEQ (parent
+ * pruned), ENOMEM (more than max_nodes candidates); on error nothing changes. */
+int tkv_search_expand(tkv_search* s, int32_t parent, int32_t n, int32_t* first_out);
+
+/* A generating candidate completed its step of n_tokens >= 1 tokens: it is queued for verification.
+ * *flush_out = 1 when a lazy-verification policy advises a flush now.  EINVAL (not generating),
+ * ENOSEQ (pruned). */
+int tkv_search_complete(tkv_search* s, int32_t node, int32_t n_tokens, int32_t* flush_out);
+
+/* One generator iteration: *flush_out = 1 if a policy advises a flush; otherwise every queued
+ * candidate's deferral count grows by one.  EINVAL. */
+int tkv_search_tick(tkv_search* s, int32_t* flush_out);
+
+/* Take the whole queue as one verification batch: nodes_out[0..*n_out) in enqueue order.  ECAP
+ * (cap < queue length, *n_out = that length, nothing changes), EINVAL. */
+int tkv_search_flush(tkv_search* s, int32_t* nodes_out, int32_t cap, int32_t* n_out);
+
+/* Verifier scores in [0, 1] of flushed candidates, applied one at a time in the given order (which
+ * is their arrival order), each followed by the pruning rules and round decisions.  A candidate
+ * pruned while its batch was verified takes no score.  EINVAL (a node not flushed, already scored
+ * or repeated; a score outside [0, 1] or NaN); on error nothing changes. */
+int tkv_search_score(tkv_search* s, int32_t n, const int32_t* nodes, const float* scores);
+
+/* Candidates pruned since the last call, ascending: nodes_out[0..*n_out).  ECAP (cap < count,
+ * *n_out = count, nothing is taken), EINVAL. */
+int tkv_search_pruned(tkv_search* s, int32_t* nodes_out, int32_t cap, int32_t* n_out);
+
+/* One candidate: state (TKV_CAND_*), parent (-1 for a root), depth, score (-1 if none).  EINVAL. */
+int tkv_search_node(const tkv_search* s, int32_t node, int32_t* state_out, int32_t* parent_out,
+                    int32_t* depth_out, float* score_out);
+
+/* Round `depth`: *decided_out = 1 once decided, with its selected candidates ascending in
+ * selected_out[0..*n_out) (0 while undecided).  ECAP, EINVAL. */
+int tkv_search_round(const tkv_search* s, int32_t depth, int32_t* selected_out, int32_t cap, int32_t* n_out,
+                     int32_t* decided_out);
+
+/* Whole state as int32 words, for bit-exact comparison in tests:
+ *   k, token_threshold, max_deferrals, n_roots (-1: none yet), queued tokens, n_nodes,
+ *   per node: parent, depth, state, n_children (-1: not expanded), tokens, deferrals, arrival (-1:
+ *   no score), score bits (0 when none),
+ *   queue length, queue[], n_rounds (1 + the deepest decided round), per round: decided,
+ *   n_selected, selected[].
+ * *used = bytes needed; ECAP if cap < *used (buf may be NULL to query the size). */
+int tkv_search_snapshot(const tkv_search* s, void* buf, size_t cap, size_t* used);
+
 /* Instrumentation.  tkv_plan_profile(plan, max_calls) makes the next max_calls attention calls on
  * this plan record HIP events taken from the kernel dispatches' own start and end timestamps: the
  * main attention phase (start of its first kernel to end of its last) and the merge kernel

@@ -10,6 +10,7 @@ Contents
   coalesce       computation-deduplication row coalescing (identical candidates submitted once)
   kv_append      new tokens' K/V rows written to their pool slots (deduplicated blocks skipped)
   cd_sample      computation-deduplication branching: potential-many draws from one row, grouped
+  search         speculative beam-search controller: early pruning and lazy verification
 
 Pins: every function here is checked in tests/test_oracle.py against values that do not come from
 this package (brute force in pure Python, closed forms, invariants, hand-worked fixtures under
@@ -19,6 +20,7 @@ from .attention import attention, gather_kv
 from .block_manager import BlockManager, BMError
 from .coalesce import coalesce
 from . import cd_sample
+from . import search
 from .kv_append import kv_append
 
-__all__ = ["attention", "gather_kv", "BlockManager", "BMError", "coalesce", "kv_append", "cd_sample"]
+__all__ = ["attention", "gather_kv", "BlockManager", "BMError", "coalesce", "kv_append", "cd_sample", "search"]

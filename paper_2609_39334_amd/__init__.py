@@ -74,6 +74,17 @@ _SIG = {
     "tkv_verify": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_kv_append": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _P, _I32, _P, _P, _P, _P, _P]),
     "tkv_cd_sample": (ctypes.c_int, [_I32, _I32, ctypes.c_float, _I32, _P, _P, _P, _P, _P, _P, _P]),
+    "tkv_search_create": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.POINTER(_P)]),
+    "tkv_search_destroy": (None, [_P]),
+    "tkv_search_expand": (ctypes.c_int, [_P, _I32, _I32, _PI32]),
+    "tkv_search_complete": (ctypes.c_int, [_P, _I32, _I32, _PI32]),
+    "tkv_search_tick": (ctypes.c_int, [_P, _PI32]),
+    "tkv_search_flush": (ctypes.c_int, [_P, _PI32, _I32, _PI32]),
+    "tkv_search_score": (ctypes.c_int, [_P, _I32, _PI32, ctypes.POINTER(ctypes.c_float)]),
+    "tkv_search_pruned": (ctypes.c_int, [_P, _PI32, _I32, _PI32]),
+    "tkv_search_node": (ctypes.c_int, [_P, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_float)]),
+    "tkv_search_round": (ctypes.c_int, [_P, _I32, _PI32, _I32, _PI32, _PI32]),
+    "tkv_search_snapshot": (ctypes.c_int, [_P, _P, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
     "tkv_plan_profile": (ctypes.c_int, [_P, _I32]),
     "tkv_plan_profile_read": (ctypes.c_int, [_P, _PI32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
 }
@@ -364,6 +375,105 @@ def tkv_plan_profile_read(plan: int):
     return n.value, a.value, b.value
 
 
+CAND_GENERATING, CAND_QUEUED, CAND_VERIFYING, CAND_VERIFIED, CAND_SELECTED, CAND_PRUNED = range(6)
+
+
+def tkv_search_create(k: int, max_nodes: int, token_threshold: int, max_deferrals: int) -> int:
+    h = _P()
+    _check(lib().tkv_search_create(k, max_nodes, token_threshold, max_deferrals, ctypes.byref(h)))
+    return h.value
+
+
+def tkv_search_destroy(s: int) -> None:
+    lib().tkv_search_destroy(s)
+
+
+def tkv_search_expand(s: int, parent: int, n: int) -> int:
+    first = _I32()
+    _check(lib().tkv_search_expand(s, parent, n, ctypes.byref(first)))
+    return first.value
+
+
+def tkv_search_complete(s: int, node: int, n_tokens: int) -> bool:
+    f = _I32()
+    _check(lib().tkv_search_complete(s, node, n_tokens, ctypes.byref(f)))
+    return bool(f.value)
+
+
+def tkv_search_tick(s: int) -> bool:
+    f = _I32()
+    _check(lib().tkv_search_tick(s, ctypes.byref(f)))
+    return bool(f.value)
+
+
+def _take(fn, s: int) -> list:
+    n = _I32()
+    rc = fn(s, None, 0, ctypes.byref(n))
+    if rc not in (TKV_OK, TKV_ECAP):
+        _check(rc)
+    out = np.zeros(max(1, n.value), dtype=np.int32)
+    _check(fn(s, _ptr(out), len(out), ctypes.byref(n)))
+    return [int(x) for x in out[:n.value]]
+
+
+def tkv_search_flush(s: int) -> list:
+    return _take(lib().tkv_search_flush, s)
+
+
+def tkv_search_score(s: int, nodes, scores) -> None:
+    nd = _i32(nodes)
+    sc = np.ascontiguousarray(np.asarray(scores, dtype=np.float32).reshape(-1))
+    if len(sc) != len(nd):
+        raise ValueError("one score per node")
+    _check(lib().tkv_search_score(s, len(nd), _ptr(nd), sc.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+
+
+def tkv_search_pruned(s: int) -> list:
+    return _take(lib().tkv_search_pruned, s)
+
+
+def tkv_search_node(s: int, node: int):
+    """Returns (state, parent, depth, score or None)."""
+    st, pa, de, sc = _I32(), _I32(), _I32(), ctypes.c_float()
+    _check(lib().tkv_search_node(s, node, ctypes.byref(st), ctypes.byref(pa), ctypes.byref(de), ctypes.byref(sc)))
+    return st.value, pa.value, de.value, (None if sc.value < 0 else sc.value)
+
+
+def tkv_search_round(s: int, depth: int):
+    """Returns (decided, selected ids ascending)."""
+    n, dec = _I32(), _I32()
+    rc = lib().tkv_search_round(s, depth, None, 0, ctypes.byref(n), ctypes.byref(dec))
+    if rc not in (TKV_OK, TKV_ECAP):
+        _check(rc)
+    out = np.zeros(max(1, n.value), dtype=np.int32)
+    _check(lib().tkv_search_round(s, depth, _ptr(out), len(out), ctypes.byref(n), ctypes.byref(dec)))
+    return bool(dec.value), [int(x) for x in out[:n.value]]
+
+
+def tkv_search_snapshot(s: int) -> dict:
+    """Parsed state: nodes as (parent, depth, state, n_children, tokens, deferrals, arrival, score bits)."""
+    used = ctypes.c_size_t()
+    lib().tkv_search_snapshot(s, None, 0, ctypes.byref(used))
+    buf = np.zeros(used.value // 4, dtype=np.int32)
+    _check(lib().tkv_search_snapshot(s, buf.ctypes.data_as(_P), used.value, ctypes.byref(used)))
+    w = [int(x) for x in buf]
+    k, thr, md, n_roots, qtok, n = w[:6]
+    i = 6
+    nodes = [tuple(w[i + 8 * j:i + 8 * j + 8]) for j in range(n)]
+    i += 8 * n
+    nq = w[i]
+    queue = w[i + 1:i + 1 + nq]
+    i += 1 + nq
+    rounds = []
+    for _ in range(w[i]):
+        i += 1
+        dec, ns = w[i], w[i + 1]
+        rounds.append((dec, tuple(w[i + 2:i + 2 + ns])))
+        i += 1 + ns
+    return {"k": k, "token_threshold": thr, "max_deferrals": md, "n_roots": n_roots, "queued_tokens": qtok,
+            "nodes": nodes, "queue": queue, "rounds": rounds}
+
+
 # ------------------------------------------------------------------------- owning wrappers
 
 class BlockManager:
@@ -435,3 +545,43 @@ class Plan:
 
     def verify(self, q, k, v, o, lse=None, stream=None):
         tkv_verify(self.h, q, k, v, o, lse, stream)
+
+
+class Search:
+    """Owns a tkv_search handle (speculative beam-search controller); methods forward to the C
+    entry points."""
+
+    def __init__(self, k: int, max_nodes: int = 4096, token_threshold: int = 2048, max_deferrals: int = 6):
+        self.h = tkv_search_create(k, max_nodes, token_threshold, max_deferrals)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            tkv_search_destroy(self.h)
+            self.h = None
+
+    def expand(self, parent, n):
+        return tkv_search_expand(self.h, parent, n)
+
+    def complete(self, node, n_tokens):
+        return tkv_search_complete(self.h, node, n_tokens)
+
+    def tick(self):
+        return tkv_search_tick(self.h)
+
+    def flush(self):
+        return tkv_search_flush(self.h)
+
+    def score(self, nodes, scores):
+        tkv_search_score(self.h, nodes, scores)
+
+    def pruned(self):
+        return tkv_search_pruned(self.h)
+
+    def node(self, node):
+        return tkv_search_node(self.h, node)
+
+    def round(self, depth):
+        return tkv_search_round(self.h, depth)
+
+    def snapshot(self):
+        return tkv_search_snapshot(self.h)

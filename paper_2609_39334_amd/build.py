@@ -17,7 +17,7 @@ LIB = os.path.join(HERE, "libtreekv.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
-HOST_SOURCES = ["capi.cpp", "bm.cpp", "plan.cpp"]
+HOST_SOURCES = ["capi.cpp", "bm.cpp", "plan.cpp", "search.cpp"]
 HIP_SOURCES = ["attn.hip", "kv_append.hip", "cd_sample.hip"]
 
 HOST_FLAGS = ["-std=c++17", "-O2", "-fPIC", "-fvisibility=hidden", "-Wall", "-Wextra", "-Wno-unused-parameter"]
