@@ -11,7 +11,10 @@
  *   - a prefix-tree KV block manager with refcounted, deduplicated step blocks (host, integer);
  *   - row coalescing of identical candidates (host, integer);
  *   - a planner that turns per-row block tables into shared segments and a device work list;
- *   - decode (q_len 1) and verify (q_len >= 1, causal within the step) attention on the GPU.
+ *   - decode (q_len 1) and verify (q_len >= 1, causal within the step) attention on the GPU;
+ *   - the decode loop's other device steps: K/V append that skips deduplicated blocks, and the
+ *     branching sampler of computation deduplication (GPU);
+ *   - the controller of early pruning and lazy verification (host).
  *
  * Conventions
  *   - Every function returns TKV_OK (0) or a negative TKV_E* code; nothing throws or aborts across
