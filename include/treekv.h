@@ -24,7 +24,7 @@
  *   - Device work is enqueued on the caller's hipStream_t (passed as void*, NULL = default
  *     stream) and is asynchronous; the caller keeps buffers alive until the stream reaches it.
  *   - bf16 is IEEE bfloat16 bit patterns (uint16); fp32 is IEEE binary32.
- *   - Handles (tkv_bm, tkv_plan) are not thread-safe; use one thread per handle.
+ *   - Handles (tkv_bm, tkv_plan, tkv_search) are not thread-safe; use one thread per handle.
  */
 #ifndef TREEKV_H
 #define TREEKV_H
