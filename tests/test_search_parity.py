@@ -100,3 +100,38 @@ def test_library_search_matches_the_oracle_run(n, m, depth, seed, p):
     assert path_c == path_o and ctl.snapshot() == ref.snapshot()
     if p == 0.0:
         assert [sorted(path_c[c] for c in ctl.round(d)[1]) for d in range(depth)] == beam_search(n, m, depth, seed)
+
+
+def test_search_abi_edges():
+    import ctypes
+    L = tkv.lib()
+    I32 = ctypes.c_int32
+    assert L.tkv_search_create(1, 8, 0, 6, None) == tkv.TKV_EINVAL
+    h = ctypes.c_void_p()
+    for bad in ((0, 8, 0, 6), (1, 0, 0, 6), (1, 8, -1, 6), (1, 8, 0, -1)):
+        assert L.tkv_search_create(*bad, ctypes.byref(h)) == tkv.TKV_EINVAL and h.value is None
+    s = tkv.Search(1, 8, 10 ** 6, 6)
+    first = I32()
+    assert L.tkv_search_expand(s.h, -1, 3, None) == tkv.TKV_EINVAL
+    assert L.tkv_search_expand(s.h, -1, -1, ctypes.byref(first)) == tkv.TKV_EINVAL
+    assert L.tkv_search_expand(s.h, -1, 9, ctypes.byref(first)) == tkv.TKV_ENOMEM   # more than max_nodes
+    assert s.expand(-1, 3) == 0
+    s.complete(0, 5)
+    s.complete(1, 7)
+    n = I32()
+    out = (I32 * 1)()
+    assert L.tkv_search_flush(s.h, out, 1, ctypes.byref(n)) == tkv.TKV_ECAP and n.value == 2
+    assert s.snapshot()["queue"] == [0, 1]                                          # nothing taken
+    assert s.flush() == [0, 1]
+    s.score([0, 1], [0.5, 0.25])
+    assert L.tkv_search_pruned(s.h, out, 0, ctypes.byref(n)) == tkv.TKV_ECAP and n.value == 1
+    assert s.pruned() == [1] and s.pruned() == []
+    dec = I32()
+    assert L.tkv_search_round(s.h, -1, out, 1, ctypes.byref(n), ctypes.byref(dec)) == tkv.TKV_EINVAL
+    assert s.round(7) == (False, [])
+    used = ctypes.c_size_t()
+    assert L.tkv_search_snapshot(s.h, None, 0, ctypes.byref(used)) == tkv.TKV_ECAP and used.value > 0
+    st, pa, de, sc = I32(), I32(), I32(), ctypes.c_float()
+    assert L.tkv_search_node(s.h, 3, ctypes.byref(st), ctypes.byref(pa), ctypes.byref(de), ctypes.byref(sc)) \
+        == tkv.TKV_EINVAL
+    assert s.node(0) == (tkv.CAND_VERIFIED, -1, 0, 0.5) and s.node(2)[0] == tkv.CAND_GENERATING
