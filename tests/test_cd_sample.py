@@ -157,3 +157,32 @@ def test_cd_branch_step_end_to_end():
         for k, t in zip(kc, toks):
             assert list(bm_c.table(k)) == bm_o.table(k) and bm_o.table(k)[:-1] == bm_o.table(s)
     assert bm_c.snapshot()["seqs"] == bm_o.snapshot()["seqs"]
+
+
+@pytest.mark.parametrize("vocab", [4096 * 512, 4096 * 512 - 1])
+def test_cd_sample_largest_vocabulary(vocab):
+    # 512 tiles of 4,096 logits, the most a row may have; the odd size takes the unaligned path
+    rng = np.random.default_rng(vocab % 1000)
+    logits = (rng.standard_normal((3, vocab)) * 2.0).astype(np.float32)
+    logits[1, rng.random(vocab) < 0.5] = -np.inf
+    potential = np.array([1, 1024, 8])
+    off, u, tok, cnt, ng = _run(logits, 0.8, potential, vocab)
+    n_amb = _check_rows(logits, 0.8, potential, off, u, tok, cnt, ng)
+    print(f"    vocab {vocab}: {int(off[-1])} draws, {n_amb} within {_delta(vocab):.1e} of a boundary", flush=True)
+
+
+def test_cd_sample_rejects_bad_arguments():
+    import paper_2609_39334_amd as tkv
+    off = torch.tensor([0, 1], dtype=torch.int32, device="cuda")
+    u = torch.full((1,), 0.5, dtype=torch.float32, device="cuda")
+    too_wide = torch.zeros((1, 4096 * 512 + 1), dtype=torch.float32, device="cuda")
+    with pytest.raises(tkv.TkvError) as e:
+        tkv.tkv_cd_sample(too_wide, 0.8, off, u, 1)
+    assert e.value.code == tkv.TKV_EINVAL
+    ok = torch.zeros((1, 10), dtype=torch.float32, device="cuda")
+    for temp, mp in ((0.0, 1), (float("inf"), 1), (float("nan"), 1), (0.8, 1025), (0.8, -1)):
+        with pytest.raises(tkv.TkvError):
+            tkv.tkv_cd_sample(ok, temp, off, u, mp)
+    empty = torch.zeros((0, 10), dtype=torch.float32, device="cuda")
+    tok, cnt, ng = tkv.tkv_cd_sample(empty, 0.8, torch.zeros(1, dtype=torch.int32, device="cuda"), u, 0)
+    assert ng.numel() == 0
