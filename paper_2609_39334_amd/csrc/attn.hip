@@ -639,8 +639,8 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
     // block descriptors of a stage: lane l holds block 4s + (l & 3) (the item's last block past its end)
     auto stage_desc = [&](int st) { return bd[min(4 * st + (lane & 3), nb - 1)]; };
     int2 dcur = stage_desc(0), dnxt = stage_desc(1);
-    const int wblk = wave * 16 * RB;  // this wave's block within a stage buffer
-    {
+    const int wblk = wave * 16 * RB;  // this wave's block within a stage buffer (waves 0-3 fetch)
+    if (wave < 4) {
         const int len = wave < nb ? __builtin_amdgcn_readlane(dcur.y, wave) : 0;
         stage_fetch<D>(kpool, vpool, static_cast<size_t>(__builtin_amdgcn_readlane(dcur.x, wave)) * blk_stride + kvh_off,
                        len, lane, k0 + wblk, v0 + wblk);
@@ -651,7 +651,7 @@ __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::To
     auto stage = [&](int st, const uint8_t* ks, const uint8_t* vs, uint8_t* kn, uint8_t* vn) {
         stage_barrier();
         // fetch the next stage while this one is contracted
-        if (st + 1 < n_stages) {
+        if (st + 1 < n_stages && wave < 4) {
             const int bn = 4 * (st + 1) + wave;
             const int len = bn < nb ? __builtin_amdgcn_readlane(dnxt.y, wave) : 0;
             stage_fetch<D>(kpool, vpool,
@@ -816,6 +816,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                    plse, hq, hkv, G, sl2, vs);
 }
 
+// Few tile items and no wave-grid work (a small verification batch): the chip has a CU for every
+// tile, and a tile's walk over its keys sets the call's time.  Eight waves of one 16-row column tile
+// each share a 128-row tile (instead of four waves of two), so each wave does half the MFMA and
+// softmax work per stage and the walk is shorter.  Waves 0-3 fetch the stages.
+template <int D>
+__global__ __launch_bounds__(2 * kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_tile8(
+    const tkv::ItemDesc* __restrict__ items, int n_tile, const tkv::TokDesc* __restrict__ toks,
+    const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
+    float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[tile_buf_bytes<D>()];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[tile_buf_bytes<D>()];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[tile_buf_bytes<D>()];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[tile_buf_bytes<D>()];
+    const int b = blockIdx.x;
+    if (b >= n_tile) return;
+    const tkv::ItemDesc it = items[b];
+    tile_item<D, 1>(it, toks, blks, q, kpool, vpool, o, lse, po, plse, hq, hkv, G, sl2, lds_k0, lds_v0, lds_k1, lds_v1);
+}
+
 // Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
 // are contiguous, sized to one thread per float4 column of the token's heads): every thread folds
 // the partials of its column in with an online softmax, eight partials' outputs and lse values in
@@ -916,7 +936,13 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     // interleaved when the grid exceeds the workgroup slots of the chip (two per CU)
     const int grid = (n_tile + 7) / 8 * 8 + (n_wave_wg + 7) / 8 * 8;
     const int runs = n_tile + n_wave_wg > kWaveWorkers / kWaveWG ? std::min((n_tile + 7) / 8, (n_wave_wg + 7) / 8) : 0;
-    if (grid > 0)
+    if (p->tile8 && n_wave_wg == 0 && n_tile > 0)
+        hipExtLaunchKernelGGL(attn_tile8<D>, dim3(static_cast<unsigned>(n_tile)), dim3(2 * kThreads), 0, st,
+                              ev ? ev[0] : nullptr, ev ? ev[1] : nullptr, 0, items, n_tile, toks, blks,
+                              static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                              static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, po, plse, hq, hkv,
+                              p->group, sl2);
+    else if (grid > 0)
         hipExtLaunchKernelGGL(attn_fwd<D>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, st,
                               ev ? ev[0] : nullptr, ev ? ev[1] : nullptr, 0, items, n_tile, n_wave_wg, runs, toks, blks,
                               wdesc, woff, wtiles, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),

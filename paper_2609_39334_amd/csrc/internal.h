@@ -32,6 +32,7 @@ constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
 constexpr int kWaveToks = 48;   // token slots of a wave-kernel record (>= 16 kWaveMaxTiles / G)
 constexpr int kWaveWorkers = 2048;  // waves of the wave kernel: 2 workgroups of kWaveWG on each of 256 CUs
 constexpr int kWaveWG = 4;      // waves per workgroup of the wave kernel (independent; no barriers)
+constexpr int kTile8MaxItems = 256;  // tile items (and no wave grid) up to which 8-wave workgroups run them: one per CU
 
 // One work item: a tile of query tokens (each with all G query heads of one KV
 // head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the
@@ -97,6 +98,7 @@ struct tkv_plan {
     std::vector<int32_t> wave_off;            // [n_waves + 1] wave w's further items: [off[w], off[w+1])
     std::vector<int32_t> wave_tiles;          // [n_waves] column tiles of the wave's items (0: no work)
     int32_t n_slots = 0;
+    bool tile8 = false;  // tile items only, few enough to run as 8-wave workgroups (kTile8MaxItems)
     // workspace layout (byte offsets)
     size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wdesc = 0, off_woff = 0, off_wtiles = 0;
     size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;

@@ -492,6 +492,11 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         }
         st.n_items_wave = static_cast<int32_t>(p->wave_items.size());
         st.n_waves = static_cast<int32_t>(p->wave_tiles.size());
+        // a plan of a few tile items and nothing else gives each tile a CU to itself: its 128 rows then
+        // run as eight 16-row waves, which shortens the tile's walk
+        int64_t tile8_max = tkv::kTile8MaxItems;
+        if (const char* env = std::getenv("TKV_TILE8_MAX_ITEMS")) tile8_max = std::atoll(env);
+        p->tile8 = p->wave_items.empty() && !p->items.empty() && static_cast<int64_t>(p->items.size()) <= tile8_max;
         st.n_slots = p->n_slots;
         st.n_merge = static_cast<int32_t>(p->merges.size());
 

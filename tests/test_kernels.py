@@ -212,3 +212,34 @@ def test_consecutive_calls_new_queries(seed, hq, hkv, d, tile_rows, monkeypatch)
         lerr = np.abs(lse.cpu().numpy() - l_ref)
         _log(f"    call {call}: max {err.max():.2e} mean {err.mean():.2e} lse max {lerr.max():.2e}")
         assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS and lerr.max() <= LSE_ABS
+
+
+def _small_verify(seed, shape, n_ctx=2, n_cands=5):
+    """Verify-only batch: contexts U{40..600} (sealed), candidate steps long enough that every row's
+    query tile reaches 64 rows (q_len * G >= 64), so the plan holds tile items only."""
+    rs = np.random.default_rng([seed, 1])
+    rt = np.random.default_rng([seed, 2])
+    g = shape.hq // shape.hkv
+    wl = W.Workload(f"small_verify_{seed}", shape, seed, note="verify-only batch")
+    cands, ctxs = [], []
+    for _ in range(n_ctx):
+        c = wl.extend(-1, rt.integers(0, 32000, int(rs.integers(40, 601))), True)
+        ctxs.append(c)
+        for _ in range(n_cands):
+            n = int(rs.integers(-(-64 // g), 201))
+            cands.append((wl.extend(c, rt.integers(0, 32000, n), True), n))
+    for c in ctxs:
+        wl.prune(c)
+    wl.launch("verify", cands)
+    return wl.finalize()
+
+
+@pytest.mark.parametrize("seed,hq,hkv,d", [(40, 28, 4, 128), (41, 8, 2, 64), (42, 16, 2, 128), (43, 4, 4, 64)])
+@pytest.mark.parametrize("tile8_max", ["0", "100000"])
+def test_small_verify_batches_on_both_tile_kernels(seed, hq, hkv, d, tile8_max, monkeypatch):
+    # a verify-only batch makes tile items alone; a few of them run as 8-wave workgroups (one 16-row
+    # column tile per wave), more of them on the 4-wave kernel -- the override forces either
+    monkeypatch.setenv("TKV_TILE8_MAX_ITEMS", tile8_max)
+    wl = _small_verify(seed, W.Shape(hq, hkv, d))
+    b, st = compare(wl, 0, repeat=2)
+    assert st["n_items_wave"] == 0 and st["n_items_row"] > 0 and st["n_items"] == st["n_items_row"]
