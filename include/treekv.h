@@ -267,16 +267,19 @@ int tkv_kv_append(const tkv_shape* shape, const int32_t* d_dst, int32_t n_tok, c
  *   d_logits    [n_rows][vocab] fp32 (finite or -inf, no NaN), device
  *   d_draw_off  [n_rows + 1] int32, device: row r draws potential_r = off[r + 1] - off[r] tokens,
  *               0 <= potential_r <= max_potential <= 1024
- *   d_uniform   [off[n_rows]] fp32 in [0, 1), device (the caller's random numbers)
- *   d_token, d_count  [off[n_rows]] int32, device: row r's groups at [off[r], off[r] + d_n_groups[r]),
+ *   d_uniform   [n_draws] fp32 in [0, 1), device (the caller's random numbers; off[n_rows] used)
+ *   n_draws     entries of d_uniform, d_token and d_count.  The offsets are device data, so the
+ *               kernel checks them: a row whose range [off[r], off[r + 1]) is not inside [0, n_draws)
+ *               reads and writes nothing and gets d_n_groups[r] = -1.
+ *   d_token, d_count  [n_draws] int32, device: row r's groups at [off[r], off[r] + d_n_groups[r]),
  *               tokens ascending, counts summing to potential_r
- *   d_n_groups  [n_rows] int32, device: distinct tokens of the row (-1: no finite logit, or a
- *               potential above 1024)
+ *   d_n_groups  [n_rows] int32, device: distinct tokens of the row (-1: no finite logit, a
+ *               potential above 1024, or offsets outside the arrays)
  * Enqueued on hip_stream.  EINVAL (n_rows < 0, vocab < 1, temperature not positive and finite,
- * max_potential outside [0, 1024], NULL pointers), EHIP. */
+ * max_potential outside [0, 1024], n_draws < 0, NULL pointers), EHIP. */
 int tkv_cd_sample(int32_t n_rows, int32_t vocab, float temperature, int32_t max_potential, const float* d_logits,
-                  const float* d_uniform, const int32_t* d_draw_off, int32_t* d_token, int32_t* d_count,
-                  int32_t* d_n_groups, void* hip_stream);
+                  const float* d_uniform, const int32_t* d_draw_off, int32_t n_draws, int32_t* d_token,
+                  int32_t* d_count, int32_t* d_n_groups, void* hip_stream);
 
 /* ======================================================================== search controller
  * Early pruning (Sec. 4.1) and lazy verification (Sec. 4.3) of a speculative beam search whose

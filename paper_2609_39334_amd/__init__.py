@@ -73,7 +73,7 @@ _SIG = {
     "tkv_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_verify": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_kv_append": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _P, _I32, _P, _P, _P, _P, _P]),
-    "tkv_cd_sample": (ctypes.c_int, [_I32, _I32, ctypes.c_float, _I32, _P, _P, _P, _P, _P, _P, _P]),
+    "tkv_cd_sample": (ctypes.c_int, [_I32, _I32, ctypes.c_float, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]),
     "tkv_search_create": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.POINTER(_P)]),
     "tkv_search_destroy": (None, [_P]),
     "tkv_search_expand": (ctypes.c_int, [_P, _I32, _I32, _PI32]),
@@ -346,7 +346,8 @@ def tkv_kv_append(dst: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, k
 def tkv_cd_sample(logits: torch.Tensor, temperature: float, draw_off: torch.Tensor, uniform: torch.Tensor,
                   max_potential: int, stream=None):
     """Draws each row's potential-many tokens and groups them; returns device tensors
-    (tokens, counts, n_groups): row r's groups at [draw_off[r], draw_off[r] + n_groups[r])."""
+    (tokens, counts, n_groups): row r's groups at [draw_off[r], draw_off[r] + n_groups[r]).  A row
+    whose draws fall outside `uniform` gets n_groups -1."""
     if logits.dim() != 2 or logits.dtype != torch.float32 or not logits.is_cuda or not logits.is_contiguous():
         raise ValueError("tkv_cd_sample: logits must be a contiguous float32 GPU tensor [n_rows, vocab]")
     n_rows, vocab = logits.shape
@@ -359,8 +360,8 @@ def tkv_cd_sample(logits: torch.Tensor, temperature: float, draw_off: torch.Tens
     cnt = torch.empty(n, dtype=torch.int32, device=logits.device)
     ng = torch.empty(max(1, n_rows), dtype=torch.int32, device=logits.device)
     _check(lib().tkv_cd_sample(n_rows, vocab, float(temperature), int(max_potential), logits.data_ptr(),
-                               uniform.data_ptr(), draw_off.data_ptr(), tok.data_ptr(), cnt.data_ptr(), ng.data_ptr(),
-                               _stream(stream)))
+                               uniform.data_ptr(), draw_off.data_ptr(), int(uniform.numel()), tok.data_ptr(),
+                               cnt.data_ptr(), ng.data_ptr(), _stream(stream)))
     return tok, cnt, ng[:n_rows]
 
 

@@ -81,7 +81,7 @@ __device__ __forceinline__ float thread_sum(const float (&x)[kPerThread], float 
 template <bool VEC>
 __global__ __launch_bounds__(kSampleThreads) void cd_sample(const float* __restrict__ logits, int vocab, float c,
                                                             const float* __restrict__ uniform,
-                                                            const int32_t* __restrict__ draw_off,
+                                                            const int32_t* __restrict__ draw_off, int32_t n_draws,
                                                             int32_t* __restrict__ out_tok, int32_t* __restrict__ out_cnt,
                                                             int32_t* __restrict__ n_groups) {
     __shared__ float base[kMaxTiles];       // b_i
@@ -96,7 +96,9 @@ __global__ __launch_bounds__(kSampleThreads) void cd_sample(const float* __restr
     const float* row = logits + static_cast<size_t>(r) * vocab;
     const int off = draw_off[r], n = draw_off[r + 1] - off;
     const int n_tiles = (vocab + kTile - 1) / kTile;
-    if (n > kMaxPotential || n_tiles > kMaxTiles) {  // the host checks both bounds
+    // a row whose draws fall outside the caller's arrays (offsets are device data the host cannot
+    // check), or too many of them, is refused before anything of it is read or written
+    if (n < 0 || off < 0 || static_cast<int64_t>(off) + n > n_draws || n > kMaxPotential || n_tiles > kMaxTiles) {
         if (t == 0) n_groups[r] = -1;
         return;
     }
@@ -239,7 +241,7 @@ __global__ __launch_bounds__(kSampleThreads) void cd_sample(const float* __restr
 
 TKV_EXPORT int tkv_cd_sample(int32_t n_rows, int32_t vocab, float temperature, int32_t max_potential,
                              const float* d_logits, const float* d_uniform, const int32_t* d_draw_off,
-                             int32_t* d_token, int32_t* d_count, int32_t* d_n_groups, void* stream) {
+                             int32_t n_draws, int32_t* d_token, int32_t* d_count, int32_t* d_n_groups, void* stream) {
     tkv::clear_error();
     if (n_rows < 0 || vocab < 1) return tkv::set_error(TKV_EINVAL, "tkv_cd_sample: n_rows %d, vocab %d", n_rows, vocab);
     if (vocab > kMaxTiles * kTile)
@@ -248,8 +250,9 @@ TKV_EXPORT int tkv_cd_sample(int32_t n_rows, int32_t vocab, float temperature, i
         return tkv::set_error(TKV_EINVAL, "tkv_cd_sample: temperature must be positive and finite");
     if (max_potential < 0 || max_potential > kMaxPotential)
         return tkv::set_error(TKV_EINVAL, "tkv_cd_sample: potential up to %d per row (got %d)", kMaxPotential, max_potential);
+    if (n_draws < 0) return tkv::set_error(TKV_EINVAL, "tkv_cd_sample: n_draws = %d < 0", n_draws);
     if (n_rows == 0) return TKV_OK;
-    if (!d_logits || !d_draw_off || !d_n_groups || (max_potential > 0 && (!d_uniform || !d_token || !d_count)))
+    if (!d_logits || !d_draw_off || !d_n_groups || (n_draws > 0 && (!d_uniform || !d_token || !d_count)))
         return tkv::set_error(TKV_EINVAL, "tkv_cd_sample: NULL pointer");
     // 16-byte loads when every row starts 16-byte aligned
     const bool vec = vocab % 4 == 0 && reinterpret_cast<uintptr_t>(d_logits) % 16 == 0;
@@ -257,10 +260,10 @@ TKV_EXPORT int tkv_cd_sample(int32_t n_rows, int32_t vocab, float temperature, i
     const hipStream_t st = static_cast<hipStream_t>(stream);
     if (vec)
         hipLaunchKernelGGL(cd_sample<true>, dim3(static_cast<unsigned>(n_rows)), dim3(kSampleThreads), 0, st, d_logits,
-                           vocab, c, d_uniform, d_draw_off, d_token, d_count, d_n_groups);
+                           vocab, c, d_uniform, d_draw_off, n_draws, d_token, d_count, d_n_groups);
     else
         hipLaunchKernelGGL(cd_sample<false>, dim3(static_cast<unsigned>(n_rows)), dim3(kSampleThreads), 0, st, d_logits,
-                           vocab, c, d_uniform, d_draw_off, d_token, d_count, d_n_groups);
+                           vocab, c, d_uniform, d_draw_off, n_draws, d_token, d_count, d_n_groups);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return tkv::set_error(TKV_EHIP, "tkv_cd_sample launch: %s", hipGetErrorString(e));
     return TKV_OK;

@@ -186,3 +186,18 @@ def test_cd_sample_rejects_bad_arguments():
     empty = torch.zeros((0, 10), dtype=torch.float32, device="cuda")
     tok, cnt, ng = tkv.tkv_cd_sample(empty, 0.8, torch.zeros(1, dtype=torch.int32, device="cuda"), u, 0)
     assert ng.numel() == 0
+
+
+def test_cd_sample_refuses_rows_outside_the_arrays():
+    # draw offsets are device data: a row whose range leaves the 6-entry arrays (row 1) or runs
+    # backwards (row 2) is refused (-1) and touches nothing; rows 0 and 3 are sampled as usual
+    import paper_2609_39334_amd as tkv
+    logits = torch.zeros((4, 100), dtype=torch.float32, device="cuda")
+    off = torch.tensor([0, 2, 9, 4, 6], dtype=torch.int32, device="cuda")
+    u = torch.tensor([0.015, 0.5, 0.25, 0.75, 0.125, 0.995], dtype=torch.float32, device="cuda")
+    tok, cnt, ng = tkv.tkv_cd_sample(logits, 1.0, off, u, 8)
+    torch.cuda.synchronize()
+    ng = ng.cpu().tolist()
+    assert ng[1] == -1 and ng[2] == -1
+    assert ng[0] == 2 and tok[0:2].cpu().tolist() == [1, 50] and cnt[0:2].cpu().tolist() == [1, 1]
+    assert ng[3] == 2 and tok[4:6].cpu().tolist() == [12, 99] and cnt[4:6].cpu().tolist() == [1, 1]
