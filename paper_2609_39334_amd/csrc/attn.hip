@@ -902,7 +902,7 @@ namespace tkv {
 int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream) {
     (void)bytes;
     if (p->desc_bytes) {
-        const hipError_t e = hipMemcpyAsync(d_ws, p->image.data(), p->desc_bytes, hipMemcpyHostToDevice,
+        const hipError_t e = hipMemcpyAsync(d_ws, p->image.get(), p->desc_bytes, hipMemcpyHostToDevice,
                                             static_cast<hipStream_t>(stream));
         if (e != hipSuccess) return set_error(TKV_EHIP, "tkv_plan_upload: hipMemcpyAsync: %s", hipGetErrorString(e));
     }

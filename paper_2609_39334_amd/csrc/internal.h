@@ -4,6 +4,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -93,8 +94,9 @@ struct tkv_plan {
     std::vector<tkv::BlkDesc> blks;
     std::vector<tkv::MergeDesc> merges;
     std::vector<int32_t> merge_slots;
-    std::vector<tkv::WaveDesc> wave_desc;     // wave-kernel items: record w is wave w's first item,
-                                              // then each wave's further items contiguously
+    std::vector<int32_t> wave_rec;            // wave-kernel records, as the wave item each holds (-1: none):
+                                              // record w is wave w's first item, then each wave's further
+                                              // items contiguously (written into the image by the layout)
     std::vector<int32_t> wave_off;            // [n_waves + 1] wave w's further items: [off[w], off[w+1])
     std::vector<int32_t> wave_tiles;          // [n_waves] column tiles of the wave's items (0: no work)
     int32_t n_slots = 0;
@@ -102,7 +104,7 @@ struct tkv_plan {
     // workspace layout (byte offsets)
     size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wdesc = 0, off_woff = 0, off_wtiles = 0;
     size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;
-    std::vector<uint8_t> image;  // host copy of the descriptor region
+    std::unique_ptr<uint8_t[]> image;  // host copy of the descriptor region (desc_bytes)
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)
     tkv_plan_stats stats{};
     // instrumentation: 3 HIP events per recorded call (see tkv_plan_profile)

@@ -62,6 +62,60 @@ struct Chunk {
     std::vector<TokDesc> toks;  // slot filled in later
 };
 
+// Dense ids for 64-bit keys in first-insertion order (open addressing, linear probing, grown at half
+// load).  Keys never equal ~0.
+class IdMap {
+  public:
+    explicit IdMap(size_t expected) { rehash(std::max<size_t>(16, expected * 2)); }
+    // The key's id; a new key takes `next_id` (and *fresh is set).
+    int32_t get(uint64_t key, int32_t next_id, bool* fresh) {
+        if (2 * (n_ + 1) > keys_.size()) rehash(keys_.size() * 2);
+        size_t h = mix(key) & mask_;
+        while (keys_[h] != kEmpty) {
+            if (keys_[h] == key) {
+                *fresh = false;
+                return vals_[h];
+            }
+            h = (h + 1) & mask_;
+        }
+        keys_[h] = key;
+        vals_[h] = next_id;
+        ++n_;
+        *fresh = true;
+        return next_id;
+    }
+
+  private:
+    static constexpr uint64_t kEmpty = ~uint64_t{0};
+    static uint64_t mix(uint64_t k) {
+        k ^= k >> 33;
+        k *= 0xff51afd7ed558ccdull;
+        k ^= k >> 33;
+        return k;
+    }
+    void rehash(size_t want) {
+        size_t cap = 16;
+        while (cap < want) cap <<= 1;
+        std::vector<uint64_t> ok;
+        std::vector<int32_t> ov;
+        ok.swap(keys_);
+        ov.swap(vals_);
+        keys_.assign(cap, kEmpty);
+        vals_.resize(cap);
+        mask_ = cap - 1;
+        for (size_t i = 0; i < ok.size(); ++i) {
+            if (ok[i] == kEmpty) continue;
+            size_t h = mix(ok[i]) & mask_;
+            while (keys_[h] != kEmpty) h = (h + 1) & mask_;
+            keys_[h] = ok[i];
+            vals_[h] = ov[i];
+        }
+    }
+    std::vector<uint64_t> keys_;
+    std::vector<int32_t> vals_;
+    size_t mask_ = 0, n_ = 0;
+};
+
 // Split n things into near-equal tiles of at most `cap`.
 template <class F>
 void tile_evenly(int32_t n, int32_t cap, F f) {
@@ -147,26 +201,22 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
 
         // ------------------------------------------------------------ shared items (small rows)
         std::vector<Node> nodes;
-        std::unordered_map<uint64_t, int32_t> child;
-        std::vector<std::vector<int32_t>> path(n_rows);
+        IdMap child(static_cast<size_t>(s.num_blocks));  // (parent node + 1, block) -> node
+        std::vector<int32_t> path(n_rows ? kv_indptr[n_rows] : 0, -1);  // trie node of each table entry
         for (int32_t r = 0; r < n_rows; ++r) {
             if (static_cast<int64_t>(L[r]) * G >= tkv::kTileRows) continue;
             int32_t cur = -1;
             for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1]; ++j) {
                 const int32_t b = kv_blocks[j];
                 const uint64_t key = (static_cast<uint64_t>(static_cast<uint32_t>(cur + 1)) << 32) | static_cast<uint32_t>(b);
-                auto it = child.find(key);
-                int32_t nd;
-                if (it == child.end()) {
-                    nd = static_cast<int32_t>(nodes.size());
+                bool fresh = false;
+                const int32_t nd = child.get(key, static_cast<int32_t>(nodes.size()), &fresh);
+                if (fresh) {
                     const int32_t pos0 = cur < 0 ? 0 : nodes[cur].pos0 + nodes[cur].len;
                     nodes.push_back(Node{cur, b, block_len[b], pos0, 0, -1});
-                    child.emplace(key, nd);
-                } else {
-                    nd = it->second;
                 }
                 nodes[nd].count += 1;
-                path[r].push_back(nd);
+                path[j] = nd;
                 cur = nd;
             }
         }
@@ -183,7 +233,8 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         }
         for (int32_t r = 0; r < n_rows; ++r) {
             int32_t last = -1;
-            for (int32_t nd : path[r]) {
+            for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1] && path[j] >= 0; ++j) {
+                const int32_t nd = path[j];
                 if (nodes[nd].seg != last) {
                     last = nodes[nd].seg;
                     segs[last].rows.push_back(r);
@@ -371,18 +422,20 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
             for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
                 const std::vector<int32_t>& its = by_t[T];
                 if (its.empty()) continue;
-                std::map<std::pair<int32_t, int32_t>, int32_t> gid;
+                IdMap gid(its.size());  // (first key block, KV head) -> group
                 std::vector<std::vector<int32_t>> groups;
                 std::vector<int64_t> gcost;
                 for (int32_t i : its) {
                     const ItemDesc& it = p->wave_items[i];
-                    auto ins = gid.emplace(std::make_pair(it.blk_off, it.kvh), static_cast<int32_t>(groups.size()));
-                    if (ins.second) {
+                    bool fresh = false;
+                    const int32_t g2 = gid.get((static_cast<uint64_t>(it.blk_off) << 8) | static_cast<uint32_t>(it.kvh),
+                                               static_cast<int32_t>(groups.size()), &fresh);
+                    if (fresh) {
                         groups.emplace_back();
                         gcost.push_back(0);
                     }
-                    groups[ins.first->second].push_back(i);
-                    gcost[ins.first->second] += cost(it);
+                    groups[g2].push_back(i);
+                    gcost[g2] += cost(it);
                 }
                 std::vector<int32_t> gorder(groups.size());
                 std::iota(gorder.begin(), gorder.end(), 0);
@@ -451,42 +504,17 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 }
                 if (src >= 0) slots[slot] = &xcd_waves[src][next[src]++];
             }
-            auto record = [&](const ItemDesc& it) {
-                // widths 1 and 2 walk blocks in pairs: an odd key list gets an empty block
-                const int32_t nb_run = it.pad <= 2 ? (it.n_blk + 1) & ~1 : it.n_blk;
-                tkv::WaveDesc wd{};
-                int32_t pos = it.pos0;
-                for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
-                    const bool in = j < it.n_blk;
-                    const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
-                    wd.e[4 * j] = bd.blk;
-                    wd.e[4 * j + 1] = in ? bd.len : 0;
-                    wd.e[4 * j + 2] = pos;
-                    if (in) pos += bd.len;
-                }
-                wd.e[3] = it.kvh;
-                wd.e[7] = it.n_tok;
-                wd.e[11] = nb_run;
-                for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
-                    const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
-                    wd.e[4 * (16 + t)] = td.qtok;
-                    wd.e[4 * (16 + t) + 1] = td.limit;
-                    wd.e[4 * (16 + t) + 2] = td.slot;
-                }
-                return wd;
-            };
             // Wave w's first item is record w (so the wave's first load depends on nothing); its
             // other items follow all first records, as the range [wave_off[w], wave_off[w + 1]).
-            p->wave_desc.assign(n_slots_w, tkv::WaveDesc{});
+            p->wave_rec.assign(n_slots_w, -1);
             for (size_t w = 0; w < n_slots_w; ++w)
-                if (slots[w] && !slots[w]->items.empty()) p->wave_desc[w] = record(p->wave_items[slots[w]->items[0]]);
+                if (slots[w] && !slots[w]->items.empty()) p->wave_rec[w] = slots[w]->items[0];
             p->wave_off.assign(1, static_cast<int32_t>(n_slots_w));
             for (size_t w = 0; w < n_slots_w; ++w) {
                 const bool busy = slots[w] && !slots[w]->items.empty();
                 if (busy)
-                    for (size_t k = 1; k < slots[w]->items.size(); ++k)
-                        p->wave_desc.push_back(record(p->wave_items[slots[w]->items[k]]));
-                p->wave_off.push_back(static_cast<int32_t>(p->wave_desc.size()));
+                    for (size_t k = 1; k < slots[w]->items.size(); ++k) p->wave_rec.push_back(slots[w]->items[k]);
+                p->wave_off.push_back(static_cast<int32_t>(p->wave_rec.size()));
                 p->wave_tiles.push_back(busy ? slots[w]->T : 0);
             }
         }
@@ -510,18 +538,20 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
             auto cost = [&](const ItemDesc& it) {
                 return static_cast<int64_t>(it.n_blk) * ((static_cast<int64_t>(it.n_tok) * G + 31) / 32) + 1;
             };
-            std::map<std::pair<int32_t, int32_t>, int32_t> gid;
+            IdMap gid(p->items.size());  // (first key block, KV head) -> group
             std::vector<std::vector<int32_t>> groups;
             std::vector<int64_t> gcost;
             for (int32_t i = 0; i < static_cast<int32_t>(p->items.size()); ++i) {
                 const ItemDesc& it = p->items[i];
-                auto ins = gid.emplace(std::make_pair(p->blks[it.blk_off].blk, it.kvh), static_cast<int32_t>(groups.size()));
-                if (ins.second) {
+                bool fresh = false;
+                const int32_t g2 = gid.get((static_cast<uint64_t>(p->blks[it.blk_off].blk) << 8) | static_cast<uint32_t>(it.kvh),
+                                           static_cast<int32_t>(groups.size()), &fresh);
+                if (fresh) {
                     groups.emplace_back();
                     gcost.push_back(0);
                 }
-                groups[ins.first->second].push_back(i);
-                gcost[ins.first->second] += cost(it);
+                groups[g2].push_back(i);
+                gcost[g2] += cost(it);
             }
             std::vector<int32_t> gorder(groups.size());
             std::iota(gorder.begin(), gorder.end(), 0);
@@ -583,7 +613,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         p->off_mslots = off;
         off = align256(off + bytes(p->merge_slots.size(), sizeof(int32_t)));
         p->off_wdesc = off;
-        off = align256(off + bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
+        off = align256(off + bytes(p->wave_rec.size(), sizeof(tkv::WaveDesc)));
         p->off_woff = off;
         off = align256(off + bytes(p->wave_off.size(), sizeof(int32_t)));
         p->off_wtiles = off;
@@ -594,18 +624,56 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         p->off_plse = off;
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq, sizeof(float)));
         p->total_bytes = std::max<size_t>(off, 256);
-        p->image.assign(p->desc_bytes, 0);
+        // a wave item's 1-KB record, written in place: 16 block slots {id, length, position, -} (the
+        // fourth words of slots 0-2 carry the KV head, token count and walked block count) and 48 token
+        // slots {query token, causal limit, partial slot, -}
+        auto write_record = [&](int32_t item, uint8_t* dst) {
+            std::memset(dst, 0, sizeof(tkv::WaveDesc));
+            if (item < 0) return;
+            const ItemDesc& it = p->wave_items[item];
+            int32_t* e = reinterpret_cast<int32_t*>(dst);
+            // widths 1 and 2 walk blocks in pairs: an odd key list gets an empty block
+            const int32_t nb_run = it.pad <= 2 ? (it.n_blk + 1) & ~1 : it.n_blk;
+            int32_t pos = it.pos0;
+            for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
+                const bool in = j < it.n_blk;
+                const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
+                e[4 * j] = bd.blk;
+                e[4 * j + 1] = in ? bd.len : 0;
+                e[4 * j + 2] = pos;
+                if (in) pos += bd.len;
+            }
+            e[3] = it.kvh;
+            e[7] = it.n_tok;
+            e[11] = nb_run;
+            for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
+                const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
+                e[4 * (16 + t)] = td.qtok;
+                e[4 * (16 + t) + 1] = td.limit;
+                e[4 * (16 + t) + 2] = td.slot;
+            }
+        };
+        // the image is written once: each section, its records in place, the padding zeroed
+        p->image.reset(new uint8_t[std::max<size_t>(p->desc_bytes, 1)]);
+        uint8_t* img = p->image.get();
+        size_t filled = 0;
         auto put = [&](size_t o, const void* src, size_t n) {
-            if (n) std::memcpy(p->image.data() + o, src, n);
+            if (o > filled) std::memset(img + filled, 0, o - filled);
+            if (n) std::memcpy(img + o, src, n);
+            filled = o + n;
         };
         put(p->off_items, p->items.data(), bytes(p->items.size(), sizeof(ItemDesc)));
         put(p->off_toks, p->toks.data(), bytes(p->toks.size(), sizeof(TokDesc)));
         put(p->off_blks, p->blks.data(), bytes(p->blks.size(), sizeof(BlkDesc)));
         put(p->off_merges, p->merges.data(), bytes(p->merges.size(), sizeof(MergeDesc)));
         put(p->off_mslots, p->merge_slots.data(), bytes(p->merge_slots.size(), sizeof(int32_t)));
-        put(p->off_wdesc, p->wave_desc.data(), bytes(p->wave_desc.size(), sizeof(tkv::WaveDesc)));
+        put(p->off_wdesc, nullptr, 0);
+        for (size_t r = 0; r < p->wave_rec.size(); ++r)
+            write_record(p->wave_rec[r], img + p->off_wdesc + r * sizeof(tkv::WaveDesc));
+        filled = p->off_wdesc + p->wave_rec.size() * sizeof(tkv::WaveDesc);
         put(p->off_woff, p->wave_off.data(), bytes(p->wave_off.size(), sizeof(int32_t)));
         put(p->off_wtiles, p->wave_tiles.data(), bytes(p->wave_tiles.size(), sizeof(int32_t)));
+        if (p->desc_bytes > filled) std::memset(img + filled, 0, p->desc_bytes - filled);
     } catch (...) {
         delete p;
         return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
