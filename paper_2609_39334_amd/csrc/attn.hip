@@ -983,7 +983,10 @@ static void free_events(const tkv_plan* p) {
     p->prof_max = p->prof_n = 0;
 }
 
-tkv_plan::~tkv_plan() { free_events(this); }
+tkv_plan::~tkv_plan() {
+    free_events(this);
+    tkv::give_image(std::move(image), image_cap);
+}
 
 TKV_EXPORT int tkv_plan_profile(tkv_plan* p, int32_t max_calls) {
     tkv::clear_error();

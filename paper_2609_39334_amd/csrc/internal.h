@@ -105,6 +105,7 @@ struct tkv_plan {
     size_t off_items = 0, off_toks = 0, off_blks = 0, off_merges = 0, off_mslots = 0, off_wdesc = 0, off_woff = 0, off_wtiles = 0;
     size_t off_po = 0, off_plse = 0, desc_bytes = 0, total_bytes = 0;
     std::unique_ptr<uint8_t[]> image;  // host copy of the descriptor region (desc_bytes)
+    size_t image_cap = 0;              // bytes allocated for it (returned to the image pool on destroy)
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)
     tkv_plan_stats stats{};
     // instrumentation: 3 HIP events per recorded call (see tkv_plan_profile)
@@ -115,6 +116,10 @@ struct tkv_plan {
 };
 
 namespace tkv {
+// Plan images of destroyed plans, kept for the next plans (plan.cpp): a decode loop that plans every
+// step then writes into memory that is already mapped.  take_image returns at least `bytes`.
+std::unique_ptr<uint8_t[]> take_image(size_t bytes, size_t* cap);
+void give_image(std::unique_ptr<uint8_t[]> image, size_t cap);
 // Launchers (attn.hip).
 int launch_attention(const tkv_plan* p, const void* q, const void* k, const void* v, void* o,
                      float* lse, void* stream);

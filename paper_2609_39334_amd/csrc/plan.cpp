@@ -27,6 +27,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <numeric>
 #include <queue>
 #include <unordered_map>
@@ -203,10 +204,21 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         std::vector<Node> nodes;
         IdMap child(static_cast<size_t>(s.num_blocks));  // (parent node + 1, block) -> node
         std::vector<int32_t> path(n_rows ? kv_indptr[n_rows] : 0, -1);  // trie node of each table entry
+        int32_t prev = -1;  // the previous row walked: rows that share a prefix are usually adjacent
         for (int32_t r = 0; r < n_rows; ++r) {
             if (static_cast<int64_t>(L[r]) * G >= tkv::kTileRows) continue;
             int32_t cur = -1;
-            for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1]; ++j) {
+            int32_t j = kv_indptr[r];
+            if (prev >= 0) {  // the blocks this row shares with the previous one lead to the same nodes
+                const int32_t len = std::min(kv_indptr[r + 1] - kv_indptr[r], kv_indptr[prev + 1] - kv_indptr[prev]);
+                for (int32_t k = 0; k < len && kv_blocks[j] == kv_blocks[kv_indptr[prev] + k]; ++k, ++j) {
+                    cur = path[kv_indptr[prev] + k];
+                    nodes[cur].count += 1;
+                    path[j] = cur;
+                }
+            }
+            prev = r;
+            for (; j < kv_indptr[r + 1]; ++j) {
                 const int32_t b = kv_blocks[j];
                 const uint64_t key = (static_cast<uint64_t>(static_cast<uint32_t>(cur + 1)) << 32) | static_cast<uint32_t>(b);
                 bool fresh = false;
@@ -327,10 +339,23 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         st.n_items_shared = static_cast<int32_t>(p->items.size() + p->wave_items.size());
 
         // ------------------------------------------------------------ row items (large rows)
+        {
+            size_t n_blk = 0, n_tok = 0, n_it = 0;
+            for (int32_t r = 0; r < n_rows; ++r) {
+                if (static_cast<int64_t>(L[r]) * G < tkv::kTileRows) continue;
+                n_blk += kv_indptr[r + 1] - kv_indptr[r];
+                n_tok += L[r];
+                n_it += static_cast<size_t>((L[r] + tpt - 1) / tpt) * s.hkv;
+            }
+            p->blks.reserve(p->blks.size() + n_blk);
+            p->toks.reserve(p->toks.size() + n_tok);
+            p->items.reserve(p->items.size() + n_it);
+        }
+        std::vector<int32_t> end_pos;  // end position of each block along a row's path
         for (int32_t r = 0; r < n_rows; ++r) {
             if (static_cast<int64_t>(L[r]) * G < tkv::kTileRows) continue;
             const int32_t row_blk_off = static_cast<int32_t>(p->blks.size());
-            std::vector<int32_t> end_pos;  // end position of each block along the path
+            end_pos.clear();
             int32_t pos = 0;
             for (int32_t j = kv_indptr[r]; j < kv_indptr[r + 1]; ++j) {
                 p->blks.push_back(BlkDesc{kv_blocks[j], block_len[kv_blocks[j]]});
@@ -654,7 +679,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
             }
         };
         // the image is written once: each section, its records in place, the padding zeroed
-        p->image.reset(new uint8_t[std::max<size_t>(p->desc_bytes, 1)]);
+        p->image = tkv::take_image(p->desc_bytes, &p->image_cap);
         uint8_t* img = p->image.get();
         size_t filled = 0;
         auto put = [&](size_t o, const void* src, size_t n) {
@@ -681,6 +706,52 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
     *out = p;
     return TKV_OK;
 }
+
+namespace tkv {
+namespace {
+struct ImagePool {
+    std::mutex m;
+    std::vector<std::pair<size_t, std::unique_ptr<uint8_t[]>>> free;  // (capacity, buffer)
+};
+// never destroyed: plans may be freed while the process exits
+ImagePool& image_pool() {
+    static ImagePool* pool = new ImagePool();
+    return *pool;
+}
+constexpr size_t kPooledImages = 2;
+}  // namespace
+
+std::unique_ptr<uint8_t[]> take_image(size_t bytes, size_t* cap) {
+    ImagePool& pool = image_pool();
+    {
+        std::lock_guard<std::mutex> lock(pool.m);
+        size_t best = pool.free.size();
+        for (size_t i = 0; i < pool.free.size(); ++i)
+            if (pool.free[i].first >= bytes && (best == pool.free.size() || pool.free[i].first < pool.free[best].first))
+                best = i;
+        if (best < pool.free.size()) {
+            *cap = pool.free[best].first;
+            std::unique_ptr<uint8_t[]> img = std::move(pool.free[best].second);
+            pool.free.erase(pool.free.begin() + static_cast<std::ptrdiff_t>(best));
+            return img;
+        }
+    }
+    *cap = std::max<size_t>(bytes + bytes / 8, 256);  // headroom for the next, slightly larger plan
+    return std::unique_ptr<uint8_t[]>(new uint8_t[*cap]);
+}
+
+void give_image(std::unique_ptr<uint8_t[]> image, size_t cap) {
+    if (!image) return;
+    ImagePool& pool = image_pool();
+    std::lock_guard<std::mutex> lock(pool.m);
+    pool.free.emplace_back(cap, std::move(image));
+    if (pool.free.size() > kPooledImages) {  // keep the largest
+        auto smallest = std::min_element(pool.free.begin(), pool.free.end(),
+                                         [](const auto& a, const auto& b) { return a.first < b.first; });
+        pool.free.erase(smallest);
+    }
+}
+}  // namespace tkv
 
 TKV_EXPORT size_t tkv_plan_workspace_bytes(const tkv_plan* p) { return p ? p->total_bytes : 0; }
 
