@@ -234,7 +234,8 @@ def _small_verify(seed, shape, n_ctx=2, n_cands=5):
     return wl.finalize()
 
 
-@pytest.mark.parametrize("seed,hq,hkv,d", [(40, 28, 4, 128), (41, 8, 2, 64), (42, 16, 2, 128), (43, 4, 4, 64)])
+@pytest.mark.parametrize("seed,hq,hkv,d", [(40, 28, 4, 128), (41, 8, 2, 64), (42, 16, 2, 128), (43, 4, 4, 64),
+                                           (44, 64, 1, 128), (45, 6, 2, 64)])
 @pytest.mark.parametrize("tile8_max", ["0", "100000"])
 def test_small_verify_batches_on_both_tile_kernels(seed, hq, hkv, d, tile8_max, monkeypatch):
     # a verify-only batch makes tile items alone; a few of them run as 8-wave workgroups (one 16-row
