@@ -196,7 +196,9 @@ size_t tkv_plan_workspace_bytes(const tkv_plan* plan);
 
 /* Copy the plan's descriptors into d_workspace (device memory of >= tkv_plan_workspace_bytes,
  * 256-byte aligned, caller-owned) on hip_stream; the plan keeps using that workspace until the
- * next upload.  The plan must outlive the copy.  EINVAL (size, alignment, NULL), EHIP. */
+ * next upload.  The plan must outlive the copy: a destroyed plan's host image is recycled by later
+ * plans.  (HIP stages a pageable host source before hipMemcpyAsync returns, which is what the
+ * library's own callers rely on.)  EINVAL (size, alignment, NULL), EHIP. */
 int tkv_plan_upload(tkv_plan* plan, void* d_workspace, size_t bytes, void* hip_stream);
 
 void tkv_plan_destroy(tkv_plan* plan);
