@@ -10,10 +10,13 @@
 * Lazy verification: each policy alone, at its boundary (tokens exceeding the threshold, the last
   sibling completing, the deferral limit), and the degenerate settings (threshold 0, limit 0).
 * Invariants after every event of random searches.
+* Rule 1 is safe against every future: on tiny searches, each candidate it prunes stays out of its
+  step's plain-beam-search selection for every assignment of the scores not yet known.
 """
 import json
 import os
 
+import numpy as np
 import pytest
 
 from oracle import search as S
@@ -215,3 +218,62 @@ def test_score_of_a_candidate_pruned_in_flight_is_ignored():
     ctl.score(batch, [0.4, 1.0])                    # their scores come back afterwards: ignored
     assert ctl.cands[1].arrival is None and ctl.round(0) == (True, [2])
     assert path_score(1, (0,)) == path_score(1, (0,))
+
+
+def _plain_selection(n, m, scores_by_path, depth):
+    """Plain beam search over a full assignment of path scores (distinct values): selected paths per step."""
+    k = n // m
+    frontier = [(i,) for i in range(n)]
+    out = []
+    for _ in range(depth):
+        keep = sorted(frontier, key=lambda p: -scores_by_path[p])[:k]
+        out.append(set(keep))
+        frontier = [p + (j,) for p in keep for j in range(m)]
+    return out
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_rule1_prunes_only_candidates_no_future_can_select(seed):
+    # tiny speculative searches (beam size 4, width 2, two steps): whenever rule 1 prunes a scored
+    # candidate, every assignment of the scores not yet known (five distinct levels each) leaves it out of
+    # its step's plain-beam-search selection
+    import itertools
+    rng = np.random.default_rng(seed)
+    n, m, depth = 4, 2, 2
+    paths = [(i,) for i in range(n)] + [(i, j) for i in range(n) for j in range(m)]
+    known = {p: float(np.float32(rng.random() * 0.9 + 0.05)) for p in paths}
+    levels = [0.011, 0.013, 0.017, 0.019, 0.023]          # fresh values: no ties with the known scores
+    ctl = S.Search(n // m, 64, 0, 6)
+    path_of = {}
+    first = ctl.expand(-1, n)
+    for i in range(n):
+        path_of[first + i] = (i,)
+    generating = list(range(first, first + n))
+    checked = 0
+    while generating:
+        c = generating.pop(int(rng.integers(0, len(generating))))
+        if ctl.cands[c].state != S.GENERATING:
+            continue
+        assert ctl.complete(c, 10)                          # threshold 0: verified at once
+        ctl.score(ctl.flush(), [known[path_of[c]]])
+        newly = ctl.pruned()
+        for x in newly:
+            cand = ctl.cands[x]
+            if cand.arrival is None:
+                continue                                    # pruned with its subtree, not by its own rank
+            scored = {path_of[y]: ctl.cands[y].score for y in path_of if ctl.cands[y].arrival is not None}
+            unknown = [p for p in paths if p not in scored]
+            if len(unknown) > 6:
+                continue
+            for vals in itertools.product(*(levels for _ in unknown)):
+                full = dict(scored)
+                full.update({p: v + 1e-4 * i for i, (p, v) in enumerate(zip(unknown, vals))})
+                assert path_of[x] not in _plain_selection(n, m, full, depth)[cand.depth]
+            checked += 1
+        if ctl.cands[c].state in (S.VERIFIED, S.SELECTED) and ctl.cands[c].depth < depth - 1:
+            f = ctl.expand(c, m)
+            for j in range(m):
+                path_of[f + j] = path_of[c] + (j,)
+                generating.append(f + j)
+        generating = [g for g in generating if ctl.cands[g].state == S.GENERATING]
+    assert checked > 0
