@@ -1,17 +1,20 @@
-"""Benchmark: tree-shared decode attention on one MI355X, against the HBM roofline on unique KV bytes.
+"""Benchmark: tree-shared decode + verify attention on one MI355X, against its roofline.
 
-    python bench.py [--steps K] [--warmup W] [--workload beam_decode] [--gpus 1] [--no-cpu]
+    python bench.py [--steps K] [--warmup W] [--workload mixed_serving] [--gpus 1] [--no-cpu]
 
+The default workload is the mixed serving batch (32/8/128; decode and causal verify rows in one
+launch, measured after 30% of the candidates were pruned and refilled); it is followed by the
+beam-search decode, step-verification and speculative-explosion workloads, reported as sub-records.
 (--workload kv_append times the K/V append kernel instead: all K/V writes of the spec_explosion
 tree, deduplicated blocks skipped.  --workload cd_sample times one CD branching step of the
-spec_explosion decode batch.)
+spec_explosion decode batch.  --workload verify_sweep and model_step are described below.)
 
 A step is one tkv_decode (or tkv_verify) call over the whole batch: the shared-segment and
-private-suffix contractions of every row and the log-sum-exp merge.  The block manager has built
-the tree, rows are coalesced and the plan is built and uploaded before timing (host times are
-reported beside the result).  Inputs are resident in HBM when the timed region starts; the
-K/V pool is rotated over several device copies so that no step finds it in the 256 MB
-Infinity Cache.  Prints one JSON line.
+private-suffix contractions of every row, the verify rows' causal tiles and the log-sum-exp merge.
+The block manager has built the tree, rows are coalesced and the plan is built and uploaded before
+timing (host times are reported beside the result).  Inputs are resident in HBM when the timed
+region starts; the K/V pool is rotated over several device copies so that no step finds it in the
+256 MB Infinity Cache.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -62,9 +65,12 @@ def _args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="beam_decode")
+    ap.add_argument("--workload", default="mixed_serving")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-sub-configs", action="store_true",
+                    help="time only the headline workload (by default the mixed_serving headline is followed by "
+                         "beam_decode, step_verify and spec_explosion, reported under 'configs')")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU baseline sample")
     ap.add_argument("--kv-copies", type=int, default=0,
                     help="device copies of the K/V pool rotated over the steps (0: enough to defeat the 256 MB MALL)")
@@ -504,29 +510,62 @@ def bench_model_step(a):
     print(json.dumps(out))
 
 
-def main():
-    a = _args()
-    if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus N with N > 1 is not supported "
-                                   "(the path shards by query tree with no exchange, see DESIGN.md)"}))
-        sys.exit(2)
+def cpu_baseline(a, qbits, kbits, vbits, tables, bl, q_lens):
+    """The oracle (fp64 NumPy gather attention, as it stands) on a bounded, seeded sample of the
+    batch's rows, on the host's cores: sub-batches of rows in parallel threads (BLAS one thread
+    each), submitted in seeded order until about `a.cpu_seconds` of wall time.  Rows are
+    independent, so a sub-batch computes what the whole batch would for its rows."""
+    from concurrent.futures import FIRST_COMPLETED, ThreadPoolExecutor, wait
+    from threadpoolctl import threadpool_limits
+    import oracle
+    import workloads as W
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    kf, vf = W.bf16_bits_to_f32(kbits), W.bf16_bits_to_f32(vbits)
+    qoff = np.concatenate([[0], np.cumsum(q_lens)]).astype(np.int64)
+    order = np.random.default_rng(0).permutation(len(tables))
+    per_sub = 4
+    subs = [order[i:i + per_sub].tolist() for i in range(0, len(order), per_sub)]
+
+    def run(sub):
+        idx = np.concatenate([np.arange(qoff[r], qoff[r + 1]) for r in sub])
+        qs = W.bf16_bits_to_f32(qbits[idx]).astype(np.float64)
+        oracle.attention(qs, kf, vf, [tables[r] for r in sub], bl, [q_lens[r] for r in sub])
+        return len(idx), len(sub)
+
+    done_tok = done_rows = n_sub = 0
+    with threadpool_limits(1):
+        with ThreadPoolExecutor(threads) as ex:
+            t0, c0 = time.perf_counter(), time.process_time()
+            pending = set()
+            k = 0
+            while True:
+                while len(pending) < threads and time.perf_counter() - t0 < a.cpu_seconds:
+                    pending.add(ex.submit(run, subs[k % len(subs)]))
+                    k += 1
+                if not pending:
+                    break
+                fin, pending = wait(pending, return_when=FIRST_COMPLETED)
+                for f in fin:
+                    nt, nr = f.result()
+                    done_tok += nt
+                    done_rows += nr
+                    n_sub += 1
+            wall, cpu_s = time.perf_counter() - t0, time.process_time() - c0
+    return {"value": round(done_tok / wall, 2), "unit": "candidate-tokens/s", "cores": threads, "kind": "oracle",
+            "effective_cores": round(cpu_s / wall, 2), "host_cpus": len(os.sched_getaffinity(0)),
+            "sample": f"{done_rows} row evaluations ({done_tok} query tokens) of this batch's {len(tables)} rows in "
+                      f"seeded order, {n_sub} sub-batches of {per_sub} rows on {threads} threads (BLAS 1 thread "
+                      f"each), fp64 NumPy gather attention, {wall:.1f} s wall, {cpu_s:.1f} s CPU"}
+
+
+def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
+    """Build the workload's tree on the library's block manager, coalesce and plan its measured
+    launch, and time `steps` calls after `warmup` ones.  Returns the result fields."""
     import torch
     import paper_2609_39334_amd as tkv
     import workloads as W
-
-    if not torch.cuda.is_available():
-        print(json.dumps({"error": "no GPU"}))
-        sys.exit(1)
-    if a.workload == "kv_append":
-        return bench_kv_append(a)
-    if a.workload == "cd_sample":
-        return bench_cd_sample(a)
-    if a.workload == "verify_sweep":
-        return bench_verify_sweep(a)
-    if a.workload == "model_step":
-        return bench_model_step(a)
     dev = torch.device("cuda:0")
-    wl = W.CONFIGS[a.workload](a.seed)
+    wl = W.CONFIGS[name](a.seed)
     s = wl.shape
     launch = len(wl.launches) - 1            # the last launch is the measured one (mixed: after prune)
 
@@ -581,22 +620,21 @@ def main():
 
     if a.calib_copy:
         calibration_copy(torch, dev)
-    for i in range(a.warmup):
+    for i in range(warmup):
         call(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record(stream)
-    for i in range(a.steps):                 # the timed steps: nothing else on the stream
+    for i in range(steps):                   # the timed steps: nothing else on the stream
         call(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
     ev1.record(stream)
     torch.cuda.synchronize()
-    ms_total = ev0.elapsed_time(ev1)
-    ms_step = ms_total / a.steps
-    # kernel durations from the library's own events (recorded on the launch stream around the
-    # attention kernels and around the merge), in a second pass of the same steps
-    tkv.tkv_plan_profile(plan.h, a.steps)
-    for i in range(a.steps):
+    ms_step = ev0.elapsed_time(ev1) / steps
+    # kernel durations from the library's own events (dispatch-packet timestamps on the launch
+    # stream around the attention kernel and around the merge), in a second pass of the same steps
+    tkv.tkv_plan_profile(plan.h, steps)
+    for i in range(steps):
         call(q, ks[i % n_copies], vs[i % n_copies], o, lse, stream)
     torch.cuda.synchronize()
     n_rec, ms_main, ms_merge = tkv.tkv_plan_profile_read(plan.h)
@@ -604,87 +642,53 @@ def main():
     t_main = ms_main / max(1, n_rec) / 1e3
     t_merge = ms_merge / max(1, n_rec) / 1e3 if st["n_merge"] else 0.0
 
-    # warm: the same steps on one pool copy, which then stays in the 256 MB Infinity Cache when it fits
-    for _ in range(a.warmup):
-        call(q, ks[0], vs[0], o, lse, stream)
-    torch.cuda.synchronize()
-    ev0.record(stream)
-    for _ in range(a.steps):
-        call(q, ks[0], vs[0], o, lse, stream)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    ms_step_warm = ev0.elapsed_time(ev1) / a.steps
-    stream_gbs = measure_copy_gbs(torch, dev, stream)
+    ms_step_warm = None
+    if warm:  # the same steps on one pool copy, which then stays in the 256 MB Infinity Cache when it fits
+        for _ in range(warmup):
+            call(q, ks[0], vs[0], o, lse, stream)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(steps):
+            call(q, ks[0], vs[0], o, lse, stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms_step_warm = ev0.elapsed_time(ev1) / steps
+    del ks, vs, k0, v0, q, o, lse, plan
+    torch.cuda.empty_cache()
 
     # ------------------------------------------------------------------ accounting
     b_uniq = st["uniq_kv_tokens"] * s.hkv * s.d * 2 * 2            # K and V, bf16
     flops = st["flops"]
-    cand_tok_s = n_qtok / (ms_step / 1e3)
-    achieved_gbs = b_uniq / t_main / 1e9
-    traffic = measured_traffic(a, a.workload, ATTN_SOURCES)
-    main_kernels = ["attn_fwd"]  # tile items and the wave grid in one launch
+    t_call = ms_step / 1e3
+    traffic = measured_traffic(a, name, ATTN_SOURCES)
+    kernel = "attn_fwd"  # tile items and the wave grid in one launch (attn_tile8 for small verify plans)
     # the bound is the one the work's arithmetic intensity puts it under (ridge: peak flop/s over
     # peak bytes/s); decode is HBM-bound, multi-token verify of long steps is MFMA-bound
     mfma_bound = flops / b_uniq > MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
     if mfma_bound:
-        achieved_tf = flops / t_main / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved_tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
-                "kernel": "+".join(main_kernels), "algorithmic_flops": flops, "kernel_us": round(t_main * 1e6, 2)}
+        achieved = flops / t_main / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic, "kernel": kernel,
+                "algorithmic_flops": flops, "kernel_us": round(t_main * 1e6, 2),
+                "frac_whole_call": round(flops / t_call / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
     else:
-        roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "+".join(main_kernels), "algorithmic_bytes": b_uniq, "kernel_us": round(t_main * 1e6, 2)}
-
-    # ------------------------------------------------------------------ CPU baseline (oracle)
-    cpu = None
-    if not a.no_cpu:
-        import oracle
-        try:
-            from threadpoolctl import threadpool_info
-            blas_threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
-        except Exception:
-            blas_threads = None
-        kf, vf = W.bf16_bits_to_f32(kbits), W.bf16_bits_to_f32(vbits)
-        qf = W.bf16_bits_to_f32(qbits).astype(np.float64)
-        order = np.random.default_rng(0).permutation(len(tables))
-        n_calls, done_tok, t_cpu, passes = 0, 0, 0.0, 0
-        while t_cpu < a.cpu_seconds:                      # rows in seeded order (repeating) until the time target
-            r = int(order[n_calls % len(order)])
-            t0 = time.perf_counter()
-            oracle.attention(qf, kf, vf, tables, bl, q_lens, rows=[r])
-            t_cpu += time.perf_counter() - t0
-            n_calls += 1
-            done_tok += q_lens[r]
-        cpu = {"value": round(done_tok / t_cpu, 2), "unit": "candidate-tokens/s",
-               "cores": blas_threads or len(os.sched_getaffinity(0)), "kind": "oracle",
-               "host_cpus": len(os.sched_getaffinity(0)),
-               "sample": f"{n_calls} row evaluations ({done_tok} query tokens; rows of this batch in seeded order, "
-                         f"{len(tables)} rows per pass), fp64 NumPy gather attention, {t_cpu:.1f} s"}
-
-    out = {
-        "metric": "candidate-tokens/s and % HBM roofline (unique KV bytes), tree decode + verify",
-        "value": round(cand_tok_s, 1),
-        "unit": "candidate-tokens/s",
-        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded trees, N(0,1) bf16 values)",
-        "config": {"workload": a.workload, "hq": s.hq, "hkv": s.hkv, "head_dim": s.d, "block_size": s.block_size,
+        achieved = b_uniq / t_main / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kernel,
+                "algorithmic_bytes": b_uniq, "kernel_us": round(t_main * 1e6, 2),
+                "frac_whole_call": round(b_uniq / t_call / 1e9 / HBM_PEAK_GBS, 4)}
+    res = {
+        "value": round(n_qtok / t_call, 1), "ms_per_step": round(ms_step, 5), "steps": steps, "warmup": warmup,
+        "config": {"workload": name, "hq": s.hq, "hkv": s.hkv, "head_dim": s.d, "block_size": s.block_size,
                    "rows": st["n_rows"], "query_tokens": n_qtok, "logical_candidate_tokens": st["logical_qtok"],
                    "decode": bool(L.decode), "unique_kv_bytes": b_uniq,
                    "per_row_kv_bytes": st["path_kv_tokens"] * s.hkv * s.d * 4,
-                   "kv_pool_copies_rotated": n_copies},
+                   "algorithmic_flops": flops, "kv_pool_copies_rotated": n_copies},
         "roofline": roof,
-        "cpu_baseline": cpu,
-        "hbm_frac_whole_call": round(b_uniq / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
-        "stream_copy_gbs": round(stream_gbs, 1),
-        "frac_of_stream_copy": round(b_uniq / t_main / 1e9 / stream_gbs, 4),
-        "warm": {"ms_per_step": round(ms_step_warm, 5), "value": round(n_qtok / (ms_step_warm / 1e3), 1),
-                 "kv_pool_fits_mall": pool_bytes <= MALL_BYTES},
-        "mfma_frac_whole_call": round(flops / (ms_step / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
-        "logical_candidate_tokens_per_s": round(st["logical_qtok"] / (ms_step / 1e3), 1),
-        "kernel_us": {"+".join(main_kernels): round(t_main * 1e6, 2), "merge_partials": round(t_merge * 1e6, 2)},
+        "hbm_frac_whole_call": round(b_uniq / t_call / 1e9 / HBM_PEAK_GBS, 4),
+        "mfma_frac_whole_call": round(flops / t_call / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "logical_candidate_tokens_per_s": round(st["logical_qtok"] / t_call, 1),
+        "kernel_us": {kernel: round(t_main * 1e6, 2), "merge_partials": round(t_merge * 1e6, 2)},
         "plan": {"items": st["n_items"], "shared_items": st["n_items_shared"], "row_items": st["n_items_row"],
                  "wave_items": st["n_items_wave"], "waves": st["n_waves"],
                  "partial_slots": st["n_slots"], "merged_tokens": st["n_merge"], "segments": st["n_segments"],
@@ -693,6 +697,72 @@ def main():
                     "plan_create_median": round(sorted(t_create)[2] * 1e3, 3),
                     "first_plan_with_workspace_and_upload": round(t_plan * 1e3, 2)},
     }
+    if ms_step_warm is not None:
+        res["warm"] = {"ms_per_step": round(ms_step_warm, 5), "value": round(n_qtok / (ms_step_warm / 1e3), 1),
+                       "kv_pool_fits_mall": pool_bytes <= MALL_BYTES}
+    if with_cpu:
+        res["cpu_baseline"] = cpu_baseline(a, qbits, kbits, vbits, tables, bl, q_lens)
+    return res
+
+
+SUB_CONFIGS = ("beam_decode", "step_verify", "spec_explosion")
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus N with N > 1 is not supported "
+                                   "(the path shards by query tree with no exchange, see DESIGN.md)"}))
+        sys.exit(2)
+    import torch
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU"}))
+        sys.exit(1)
+    if a.workload == "kv_append":
+        return bench_kv_append(a)
+    if a.workload == "cd_sample":
+        return bench_cd_sample(a)
+    if a.workload == "verify_sweep":
+        return bench_verify_sweep(a)
+    if a.workload == "model_step":
+        return bench_model_step(a)
+    import paper_2609_39334_amd as tkv
+    tkv.lib()                                  # fails loudly if the HIP library is missing
+    head = run_attention(a, a.workload, a.steps, a.warmup, with_cpu=not a.no_cpu)
+    torch.cuda.synchronize()
+    stream_gbs = measure_copy_gbs(torch, torch.device("cuda:0"), torch.cuda.current_stream())
+    out = {
+        "metric": "candidate-tokens/s and % HBM roofline (unique KV bytes), tree decode + verify",
+        "value": head["value"],
+        "unit": "candidate-tokens/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded trees, N(0,1) bf16 values)",
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "cpu_baseline": head.get("cpu_baseline"),
+        "hbm_frac_whole_call": head["hbm_frac_whole_call"],
+        "mfma_frac_whole_call": head["mfma_frac_whole_call"],
+        "stream_copy_gbs": round(stream_gbs, 1),
+        "unique_kv_frac_of_stream_copy": round(head["config"]["unique_kv_bytes"] / (head["kernel_us"]["attn_fwd"] / 1e6)
+                                               / 1e9 / stream_gbs, 4),
+        "logical_candidate_tokens_per_s": head["logical_candidate_tokens_per_s"],
+        "kernel_us": head["kernel_us"], "plan": head["plan"], "host_ms": head["host_ms"],
+    }
+    if "warm" in head:
+        out["warm"] = head["warm"]
+    if not a.no_sub_configs and a.workload == "mixed_serving":
+        subs = {}
+        for name in SUB_CONFIGS:       # the other workloads, each timed the same way (no CPU baseline)
+            r = run_attention(a, name, max(a.steps, 100), max(a.warmup, 10), warm=False)
+            subs[name] = {"value": r["value"], "ms_per_step": r["ms_per_step"], "steps": r["steps"],
+                          "rows": r["config"]["rows"], "query_tokens": r["config"]["query_tokens"],
+                          "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "unit", "frac",
+                                                                     "frac_whole_call", "kernel_us", "traffic")},
+                          "kernel_us": r["kernel_us"], "plan_create_ms": r["host_ms"]["plan_create_median"]}
+        out["configs"] = subs
     print(json.dumps(out))
 
 

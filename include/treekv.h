@@ -166,6 +166,9 @@ int tkv_bm_coalesce(const tkv_bm* bm, int32_t n_cand, const int32_t* seqs, const
  *          never read)
  *   lse    [n_qtok][hq] fp32, nullable
  * Supported: block_size 16, d in {64, 128}, hq % hkv == 0, hq / hkv <= 64, hq <= 256.
+ * Inputs must be finite: q and the K/V slots a row reads may not hold NaN or infinity (the kernels
+ * are built on the assumption that no NaN enters the arithmetic; a NaN input gives an unspecified
+ * result, not an error).  Padding slots past a block's length are never read and may hold anything.
  */
 typedef struct {
     int32_t hq, hkv, d, block_size, num_blocks;
@@ -178,18 +181,37 @@ typedef struct tkv_plan tkv_plan;
  *   kv_indptr[n_rows+1] offsets into kv_blocks; kv_blocks = the rows' block tables in path order;
  *   block_len[num_blocks] = tokens per block (tkv_bm_block_len); multiplicity[n_rows] = logical
  *   candidates per row (nullable: all 1; used for accounting only).
- * The planner finds the blocks that several rows share (a trie over the tables) so that each
- * shared K/V block is contracted against all query rows that reference it, splits long runs,
- * and lays out descriptors for the device.  EINVAL: bad shape, q_len < 1, q_len > kv_len, a block
- * id out of range or with block_len outside [1, block_size], multiplicity < 1.
- * Work placement can be tuned through the environment, read at each call (the results do not
- * depend on it): TKV_WAVE_MAX_ROWS (widest shared chunk, in query rows, kept on the wave kernel;
- * default 96), TKV_TILE_MIN_ITEMS (wider chunks go to 128-row tiles only if they make at least
- * this many; default 0), TKV_WAVES (size of the wave grid; default 2048, less the 4 waves of
- * each workgroup slot that the 128-row tiles take when they are fewer than the 512 slots). */
+ * The planner finds the blocks that several rows share (a trie over the tables).  Rows whose own
+ * query tile is small (q_len * G < 64: decode rows and short verify rows) go through the shared
+ * segments, so that each shared K/V block is contracted once against all of those rows' query
+ * tokens.  A longer verify row fills 128-row tiles of its own tokens, each walking the row's whole
+ * path: its shared context is then read once per tile (mostly from L2: tiles of one context are
+ * launched together on one XCD), which costs no extra arithmetic, since every query token needs
+ * its own dot products with every context key either way.  Long runs are split, and descriptors
+ * are laid out for the device.  EINVAL: bad shape, q_len < 1, q_len > kv_len, a block
+ * id out of range or with block_len outside [1, block_size], multiplicity < 1. */
 int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
                     const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
                     const int32_t* multiplicity, tkv_plan** out);
+
+/* Work placement, for tests and tuning: which kernel path and grid the planner uses.  The results
+ * do not depend on it (every placement computes the same attention up to fp32 summation order).
+ * A negative field keeps the default.
+ *   wave_max_rows    widest shared chunk, in query rows, kept on the wave kernel (default 96)
+ *   tile_min_items   wider chunks go to 128-row tiles only if they make at least this many items
+ *                    (default 0)
+ *   waves            size of the wave grid (default 2048, less the 4 waves of each workgroup slot
+ *                    that the 128-row tiles take when they are fewer than the 512 slots; 0: default)
+ *   tile8_max_items  a plan of at most this many tile items and no wave-grid work runs them as
+ *                    8-wave workgroups (default 256) */
+typedef struct {
+    int32_t wave_max_rows, tile_min_items, waves, tile8_max_items;
+} tkv_plan_options;
+
+/* tkv_plan_create with placement options (opts may be NULL: all defaults). */
+int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
+                       const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
+                       const int32_t* multiplicity, const tkv_plan_options* opts, tkv_plan** out);
 
 /* Device workspace the plan needs (descriptors + partial results), in bytes (>= 256). */
 size_t tkv_plan_workspace_bytes(const tkv_plan* plan);

@@ -8,8 +8,8 @@ speculation (Sec. 3) a candidate expands as soon as its own score is known, befo
 settled, so several depths are in flight at once.
 
 Early pruning (Sec. 4.1):
-* Rule 1.  Once more than k candidates are verified, a candidate ranked below the current top k
-  cannot enter the final top k, whatever the remaining scores are, and is pruned at once.
+* Rule 1.  A scored candidate is pruned as soon as k scored candidates that are sure to share its
+  round outscore it: no later score can lift it into that round's selection.
 * Rule 2.  Scores lie in [0, 1] and 1.0 is perfect.  Once k candidates have the perfect score they
   are the selection and every other candidate of the round is pruned.  (The paper notes that this
   rule may change the selection when later candidates would tie at 1.0; the first k to arrive win.)
@@ -19,8 +19,8 @@ Readings (the paper does not spell these out):
   While round d-1 is open, a depth-d candidate is speculative: it belongs to round d only if its
   parent is selected, and then so do its siblings.  The rules only use candidates that are sure to
   share the judged candidate's round: its siblings while speculative, all members otherwise.
-* "Ranked below the top k": at least k of those candidates have a strictly higher score (ties are
-  kept until the round is settled).  "First k": in the order in which scores arrived.
+* Below the top k: at least k of those candidates have a strictly higher score (ties are kept
+  until the round is settled).  The first k perfect scores: in the order in which scores arrived.
 * A round is settled by rule 2, or once every selected parent has expanded and every unpruned member
   has a score: the k best by (score descending, arrival ascending) are selected.  The other
   candidates of the round are pruned, and pruning a candidate prunes everything expanded from it.

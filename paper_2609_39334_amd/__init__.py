@@ -32,6 +32,10 @@ class tkv_shape(ctypes.Structure):
                 ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int32)]
 
 
+class tkv_plan_options(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("wave_max_rows", "tile_min_items", "waves", "tile8_max_items")]
+
+
 class tkv_plan_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("n_rows", "n_qtok", "n_items", "n_items_shared", "n_items_row",
                                               "n_slots", "n_merge", "n_segments", "n_shared_segments",
@@ -65,6 +69,8 @@ _SIG = {
     "tkv_bm_coalesce": (ctypes.c_int, [_P, _I32, _PI32, _PI32, _PI32, _PI32, _PI32, _PI32]),
     "tkv_plan_create": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _I32, _PI32, _PI32, _PI32, _PI32, _PI32,
                                        ctypes.POINTER(_P)]),
+    "tkv_plan_create_ex": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _I32, _PI32, _PI32, _PI32, _PI32, _PI32,
+                                          ctypes.POINTER(tkv_plan_options), ctypes.POINTER(_P)]),
     "tkv_plan_workspace_bytes": (ctypes.c_size_t, [_P]),
     "tkv_plan_upload": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P]),
     "tkv_plan_destroy": (None, [_P]),
@@ -272,6 +278,25 @@ def tkv_plan_create(shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplici
     h = _P()
     _check(lib().tkv_plan_create(ctypes.byref(sh), len(qi) - 1, _ptr(qi), _ptr(ki), _ptr(kb) if len(kb) else None,
                                  _ptr(bl), None if mu is None else _ptr(mu), ctypes.byref(h)))
+    return h.value
+
+
+def tkv_plan_create_ex(shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity=None, options=None) -> int:
+    """tkv_plan_create with placement options: a dict over the tkv_plan_options fields (missing
+    fields, or None, keep the defaults)."""
+    sh = tkv_shape(*[int(x) for x in shape])
+    qi, ki, kb, bl = _i32(q_indptr), _i32(kv_indptr), _i32(kv_blocks), _i32(block_len)
+    mu = None if multiplicity is None else _i32(multiplicity)
+    opts = None
+    if options is not None:
+        unknown = set(options) - {f for f, _ in tkv_plan_options._fields_}
+        if unknown:
+            raise ValueError(f"unknown plan options {sorted(unknown)}")
+        opts = tkv_plan_options(*[int(options.get(f, -1)) for f, _ in tkv_plan_options._fields_])
+    h = _P()
+    _check(lib().tkv_plan_create_ex(ctypes.byref(sh), len(qi) - 1, _ptr(qi), _ptr(ki), _ptr(kb) if len(kb) else None,
+                                    _ptr(bl), None if mu is None else _ptr(mu),
+                                    None if opts is None else ctypes.byref(opts), ctypes.byref(h)))
     return h.value
 
 
@@ -521,8 +546,8 @@ class Plan:
     """Owns a tkv_plan handle and the device workspace it was uploaded to."""
 
     def __init__(self, shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity=None,
-                 device="cuda", stream=None, upload=True):
-        self.h = tkv_plan_create(shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity)
+                 device="cuda", stream=None, upload=True, options=None):
+        self.h = tkv_plan_create_ex(shape, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity, options)
         self.workspace = None
         if upload:
             nbytes = tkv_plan_workspace_bytes(self.h)

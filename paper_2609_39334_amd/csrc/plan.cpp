@@ -24,7 +24,6 @@
 // Sec. 3.2; decode is L = 1).  A shared segment sits at the same positions in every row through
 // it, so one per-token limit suffices.
 #include <algorithm>
-#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -131,8 +130,18 @@ void tile_evenly(int32_t n, int32_t cap, F f) {
 TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
                                const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
                                const int32_t* multiplicity, tkv_plan** out) {
+    return tkv_plan_create_ex(shape, n_rows, q_indptr, kv_indptr, kv_blocks, block_len, multiplicity, nullptr, out);
+}
+
+TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
+                                  const int32_t* kv_indptr, const int32_t* kv_blocks, const int32_t* block_len,
+                                  const int32_t* multiplicity, const tkv_plan_options* opts, tkv_plan** out) {
     tkv::clear_error();
     if (!out) return set_error(TKV_EINVAL, "tkv_plan_create: out is NULL");
+    // placement options: a negative field (or no options) keeps the default
+    auto opt = [&](int32_t tkv_plan_options::*f, int64_t dflt) -> int64_t {
+        return opts && opts->*f >= 0 ? static_cast<int64_t>(opts->*f) : dflt;
+    };
     *out = nullptr;
     if (!shape) return set_error(TKV_EINVAL, "tkv_plan_create: shape is NULL");
     const tkv_shape s = *shape;
@@ -260,8 +269,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         // (none by default: tile items and the wave grid share one launch, and the wave grid
         // gives up the workgroup slots the tile items take); otherwise everything with G <= 16
         // stays on the wave grid.
-        int64_t wave_max_rows = tkv::kWaveMaxRows;
-        if (const char* env = std::getenv("TKV_WAVE_MAX_ROWS")) wave_max_rows = std::atoll(env);
+        int64_t wave_max_rows = opt(&tkv_plan_options::wave_max_rows, tkv::kWaveMaxRows);
         if (G <= tkv::kWaveRows) {
             int64_t wide_items = 0;
             for (const Segment& sg : segs) {
@@ -271,8 +279,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
                 const int64_t nb = static_cast<int64_t>(sg.nodes.size());
                 wide_items += (nb + kChunkBlocksWide - 1) / kChunkBlocksWide * ((seg_tok + tpt - 1) / tpt) * s.hkv;
             }
-            int64_t min_items = tkv::kTileMinItems;
-            if (const char* env = std::getenv("TKV_TILE_MIN_ITEMS")) min_items = std::atoll(env);
+            const int64_t min_items = opt(&tkv_plan_options::tile_min_items, tkv::kTileMinItems);
             if (wide_items < min_items) wave_max_rows = int64_t{1} << 40;
         }
         std::vector<Chunk> chunks;
@@ -393,7 +400,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
             const int32_t n_tile = static_cast<int32_t>(p->items.size());
             int32_t target = tkv::kWaveWorkers;
             if (n_tile < wg_slots) target = std::max(wg_slots / 2, wg_slots - n_tile) / kXcds * kXcds * tkv::kWaveWG;
-            if (const char* env = std::getenv("TKV_WAVES")) target = std::max(kXcds, std::atoi(env));
+            if (opts && opts->waves > 0) target = std::max(kXcds, opts->waves);
             auto cost = [](const ItemDesc& it) { return static_cast<int64_t>(it.n_blk) * (3 + it.pad) + 4; };
             std::vector<std::vector<int32_t>> by_t(tkv::kWaveMaxTiles + 1);
             std::vector<int64_t> cost_t(tkv::kWaveMaxTiles + 1, 0);
@@ -547,8 +554,7 @@ TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int
         st.n_waves = static_cast<int32_t>(p->wave_tiles.size());
         // a plan of a few tile items and nothing else gives each tile a CU to itself: its 128 rows then
         // run as eight 16-row waves, which shortens the tile's walk
-        int64_t tile8_max = tkv::kTile8MaxItems;
-        if (const char* env = std::getenv("TKV_TILE8_MAX_ITEMS")) tile8_max = std::atoll(env);
+        const int64_t tile8_max = opt(&tkv_plan_options::tile8_max_items, tkv::kTile8MaxItems);
         p->tile8 = p->wave_items.empty() && !p->items.empty() && static_cast<int64_t>(p->items.size()) <= tile8_max;
         st.n_slots = p->n_slots;
         st.n_merge = static_cast<int32_t>(p->merges.size());

@@ -12,15 +12,18 @@ Sec. 4.3 verification batch scale), with the datasets and models replaced by see
 random tokens and N(0,1) values.
 
 Streams (NumPy PCG64 seeded with a list):
-  [seed, 1]          tree structure (step lengths, branching choices, prune choices)
-  [seed, 2]          token ids, uniform over a 32,000-entry vocabulary
-  [seed, 3, 0]       K pool values, [seed, 3, 1] V pool values
-  [seed, 3, 2 + j]   query values of launch j
+  [seed, 1]             tree structure (step lengths, branching choices, prune choices)
+  [seed, 2]             token ids, uniform over a 32,000-entry vocabulary
+  [seed, 3, 0, c]       K pool values, [seed, 3, 1, c] V pool values
+  [seed, 3, 2 + j, c]   query values of launch j
+where c numbers the 2^24-value chunks of the flattened tensor (each chunk has its own stream, so
+the chunks are drawn in parallel threads and the values do not depend on the thread count).
 Values are drawn as float32 N(0,1) and rounded once to bf16 (round to nearest even).
 """
 from __future__ import annotations
 
 import math
+import os
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence, Tuple
 
@@ -47,12 +50,29 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def _normal_bf16(rng: np.random.Generator, shape: Tuple[int, ...], chunk: int = 1 << 24) -> np.ndarray:
+CHUNK = 1 << 24
+
+
+def _normal_bf16(key: Sequence[int], shape: Tuple[int, ...]) -> np.ndarray:
+    """N(0,1) float32 draws rounded to bf16 bits; chunk c of the flattened tensor comes from the
+    stream [*key, c]."""
+    from concurrent.futures import ThreadPoolExecutor
     n = int(np.prod(shape))
     out = np.empty(n, dtype=np.uint16)
-    for s in range(0, n, chunk):
-        e = min(n, s + chunk)
+
+    def fill(c):
+        s, e = c * CHUNK, min(n, (c + 1) * CHUNK)
+        rng = np.random.default_rng([*key, c])
         out[s:e] = f32_to_bf16_bits(rng.standard_normal(e - s, dtype=np.float32))
+
+    n_chunks = -(-n // CHUNK)
+    if n_chunks <= 1:
+        for c in range(n_chunks):
+            fill(c)
+    else:
+        workers = min(n_chunks, 16, len(os.sched_getaffinity(0)))
+        with ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill, range(n_chunks)))
     return out.reshape(shape)
 
 
@@ -136,14 +156,14 @@ class Workload:
         """K and V pools as bf16 bits, [num_blocks, hkv, block_size, d] each."""
         s = self.shape
         shp = (self.num_blocks, s.hkv, s.block_size, s.d)
-        k = _normal_bf16(np.random.default_rng([self.seed, 3, 0]), shp)
-        v = _normal_bf16(np.random.default_rng([self.seed, 3, 1]), shp)
+        k = _normal_bf16([self.seed, 3, 0], shp)
+        v = _normal_bf16([self.seed, 3, 1], shp)
         return k, v
 
     def q_values(self, launch_index: int, n_qtok: int) -> np.ndarray:
         """Queries of launch `launch_index` as bf16 bits, [n_qtok, hq, d]."""
         s = self.shape
-        return _normal_bf16(np.random.default_rng([self.seed, 3, 2 + launch_index]), (n_qtok, s.hq, s.d))
+        return _normal_bf16([self.seed, 3, 2 + launch_index], (n_qtok, s.hq, s.d))
 
 
 def poison_padding(k: np.ndarray, v: np.ndarray, block_len: np.ndarray) -> None:
