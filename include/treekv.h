@@ -265,6 +265,24 @@ int tkv_decode(const tkv_plan* plan, const void* q, const void* k, const void* v
 int tkv_verify(const tkv_plan* plan, const void* q, const void* k, const void* v, void* o,
                float* lse, void* hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): tkv_verify (decode batches included) with the plan's
+ * workspace in a device array of the library's own instead of a caller-uploaded one.  The plan
+ * need not be uploaded: each call copies its descriptors into that array (hipMemcpyAsync from the
+ * plan's host image on hip_stream) and then runs the same kernels as tkv_verify, with the same
+ * results.  The call allocates nothing: no hipMalloc, hipFree or allocating library routine.
+ *   - The array is TKV_NOALLOC_MAX_BYTES (64 MiB) on each GPU, held until the process ends; a plan
+ *     whose tkv_plan_workspace_bytes exceeds it is refused (EINVAL, nothing enqueued).
+ *   - It is the calling thread's current device's array; hip_stream must belong to that device.
+ *   - Every call on one GPU shares that array: calls that overlap on one GPU (two streams, or two
+ *     threads) race and give undefined results.  Calls ordered on one stream are safe.  Nothing in
+ *     the array needs to start at zero, and a call reads nothing that an earlier call left there.
+ *   - The plan must outlive the copy, as for tkv_plan_upload.
+ * EINVAL (NULL plan or tensors, plan too large), EHIP (symbol lookup, copy or launch failure). */
+#define TKV_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+int tkv_verify_noalloc(const tkv_plan* plan, const void* q, const void* k, const void* v, void* o,
+                       float* lse, void* hip_stream);
+
 /* Write the K and V of n_tok new tokens into the paged pool: the step before attention in a decode
  * loop.  Token t's rows go to pool slot d_dst[t] = block * block_size + position (tkv_bm_append for
  * tokens decoded one at a time, tkv_extend_slots for a completed step).  A slot of -1 -- a token of a

@@ -19,6 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtreekv.so")
 
 TKV_OK, TKV_EINVAL, TKV_ENOMEM, TKV_ENOSEQ, TKV_ECAP, TKV_EHIP = 0, -1, -2, -3, -4, -5
+TKV_NOALLOC_MAX_BYTES = 64 << 20   # the static workspace of tkv_verify_noalloc (treekv.h)
 
 
 class TkvError(RuntimeError):
@@ -78,6 +79,7 @@ _SIG = {
     "tkv_plan_get_view": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_view)]),
     "tkv_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_verify": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
+    "tkv_verify_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "tkv_kv_append": (ctypes.c_int, [ctypes.POINTER(tkv_shape), _P, _I32, _P, _P, _P, _P, _P]),
     "tkv_cd_sample": (ctypes.c_int, [_I32, _I32, ctypes.c_float, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]),
     "tkv_search_create": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.POINTER(_P)]),
@@ -348,6 +350,11 @@ def tkv_decode(plan: int, q, k, v, o, lse=None, stream=None) -> None:
 
 def tkv_verify(plan: int, q, k, v, o, lse=None, stream=None) -> None:
     _attn(lib().tkv_verify, plan, q, k, v, o, lse, stream)
+
+
+def tkv_verify_noalloc(plan: int, q, k, v, o, lse=None, stream=None) -> None:
+    """tkv_verify on the library's static workspace (the plan need not be uploaded)."""
+    _attn(lib().tkv_verify_noalloc, plan, q, k, v, o, lse, stream)
 
 
 def tkv_kv_append(dst: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, k: torch.Tensor, v: torch.Tensor,

@@ -28,6 +28,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 #include "internal.h"
 
 namespace {
@@ -911,9 +912,8 @@ int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream) {
 }
 
 template <int D>
-static int launch_d(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
+static int launch_d(const tkv_plan* p, uint8_t* ws, const void* q, const void* k, const void* v, void* o, float* lse,
                     hipStream_t st) {
-    uint8_t* ws = static_cast<uint8_t*>(p->d_ws);
     const auto* merges = reinterpret_cast<const MergeDesc*>(ws + p->off_merges);
     const auto* items = reinterpret_cast<const ItemDesc*>(ws + p->off_items);
     const auto* wdesc = reinterpret_cast<const int4*>(ws + p->off_wdesc);
@@ -966,16 +966,74 @@ static int launch_d(const tkv_plan* p, const void* q, const void* k, const void*
     return TKV_OK;
 }
 
+static int launch_ws(const tkv_plan* p, uint8_t* ws, const void* q, const void* k, const void* v, void* o, float* lse,
+                     hipStream_t st) {
+    return p->shape.d == 128 ? launch_d<128>(p, ws, q, k, v, o, lse, st) : launch_d<64>(p, ws, q, k, v, o, lse, st);
+}
+
 int launch_attention(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
                      void* stream) {
     if (!p->d_ws) return set_error(TKV_EINVAL, "attention: plan has not been uploaded");
     if (p->items.empty() && p->wave_items.empty()) return TKV_OK;
     if (!q || !k || !v || !o) return set_error(TKV_EINVAL, "attention: NULL tensor pointer");
-    const hipStream_t st = static_cast<hipStream_t>(stream);
-    return p->shape.d == 128 ? launch_d<128>(p, q, k, v, o, lse, st) : launch_d<64>(p, q, k, v, o, lse, st);
+    return launch_ws(p, static_cast<uint8_t*>(p->d_ws), q, k, v, o, lse, static_cast<hipStream_t>(stream));
 }
 
 }  // namespace tkv
+
+// ---------------------------------------------------------------------------- no-allocation variant
+// A workspace of the library's own, for callers that cannot allocate device memory: a file-scope
+// device array that each GPU holds for the life of the process.  Host code never uses its name as
+// an address: its per-device address comes from hipGetSymbolAddress, taken once per device with
+// that device current.  No part of it needs to start at zero: a call overwrites the descriptor
+// region first, and every partial slot is written by its item before the merge reads it.
+static constexpr size_t kScratchBytes = size_t{64} << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+static_assert(TKV_NOALLOC_MAX_BYTES == kScratchBytes, "header limit and device array agree");
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_for_current_device(uint8_t** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return tkv::set_error(TKV_EHIP, "tkv_verify_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices) return tkv::set_error(TKV_EINVAL, "tkv_verify_noalloc: device %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return tkv::set_error(TKV_EHIP, "tkv_verify_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = static_cast<uint8_t*>(g_scratch_ptr[dev]);
+    return TKV_OK;
+}
+}  // namespace
+
+TKV_EXPORT int tkv_verify_noalloc(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
+                                  void* stream) {
+    tkv::clear_error();
+    if (!p) return tkv::set_error(TKV_EINVAL, "tkv_verify_noalloc: plan is NULL");
+    if (p->total_bytes > kScratchBytes)
+        return tkv::set_error(TKV_EINVAL, "tkv_verify_noalloc: the plan needs a %zu-byte workspace, more than the %zu bytes "
+                              "of the library's static one (use tkv_plan_upload and tkv_verify)", p->total_bytes,
+                              kScratchBytes);
+    if (p->items.empty() && p->wave_items.empty()) return TKV_OK;
+    if (!q || !k || !v || !o) return tkv::set_error(TKV_EINVAL, "tkv_verify_noalloc: NULL tensor pointer");
+    uint8_t* ws = nullptr;
+    int rc = scratch_for_current_device(&ws);
+    if (rc != TKV_OK) return rc;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (p->desc_bytes) {
+        const hipError_t e = hipMemcpyAsync(ws, p->image.get(), p->desc_bytes, hipMemcpyHostToDevice, st);
+        if (e != hipSuccess) return tkv::set_error(TKV_EHIP, "tkv_verify_noalloc: hipMemcpyAsync: %s", hipGetErrorString(e));
+    }
+    return tkv::launch_ws(p, ws, q, k, v, o, lse, st);
+}
 
 static void free_events(const tkv_plan* p) {
     for (void* e : p->prof_events) (void)hipEventDestroy(static_cast<hipEvent_t>(e));

@@ -30,3 +30,9 @@ def test_binding_covers_every_declared_symbol():
     assert sorted(tkv.EXPORTED) == _declared()
     for name in _declared():
         assert callable(getattr(tkv, name)), name
+
+
+def test_noalloc_limit_matches_header():
+    src = open(HEADER).read()
+    m = re.search(r"#define TKV_NOALLOC_MAX_BYTES \(\(size_t\)(\d+) << (\d+)\)", src)
+    assert m and int(m.group(1)) << int(m.group(2)) == tkv.TKV_NOALLOC_MAX_BYTES
