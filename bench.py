@@ -70,13 +70,16 @@ def _args():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-sub-configs", action="store_true",
                     help="time only the headline workload (by default the mixed_serving headline is followed by "
-                         "beam_decode, step_verify and spec_explosion, reported under 'configs')")
+                         "beam_decode, step_verify, spec_explosion and spec_prompts, reported under 'configs')")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU baseline sample")
     ap.add_argument("--kv-copies", type=int, default=0,
                     help="device copies of the K/V pool rotated over the steps (0: enough to defeat the 256 MB MALL)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="JSON with per-launch HBM bytes of the main kernel from rocprofv3 counters (used only if "
                          "the kernel sources are unchanged since they were taken)")
+    ap.add_argument("--plan-options", default=None,
+                    help="placement options of the attention plan as JSON (tkv_plan_options fields), e.g. "
+                         "'{\"wave_max_rows\": 8}'")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one plain 256 MiB device-to-device copy first (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -558,6 +561,24 @@ def cpu_baseline(a, qbits, kbits, vbits, tables, bl, q_lens):
                       f"each), fp64 NumPy gather attention, {wall:.1f} s wall, {cpu_s:.1f} s CPU"}
 
 
+def shared_pass_flops(view, s):
+    """Algorithmic flops of the shared-prefix pass: the 128-row tile items over shared chunks (item
+    kind 0), each query token counted against the chunk keys its causal limit lets it see."""
+    items = view["items"].reshape(-1, 8).astype(np.int64)
+    toks = view["toks"].reshape(-1, 4).astype(np.int64)
+    blen = view["blks"].reshape(-1, 2)[:, 1].astype(np.int64)
+    g = s.hq // s.hkv
+    cum = np.concatenate([[0], np.cumsum(blen)])
+    total = 0
+    for kvh, to, nt, bo, nb, pos0, kind, _ in items:
+        if kind != 0:
+            continue
+        keys = cum[bo + nb] - cum[bo]
+        vis = np.clip(toks[to:to + nt, 1] - pos0 + 1, 0, keys)
+        total += int(vis.sum())
+    return total * g * 4 * s.d
+
+
 def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
     """Build the workload's tree on the library's block manager, coalesce and plan its measured
     launch, and time `steps` calls after `warmup` ones.  Returns the result fields."""
@@ -591,14 +612,18 @@ def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
     t_create = []                              # the host planner alone (what a decode loop pays per step)
     for _ in range(5):
         t0 = time.perf_counter()
-        h = tkv.tkv_plan_create((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, bl, mult)
+        h = tkv.tkv_plan_create_ex((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, bl, mult,
+                                   json.loads(a.plan_options) if a.plan_options else None)
         t_create.append(time.perf_counter() - t0)
         tkv.tkv_plan_destroy(h)
     t0 = time.perf_counter()
-    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, bl, mult, device=dev)
+    options = json.loads(a.plan_options) if a.plan_options else None
+    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, bl, mult, device=dev,
+                    options=options)
     torch.cuda.synchronize()
     t_plan = time.perf_counter() - t0
     st = plan.stats
+    f_shared = shared_pass_flops(plan.view(), s)
 
     # ------------------------------------------------------------------ device inputs
     kbits, vbits = wl.kv_values()
@@ -677,8 +702,10 @@ def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kernel,
                 "algorithmic_bytes": b_uniq, "kernel_us": round(t_main * 1e6, 2),
                 "frac_whole_call": round(b_uniq / t_call / 1e9 / HBM_PEAK_GBS, 4)}
+    shared = {"flops": f_shared, "frac_of_mfma_peak_over_attn_fwd": round(f_shared / t_main / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
     res = {
         "value": round(n_qtok / t_call, 1), "ms_per_step": round(ms_step, 5), "steps": steps, "warmup": warmup,
+        "shared_pass": shared,
         "config": {"workload": name, "hq": s.hq, "hkv": s.hkv, "head_dim": s.d, "block_size": s.block_size,
                    "rows": st["n_rows"], "query_tokens": n_qtok, "logical_candidate_tokens": st["logical_qtok"],
                    "decode": bool(L.decode), "unique_kv_bytes": b_uniq,
@@ -705,7 +732,7 @@ def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
     return res
 
 
-SUB_CONFIGS = ("beam_decode", "step_verify", "spec_explosion")
+SUB_CONFIGS = ("beam_decode", "step_verify", "spec_explosion", "spec_prompts")
 
 
 def main():
@@ -740,7 +767,7 @@ def main():
         "ms_per_step": head["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded trees, N(0,1) bf16 values)",
-        "config": head["config"],
+        "config": dict(head["config"], **({"plan_options": json.loads(a.plan_options)} if a.plan_options else {})),
         "roofline": head["roofline"],
         "cpu_baseline": head.get("cpu_baseline"),
         "hbm_frac_whole_call": head["hbm_frac_whole_call"],
@@ -749,7 +776,8 @@ def main():
         "unique_kv_frac_of_stream_copy": round(head["config"]["unique_kv_bytes"] / (head["kernel_us"]["attn_fwd"] / 1e6)
                                                / 1e9 / stream_gbs, 4),
         "logical_candidate_tokens_per_s": head["logical_candidate_tokens_per_s"],
-        "kernel_us": head["kernel_us"], "plan": head["plan"], "host_ms": head["host_ms"],
+        "kernel_us": head["kernel_us"], "shared_pass": head["shared_pass"], "plan": head["plan"],
+        "host_ms": head["host_ms"],
     }
     if "warm" in head:
         out["warm"] = head["warm"]
@@ -761,7 +789,8 @@ def main():
                           "rows": r["config"]["rows"], "query_tokens": r["config"]["query_tokens"],
                           "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "unit", "frac",
                                                                      "frac_whole_call", "kernel_us", "traffic")},
-                          "kernel_us": r["kernel_us"], "plan_create_ms": r["host_ms"]["plan_create_median"]}
+                          "kernel_us": r["kernel_us"], "shared_pass": r["shared_pass"],
+                          "plan_create_ms": r["host_ms"]["plan_create_median"]}
         out["configs"] = subs
     print(json.dumps(out))
 

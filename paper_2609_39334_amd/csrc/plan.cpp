@@ -125,6 +125,14 @@ void tile_evenly(int32_t n, int32_t cap, F f) {
     for (int32_t a = 0; a < n; a += per) f(a, std::min(n, a + per));
 }
 
+// Split n query tokens into full tiles of `cap` and one last partial tile.  A workgroup-kernel
+// tile costs MFMA time per active wave of 32 rows whatever the wave's fill, so full tiles leave
+// at most one partly filled wave per row (near-equal tiles leave one per tile).
+template <class F>
+void tile_full(int32_t n, int32_t cap, F f) {
+    for (int32_t a = 0; a < n; a += cap) f(a, std::min(n, a + cap));
+}
+
 }  // namespace
 
 TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
@@ -333,7 +341,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             const bool wave = G <= tkv::kWaveRows && rows <= wave_max_rows && c.n_blk <= kChunkBlocks;
             const int32_t T = static_cast<int32_t>(std::min<int64_t>(tkv::kWaveMaxTiles, (rows + 15) / 16));
             const int32_t per_tile = wave ? tkv::kWaveRows * T / G : tpt;
-            tile_evenly(static_cast<int32_t>(c.toks.size()), per_tile, [&](int32_t a, int32_t e) {
+            auto emit = [&](int32_t a, int32_t e) {
                 const int32_t tok_off = static_cast<int32_t>(p->toks.size());
                 p->toks.insert(p->toks.end(), c.toks.begin() + a, c.toks.begin() + e);
                 for (int32_t h = 0; h < s.hkv; ++h) {
@@ -341,7 +349,12 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                                      wave ? tkv::kItemWave : tkv::kItemShared, wave ? T : 0};
                     (wave ? p->wave_items : p->items).push_back(d);
                 }
-            });
+            };
+            // wave tiles balance the per-wave lists; 128-row tiles are filled (their cost is per wave)
+            if (wave)
+                tile_evenly(static_cast<int32_t>(c.toks.size()), per_tile, emit);
+            else
+                tile_full(static_cast<int32_t>(c.toks.size()), per_tile, emit);
         }
         st.n_items_shared = static_cast<int32_t>(p->items.size() + p->wave_items.size());
 
@@ -369,7 +382,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                 pos += block_len[kv_blocks[j]];
                 end_pos.push_back(pos);
             }
-            tile_evenly(L[r], tpt, [&](int32_t a, int32_t e) {
+            tile_full(L[r], tpt, [&](int32_t a, int32_t e) {
                 const int32_t max_lim = N[r] - L[r] + e - 1;
                 // blocks whose first position is <= max_lim
                 const int32_t nb = static_cast<int32_t>(std::upper_bound(end_pos.begin(), end_pos.end(), max_lim) - end_pos.begin()) + 1;

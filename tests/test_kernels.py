@@ -115,7 +115,7 @@ def test_verify_long_steps_and_single_token_rows():
     compare(wl, 0)
 
 
-@pytest.mark.parametrize("name", ["beam_decode", "step_verify"])
+@pytest.mark.parametrize("name", ["beam_decode", "step_verify", "spec_prompts"])
 def test_full_size_every_row(name):
     compare(W.CONFIGS[name](0), 0)
 
@@ -239,3 +239,4 @@ def test_small_verify_batches_on_both_tile_kernels(seed, hq, hkv, d, tile8_max):
     wl = _small_verify(seed, W.Shape(hq, hkv, d))
     b, st = compare(wl, 0, options={"tile8_max_items": tile8_max})
     assert st["n_items_wave"] == 0 and st["n_items_row"] > 0 and st["n_items"] == st["n_items_row"]
+

@@ -315,6 +315,27 @@ def spec_explosion(seed: int = 0, n_queries: int = 8) -> Workload:
     return wl.finalize()
 
 
+def spec_prompts(seed: int = 0, n_queries: int = 8, n_cands: int = 204) -> Workload:
+    """The shared-prefix pass of the speculative explosion on its own: 12 query heads, 2 KV heads,
+    head_dim 128.  Per query a prompt U{512..6144} (sealed), as in spec_explosion, shared by
+    n_cands candidates (about spec_explosion's distinct rows per query), each decoding one token of
+    its own (an unsealed 1-token step); prompts released; decode.  Every prompt block is read by
+    n_cands x 6 query rows per KV head, so the call's work is almost all the shared pass."""
+    rs, rt = _rngs(seed)
+    wl = Workload("spec_prompts", Shape(12, 2, 128), seed,
+                  note=f"{n_queries} queries x (prompt U{{512..6144}} shared by {n_cands} 1-token candidates)")
+    prompts, cands = [], []
+    for _ in range(n_queries):
+        p = wl.extend(-1, _toks(rt, rs.integers(512, 6145)), True)
+        prompts.append(p)
+        for _ in range(n_cands):
+            cands.append(wl.extend(p, _toks(rt, 1), False))
+    for h in prompts:
+        wl.prune(h)
+    wl.launch("decode", [(c, 1) for c in cands])
+    return wl.finalize()
+
+
 def mixed_serving(seed: int = 0, n_queries: int = 64) -> Workload:
     """Mixed serving batch: 32 query heads, 8 KV heads, head_dim 128.
     Per query: prompt U{256..2048}; U{4..64} candidates in sibling groups of 4, each group under a
@@ -360,6 +381,7 @@ CONFIGS = {
     "step_verify": step_verify,
     "spec_explosion": spec_explosion,
     "mixed_serving": mixed_serving,
+    "spec_prompts": spec_prompts,
 }
 
 
