@@ -203,9 +203,11 @@ int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_ind
  *   waves            size of the wave grid (default 2048, less the 4 waves of each workgroup slot
  *                    that the 128-row tiles take when they are fewer than the 512 slots; 0: default)
  *   tile8_max_items  a plan of at most this many tile items and no wave-grid work runs them as
- *                    8-wave workgroups (default 256) */
+ *                    8-wave workgroups (default 256)
+ *   wide_chunk_blocks  longest key run, in blocks, of a shared chunk on the 128-row tiles
+ *                    (default 64) */
 typedef struct {
-    int32_t wave_max_rows, tile_min_items, waves, tile8_max_items;
+    int32_t wave_max_rows, tile_min_items, waves, tile8_max_items, wide_chunk_blocks;
 } tkv_plan_options;
 
 /* tkv_plan_create with placement options (opts may be NULL: all defaults). */

@@ -34,7 +34,8 @@ class tkv_shape(ctypes.Structure):
 
 
 class tkv_plan_options(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("wave_max_rows", "tile_min_items", "waves", "tile8_max_items")]
+    _fields_ = [(n, ctypes.c_int32) for n in ("wave_max_rows", "tile_min_items", "waves", "tile8_max_items",
+                                              "wide_chunk_blocks")]
 
 
 class tkv_plan_stats(ctypes.Structure):

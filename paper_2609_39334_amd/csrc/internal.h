@@ -34,6 +34,8 @@ constexpr int kWaveToks = 48;   // token slots of a wave-kernel record (>= 16 kW
 constexpr int kWaveWorkers = 2048;  // waves of the wave kernel: 2 workgroups of kWaveWG on each of 256 CUs
 constexpr int kWaveWG = 4;      // waves per workgroup of the wave kernel (independent; no barriers)
 constexpr int kTile8MaxItems = 256;  // tile items (and no wave grid) up to which 8-wave workgroups run them: one per CU
+constexpr int kInterleaveRun = 32;   // workgroups per run when tile items and wave-grid workgroups alternate:
+                                     // 8 XCDs x 4 shader engines, one workgroup of a kind per engine
 
 // One work item: a tile of query tokens (each with all G query heads of one KV
 // head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the

@@ -278,6 +278,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         // gives up the workgroup slots the tile items take); otherwise everything with G <= 16
         // stays on the wave grid.
         int64_t wave_max_rows = opt(&tkv_plan_options::wave_max_rows, tkv::kWaveMaxRows);
+        const int32_t chunk_wide = static_cast<int32_t>(std::max<int64_t>(1, opt(&tkv_plan_options::wide_chunk_blocks, kChunkBlocksWide)));
         if (G <= tkv::kWaveRows) {
             int64_t wide_items = 0;
             for (const Segment& sg : segs) {
@@ -285,7 +286,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                 for (int32_t r : sg.rows) seg_tok += L[r];
                 if (seg_tok * G <= wave_max_rows) continue;
                 const int64_t nb = static_cast<int64_t>(sg.nodes.size());
-                wide_items += (nb + kChunkBlocksWide - 1) / kChunkBlocksWide * ((seg_tok + tpt - 1) / tpt) * s.hkv;
+                wide_items += (nb + chunk_wide - 1) / chunk_wide * ((seg_tok + tpt - 1) / tpt) * s.hkv;
             }
             const int64_t min_items = opt(&tkv_plan_options::tile_min_items, tkv::kTileMinItems);
             if (wide_items < min_items) wave_max_rows = int64_t{1} << 40;
@@ -302,7 +303,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             int64_t seg_rows = 0;
             for (int32_t r : sg.rows) seg_rows += static_cast<int64_t>(L[r]) * G;
             const bool wide = G > tkv::kWaveRows || seg_rows > wave_max_rows;
-            tile_evenly(nb, wide ? kChunkBlocksWide : kChunkBlocks, [&](int32_t a, int32_t e) {
+            tile_evenly(nb, wide ? chunk_wide : kChunkBlocks, [&](int32_t a, int32_t e) {
                 Chunk c;
                 c.blk_off = seg_blk_off + a;
                 c.n_blk = e - a;
