@@ -982,9 +982,6 @@ static int launch_ws(const tkv_plan* p, uint8_t* ws, const void* q, const void* 
 
 int launch_attention(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
                      void* stream) {
-    if (!p->d_ws) return set_error(TKV_EINVAL, "attention: plan has not been uploaded");
-    if (p->items.empty() && p->wave_items.empty()) return TKV_OK;
-    if (!q || !k || !v || !o) return set_error(TKV_EINVAL, "attention: NULL tensor pointer");
     return launch_ws(p, static_cast<uint8_t*>(p->d_ws), q, k, v, o, lse, static_cast<hipStream_t>(stream));
 }
 

@@ -122,7 +122,8 @@ namespace tkv {
 // step then writes into memory that is already mapped.  take_image returns at least `bytes`.
 std::unique_ptr<uint8_t[]> take_image(size_t bytes, size_t* cap);
 void give_image(std::unique_ptr<uint8_t[]> image, size_t cap);
-// Launchers (attn.hip).
+// Launchers (attn.hip).  launch_attention: an uploaded plan with work and non-NULL tensors (the
+// entry points check these first).
 int launch_attention(const tkv_plan* p, const void* q, const void* k, const void* v, void* o,
                      float* lse, void* stream);
 int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream);

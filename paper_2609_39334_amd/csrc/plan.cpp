@@ -813,17 +813,26 @@ TKV_EXPORT int tkv_plan_upload(tkv_plan* p, void* d_ws, size_t bytes, void* stre
     return tkv::upload(p, d_ws, bytes, stream);
 }
 
+// The checks of an attention call before anything is enqueued; then the launch (attn.hip).
+static int attention_call(const char* fn, const tkv_plan* p, const void* q, const void* k, const void* v, void* o,
+                          float* lse, void* stream) {
+    if (!p->d_ws) return set_error(TKV_EINVAL, "%s: plan has not been uploaded", fn);
+    if (p->items.empty() && p->wave_items.empty()) return TKV_OK;
+    if (!q || !k || !v || !o) return set_error(TKV_EINVAL, "%s: NULL tensor pointer", fn);
+    return tkv::launch_attention(p, q, k, v, o, lse, stream);
+}
+
 TKV_EXPORT int tkv_decode(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
                           void* stream) {
     tkv::clear_error();
     if (!p) return set_error(TKV_EINVAL, "tkv_decode: plan is NULL");
     if (!p->all_decode) return set_error(TKV_EINVAL, "tkv_decode: every row must have q_len 1 (use tkv_verify)");
-    return tkv::launch_attention(p, q, k, v, o, lse, stream);
+    return attention_call("tkv_decode", p, q, k, v, o, lse, stream);
 }
 
 TKV_EXPORT int tkv_verify(const tkv_plan* p, const void* q, const void* k, const void* v, void* o, float* lse,
                           void* stream) {
     tkv::clear_error();
     if (!p) return set_error(TKV_EINVAL, "tkv_verify: plan is NULL");
-    return tkv::launch_attention(p, q, k, v, o, lse, stream);
+    return attention_call("tkv_verify", p, q, k, v, o, lse, stream);
 }
