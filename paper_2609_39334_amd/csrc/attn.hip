@@ -51,6 +51,19 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> packed fp16 pair, round to nearest even (the partial results' storage type).
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, f16x2_t));
+}
+
+__device__ __forceinline__ float4 unpack_f16x4(uint2 u) {
+    const f32x2_t a = __builtin_convertvector(__builtin_bit_cast(f16x2_t, u.x), f32x2_t);
+    const f32x2_t b = __builtin_convertvector(__builtin_bit_cast(f16x2_t, u.y), f32x2_t);
+    return make_float4(a[0], a[1], b[0], b[1]);
+}
+
 // acc + lo + hi of a packed bf16 pair, in fp32 (v_dot2_f32_bf16 against the pair (1, 1)).
 __device__ __forceinline__ float sum_bf16x2(uint32_t p, float acc) {
     const bf16x2_t one{static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
@@ -281,12 +294,12 @@ __device__ __forceinline__ void stage_base(WaveAcc<D, T>& A, const f32x4_t (&sc)
 }
 
 // Normalise one column tile's rows and write them: the final bf16 output and lse (slot < 0) or an
-// fp32 partial and its lse.  Lane holds columns 16ct + 4kg + r of its row; l is summed over the
+// fp16 partial and its fp32 lse.  Lane holds columns 16ct + 4kg + r of its row; l is summed over the
 // four lanes of the row.
 template <int D>
 __device__ __forceinline__ void write_rows(const f32x4_t (&acc)[D / 16], float m, float l, bool ok, int qtok, int h,
                                            int slot, int kg, uint16_t* __restrict__ o, float* __restrict__ lse,
-                                           float* __restrict__ po, float* __restrict__ plse, int hq, float sl2) {
+                                           uint16_t* __restrict__ po, float* __restrict__ plse, int hq, float sl2) {
     float l_tot = l + __shfl_xor(l, 16);
     l_tot += __shfl_xor(l_tot, 32);
     if (!ok) return;
@@ -303,11 +316,14 @@ __device__ __forceinline__ void write_rows(const f32x4_t (&acc)[D / 16], float m
         }
         if (lse && kg == 0) lse[static_cast<size_t>(qtok) * hq + h] = lse_v;
     } else {
-        float* prow = po + (static_cast<size_t>(slot) * hq + h) * D;
+        uint16_t* prow = po + (static_cast<size_t>(slot) * hq + h) * D;
 #pragma unroll
-        for (int ct = 0; ct < D / 16; ++ct)
-            *reinterpret_cast<float4*>(prow + ct * 16 + kg * 4) =
-                make_float4(acc[ct][0] * inv, acc[ct][1] * inv, acc[ct][2] * inv, acc[ct][3] * inv);
+        for (int ct = 0; ct < D / 16; ++ct) {
+            uint2 wv;
+            wv.x = pack_f16x2(acc[ct][0] * inv, acc[ct][1] * inv);
+            wv.y = pack_f16x2(acc[ct][2] * inv, acc[ct][3] * inv);
+            *reinterpret_cast<uint2*>(prow + ct * 16 + kg * 4) = wv;
+        }
         if (kg == 0) plse[static_cast<size_t>(slot) * hq + h] = lse_v;
     }
 }
@@ -390,7 +406,7 @@ template <int D, int T>
 __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, const WaveList& L,
                                               const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
                                               const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
-                                              float* __restrict__ lse, float* __restrict__ po,
+                                              float* __restrict__ lse, uint16_t* __restrict__ po,
                                               float* __restrict__ plse, int hq, int hkv, int G, float sl2,
                                               uint8_t* vs, int lane) {
     constexpr int VROW = 2 * D + 32;
@@ -514,7 +530,7 @@ __device__ __forceinline__ void wave_worker(int w, int lane, const int4* __restr
                                             const int32_t* __restrict__ woff, const int32_t* __restrict__ wtiles,
                                             const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
                                             const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o,
-                                            float* __restrict__ lse, float* __restrict__ po, float* __restrict__ plse,
+                                            float* __restrict__ lse, uint16_t* __restrict__ po, float* __restrict__ plse,
                                             int hq, int hkv, int G, float sl2, uint8_t* vs) {
     const int T = wtiles[w];
     if (T == 0) return;
@@ -597,7 +613,7 @@ template <int D, int T>
 __device__ __forceinline__ void tile_item(const tkv::ItemDesc& it, const tkv::TokDesc* __restrict__ toks,
                                           const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q,
                                           const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-                                          uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
+                                          uint16_t* __restrict__ o, float* __restrict__ lse, uint16_t* __restrict__ po,
                                           float* __restrict__ plse, int hq, int hkv, int G, float sl2, uint8_t* k0,
                                           uint8_t* v0, uint8_t* k1, uint8_t* v1) {
     constexpr int RB = 2 * D;  // bytes per K/V row in the stage buffers
@@ -786,7 +802,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const tkv::ItemDesc* __restrict__ items, int n_tile, int n_wave_wg, int runs, const tkv::TokDesc* __restrict__ toks,
     const tkv::BlkDesc* __restrict__ blks, const int4* __restrict__ wdesc, const int32_t* __restrict__ woff,
     const int32_t* __restrict__ wtiles, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
-    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
+    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, uint16_t* __restrict__ po,
     float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
     // the tile path's two stage buffers of K and V; the wave grid gives one of the four to each wave
     __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[tile_buf_bytes<D>()];
@@ -831,7 +847,7 @@ template <int D>
 __global__ __launch_bounds__(2 * kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_tile8(
     const tkv::ItemDesc* __restrict__ items, int n_tile, const tkv::TokDesc* __restrict__ toks,
     const tkv::BlkDesc* __restrict__ blks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
-    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ po,
+    const uint16_t* __restrict__ vpool, uint16_t* __restrict__ o, float* __restrict__ lse, uint16_t* __restrict__ po,
     float* __restrict__ plse, int hq, int hkv, int G, float sl2) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[tile_buf_bytes<D>()];
     __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[tile_buf_bytes<D>()];
@@ -844,19 +860,19 @@ __global__ __launch_bounds__(2 * kThreads) __attribute__((amdgpu_waves_per_eu(2,
 }
 
 // Log-sum-exp merge of one query token's partials (one workgroup per token, whose partial slots
-// are contiguous, sized to one thread per float4 column of the token's heads): every thread folds
+// are contiguous, sized to one thread per four columns of the token's heads): every thread folds
 // the partials of its column in with an online softmax, eight partials' outputs and lse values in
 // flight at a time -- one round of memory latency per eight partials, no barriers.
 template <int D>
 __global__ __launch_bounds__(1024) void merge_partials(const tkv::MergeDesc* __restrict__ md,
-                                                           const float* __restrict__ po,
+                                                           const uint16_t* __restrict__ po,
                                                            const float* __restrict__ plse,
                                                            uint16_t* __restrict__ o, float* __restrict__ lse, int hq) {
     constexpr int C4 = D / 4;
     const tkv::MergeDesc m = md[blockIdx.x];
     const size_t s0 = static_cast<size_t>(m.slot_off);
     const int n = m.n_slots;
-    const float4* po4 = reinterpret_cast<const float4*>(po);
+    const uint2* po4 = reinterpret_cast<const uint2*>(po);  // four fp16 columns
     for (int idx = threadIdx.x; idx < hq * C4; idx += blockDim.x) {
         const int h = idx / C4;
         float mx = -INFINITY, sum = 0.f;
@@ -867,7 +883,7 @@ __global__ __launch_bounds__(1024) void merge_partials(const tkv::MergeDesc* __r
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
                 const size_t sl = s0 + min(j0 + v, n - 1);
-                x[v] = po4[(sl * hq) * C4 + idx];
+                x[v] = unpack_f16x4(po4[(sl * hq) * C4 + idx]);
                 lj[v] = j0 + v < n ? plse[sl * hq + h] : -INFINITY;
             }
             float cm = lj[0];
@@ -927,7 +943,7 @@ static int launch_d(const tkv_plan* p, uint8_t* ws, const void* q, const void* k
     const auto* wtiles = reinterpret_cast<const int32_t*>(ws + p->off_wtiles);
     const auto* toks = reinterpret_cast<const TokDesc*>(ws + p->off_toks);
     const auto* blks = reinterpret_cast<const BlkDesc*>(ws + p->off_blks);
-    float* po = reinterpret_cast<float*>(ws + p->off_po);
+    uint16_t* po = reinterpret_cast<uint16_t*>(ws + p->off_po);
     float* plse = reinterpret_cast<float*>(ws + p->off_plse);
     const float sl2 = 1.4426950408889634f / std::sqrt(static_cast<float>(D));
     const int hq = p->shape.hq, hkv = p->shape.hkv;
@@ -964,7 +980,7 @@ static int launch_d(const tkv_plan* p, uint8_t* ws, const void* q, const void* k
         const int merge_threads = std::min(1024, (hq * (D / 4) + 63) / 64 * 64);
         hipExtLaunchKernelGGL(merge_partials<D>, dim3(static_cast<unsigned>(p->merges.size())), dim3(merge_threads), 0, st,
                               ev ? ev[2] : nullptr, ev ? ev[3] : nullptr, 0, merges,
-                              static_cast<const float*>(po), static_cast<const float*>(plse),
+                              static_cast<const uint16_t*>(po), static_cast<const float*>(plse),
                               static_cast<uint16_t*>(o), lse, hq);
         e = hipGetLastError();
         if (e != hipSuccess) return set_error(TKV_EHIP, "merge launch: %s", hipGetErrorString(e));

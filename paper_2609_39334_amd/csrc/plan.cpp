@@ -665,7 +665,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         off = align256(off + bytes(p->wave_tiles.size(), sizeof(int32_t)));
         p->desc_bytes = off;
         p->off_po = off;
-        off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq * s.d, sizeof(float)));
+        off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq * s.d, sizeof(uint16_t)));  // fp16 partial o
         p->off_plse = off;
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq, sizeof(float)));
         p->total_bytes = std::max<size_t>(off, 256);
