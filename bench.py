@@ -579,6 +579,54 @@ def shared_pass_flops(view, s):
     return total * g * 4 * s.d
 
 
+def time_plan_updates(wl, steps=48, seed=0):
+    """Host cost of a decode loop's planning: the workload's measured launch on a block manager with
+    room to grow, then `steps` decode steps (one token more for every candidate, a new block when
+    its last is full), each followed by tkv_plan_update of one plan.  A fresh tkv_plan_create of the
+    same tables is timed every eighth step for comparison.  Host only; no device memory."""
+    import paper_2609_39334_amd as tkv
+    import workloads as W
+    s = wl.shape
+    nb = wl.num_blocks + 8192
+    bm = tkv.BlockManager(nb, s.block_size, wl.max_seqs)
+    cap = {}
+    W.drive(wl, bm, on_launch=lambda i, l, c: cap.__setitem__(i, (l, c)))
+    _, cands = cap[len(wl.launches) - 1]
+    seqs = [x for x, _ in cands]
+    qls = [q for _, q in cands]
+    _, first, mult = bm.coalesce(seqs, qls)
+    rows = [seqs[c] for c in first]
+    qi = np.concatenate([[0], np.cumsum([qls[c] for c in first])]).astype(np.int32)
+    shape = (s.hq, s.hkv, s.d, s.block_size, nb)
+
+    def tables():
+        t = [bm.table(x) for x in rows]
+        return (np.concatenate([[0], np.cumsum([len(x) for x in t])]).astype(np.int32),
+                np.concatenate(t).astype(np.int32), bm.block_len())
+
+    h = tkv.tkv_plan_create(shape, qi, *tables(), mult)
+    rng = np.random.default_rng(seed)
+    t_upd, in_place, t_create = [], 0, []
+    try:
+        for k in range(steps):
+            for x in rows:
+                bm.append(x, rng.integers(0, 1 << 15, 1).astype(np.int32))
+            ki, kb, bl = tables()
+            t0 = time.perf_counter()
+            in_place += tkv.tkv_plan_update(h, ki, kb, bl)
+            t_upd.append(time.perf_counter() - t0)
+            if k % 8 == 0:
+                t0 = time.perf_counter()
+                h2 = tkv.tkv_plan_create(shape, qi, ki, kb, bl, mult)
+                t_create.append(time.perf_counter() - t0)
+                tkv.tkv_plan_destroy(h2)
+    finally:
+        tkv.tkv_plan_destroy(h)
+    return {"decode_steps": steps, "plan_update_median": round(float(np.median(t_upd)) * 1e3, 4),
+            "plan_update_mean": round(float(np.mean(t_upd)) * 1e3, 4), "updates_in_place": in_place,
+            "plan_create_median_same_tables": round(float(np.median(t_create)) * 1e3, 3)}
+
+
 def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
     """Build the workload's tree on the library's block manager, coalesce and plan its measured
     launch, and time `steps` calls after `warmup` ones.  Returns the result fields."""
@@ -727,6 +775,8 @@ def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
     if ms_step_warm is not None:
         res["warm"] = {"ms_per_step": round(ms_step_warm, 5), "value": round(n_qtok / (ms_step_warm / 1e3), 1),
                        "kv_pool_fits_mall": pool_bytes <= MALL_BYTES}
+    if L.decode:
+        res["host_ms"]["decode_loop"] = time_plan_updates(wl)
     if with_cpu:
         res["cpu_baseline"] = cpu_baseline(a, qbits, kbits, vbits, tables, bl, q_lens)
     return res
@@ -791,6 +841,8 @@ def main():
                                                                      "frac_whole_call", "kernel_us", "traffic")},
                           "kernel_us": r["kernel_us"], "shared_pass": r["shared_pass"],
                           "plan_create_ms": r["host_ms"]["plan_create_median"]}
+            if "decode_loop" in r["host_ms"]:
+                subs[name]["decode_loop_host_ms"] = r["host_ms"]["decode_loop"]
         out["configs"] = subs
     print(json.dumps(out))
 

@@ -227,12 +227,47 @@ int tkv_plan_upload(tkv_plan* plan, void* d_workspace, size_t bytes, void* hip_s
 
 void tkv_plan_destroy(tkv_plan* plan);
 
+/* Bring a plan to new block tables for the same rows (same count, order, q_len and multiplicity
+ * as at creation), as a decode loop needs after every step: kv_indptr[n_rows+1], kv_blocks and
+ * block_len[num_blocks] as for tkv_plan_create.
+ *   - In place (*in_place = 1: a scan of the tables and of block_len, no planning) when every
+ *     row kept its blocks and at most appended new ones (ids in no table before), and the blocks
+ *     that changed length
+ *     are the last blocks of decode rows (q_len 1) whose path ends in a chunk of their own on the
+ *     wave kernel (the blocks a decode step writes).  The new blocks fill that chunk up to 16
+ *     blocks; one more chunk per row may open (its partial goes to a slot the plan keeps free for
+ *     the row, its work to one of the plan's idle waves).  The plan then does exactly the work of
+ *     a plan made from the new tables -- the same items, blocks, tokens, partial slots in path
+ *     order and merges, so the same results bit for bit -- but keeps its wave assignment: where
+ *     only lengths changed its image equals that plan's byte for byte.
+ *   - Otherwise (*in_place = 0) the plan is made again from the new tables, as tkv_plan_create
+ *     would (its options kept); its workspace size may change.
+ * Either way the plan must be uploaded again before the next attention call (EINVAL until then).
+ * in_place may be NULL.  Errors (the plan is then unchanged): EINVAL (NULL arguments, or what
+ * tkv_plan_create rejects in the new tables), ENOMEM. */
+int tkv_plan_update(tkv_plan* plan, const int32_t* kv_indptr, const int32_t* kv_blocks,
+                    const int32_t* block_len, int32_t* in_place);
+
+/* The plan's host descriptor image, what tkv_plan_upload copies (valid until the plan is updated
+ * or destroyed; for tests and tools), and where its sections start, in bytes: tile items, their
+ * tokens and blocks (the tkv_plan_get_view formats), merge entries, merge slot list, the wave
+ * items' 1-KB records (one 16-byte word per lane: words 0-15 the key blocks {id, length,
+ * position, header word}, header words KV head, token count, walked block count; words 16-63 the
+ * tokens {query token, causal limit, slot, 0}), each wave's further records [off[w], off[w+1])
+ * (int32, n_waves + 1), each wave's column tiles (int32, 0: no work); `end` = bytes uploaded.
+ * Wave w runs record w, then its further records. */
+typedef struct {
+    size_t items, toks, blks, merges, merge_slots, wave_records, wave_off, wave_tiles, end;
+} tkv_plan_layout;
+int tkv_plan_image(const tkv_plan* plan, const void** data, tkv_plan_layout* layout);
+
 /* Counts for accounting and tests. */
 typedef struct {
     int32_t n_rows, n_qtok, n_items, n_items_shared, n_items_row, n_slots, n_merge;
     int32_t n_segments, n_shared_segments;
     int32_t n_items_wave;   /* items run by the wave kernel (a subset of the shared items) */
     int32_t n_waves;        /* waves of the wave kernel */
+    int32_t n_idle_waves;   /* of those, waves with no work (kept for tkv_plan_update) */
     int64_t logical_qtok;   /* sum of multiplicity * q_len */
     int64_t uniq_kv_tokens; /* tokens in the union of the rows' blocks */
     int64_t path_kv_tokens; /* sum over rows of kv_len (what per-row gathering would read) */
@@ -240,12 +275,13 @@ typedef struct {
 } tkv_plan_stats;
 int tkv_plan_get_stats(const tkv_plan* plan, tkv_plan_stats* out);
 
-/* Read-only view of the plan's host descriptor arrays (valid until tkv_plan_destroy), for tests
- * and tools.  Formats (int32 words):
+/* Read-only view of the plan's host descriptor arrays (valid until the plan is viewed again,
+ * updated or destroyed), for tests and tools.  Formats (int32 words):
  *   items[n_items][8]  {kv_head, tok_off, n_tok, blk_off, n_blk, pos0, kind, tiles}: kind 0 shared
  *                      chunk (workgroup kernel), 1 whole-path row tile, 2 shared chunk on the wave
  *                      kernel with `tiles` column tiles of 16 query rows (0 for kinds 0 and 1)
- *   toks[n_toks][4]    {query token, largest visible key position, partial slot or -1, 0}
+ *   toks[n_toks][4]    {query token, largest visible key position (2^30 for a q_len-1 token,
+ *                      which sees its whole path), partial slot or -1, 0}
  *   blks[n_blks][2]    {block id, block length}
  *   merges[n_merge][4] {query token, offset into merge_slots, slot count, 0}
  * An item contracts the G query heads of KV head kv_head of toks[tok_off .. +n_tok) against the

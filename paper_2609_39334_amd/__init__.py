@@ -41,8 +41,13 @@ class tkv_plan_options(ctypes.Structure):
 class tkv_plan_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("n_rows", "n_qtok", "n_items", "n_items_shared", "n_items_row",
                                               "n_slots", "n_merge", "n_segments", "n_shared_segments",
-                                              "n_items_wave", "n_waves")] + \
+                                              "n_items_wave", "n_waves", "n_idle_waves")] + \
                [(n, ctypes.c_int64) for n in ("logical_qtok", "uniq_kv_tokens", "path_kv_tokens", "flops")]
+
+
+class tkv_plan_layout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in ("items", "toks", "blks", "merges", "merge_slots", "wave_records",
+                                               "wave_off", "wave_tiles", "end")]
 
 
 class tkv_plan_view(ctypes.Structure):
@@ -75,6 +80,8 @@ _SIG = {
                                           ctypes.POINTER(tkv_plan_options), ctypes.POINTER(_P)]),
     "tkv_plan_workspace_bytes": (ctypes.c_size_t, [_P]),
     "tkv_plan_upload": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P]),
+    "tkv_plan_update": (ctypes.c_int, [_P, _P, _P, _P, ctypes.POINTER(ctypes.c_int32)]),
+    "tkv_plan_image": (ctypes.c_int, [_P, ctypes.POINTER(_P), ctypes.POINTER(tkv_plan_layout)]),
     "tkv_plan_destroy": (None, [_P]),
     "tkv_plan_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_stats)]),
     "tkv_plan_get_view": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_view)]),
@@ -314,6 +321,24 @@ def tkv_plan_upload(plan: int, workspace: torch.Tensor, stream=None) -> None:
 
 def tkv_plan_destroy(plan: int) -> None:
     lib().tkv_plan_destroy(plan)
+
+
+def tkv_plan_update(plan: int, kv_indptr, kv_blocks, block_len) -> bool:
+    """Bring the plan to new tables for the same rows; True if it was patched in place, False if
+    it was planned again.  It must be uploaded again either way."""
+    ki, kb, bl = _i32(kv_indptr), _i32(kv_blocks), _i32(block_len)
+    flag = ctypes.c_int32(0)
+    _check(lib().tkv_plan_update(plan, _ptr(ki), _ptr(kb) if len(kb) else None, _ptr(bl), ctypes.byref(flag)))
+    return bool(flag.value)
+
+
+def tkv_plan_image(plan: int):
+    """A copy of the plan's host descriptor image (what tkv_plan_upload copies) and the byte
+    offsets of its sections: (bytes, dict)."""
+    data, lay = _P(), tkv_plan_layout()
+    _check(lib().tkv_plan_image(plan, ctypes.byref(data), ctypes.byref(lay)))
+    layout = {f: int(getattr(lay, f)) for f, _ in tkv_plan_layout._fields_}
+    return (ctypes.string_at(data.value, layout["end"]) if layout["end"] else b""), layout
 
 
 def tkv_plan_get_stats(plan: int) -> dict:
@@ -570,6 +595,20 @@ class Plan:
     @property
     def stats(self):
         return tkv_plan_get_stats(self.h)
+
+    def update(self, kv_indptr, kv_blocks, block_len, stream=None) -> bool:
+        """tkv_plan_update, then (for an uploaded plan) the upload again, into a larger workspace
+        if the plan now needs one.  Returns whether the plan was patched in place."""
+        in_place = tkv_plan_update(self.h, kv_indptr, kv_blocks, block_len)
+        if self.workspace is not None:
+            nbytes = tkv_plan_workspace_bytes(self.h)
+            if nbytes > self.workspace.numel():
+                self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.workspace.device)
+            tkv_plan_upload(self.h, self.workspace, stream)
+        return in_place
+
+    def image(self) -> bytes:
+        return tkv_plan_image(self.h)
 
     def view(self):
         return tkv_plan_get_view(self.h)

@@ -36,6 +36,7 @@ constexpr int kWaveWG = 4;      // waves per workgroup of the wave kernel (indep
 constexpr int kTile8MaxItems = 256;  // tile items (and no wave grid) up to which 8-wave workgroups run them: one per CU
 constexpr int kInterleaveRun = 32;   // workgroups per run when tile items and wave-grid workgroups alternate:
                                      // 8 XCDs x 4 shader engines, one workgroup of a kind per engine
+constexpr int32_t kNoLimit = 1 << 30;  // causal limit of a q_len-1 token: it sees its whole path (kv_len <= 2^30)
 
 // One work item: a tile of query tokens (each with all G query heads of one KV
 // head) contracted against an ordered list of KV blocks.  Every query token of the tile sees the
@@ -66,7 +67,7 @@ struct BlkDesc {
 // A wave-kernel item as one 1-KB record that a wave loads with one 16-byte load per lane (lane l
 // gets e[l]); block fields come out with v_readlane, token fields with ds_bpermute.
 //   e[j]      (j < 16): {pool block id, length, path position, header word j} of key block j
-//                       (block 0's id and length 0 past the item's blocks); header words:
+//                       ({block 0's id, 0, 0} past the item's blocks); header words:
 //                       0 KV head, 1 tile tokens, 2 key blocks (rounded up to even for tile widths
 //                       1 and 2, whose waves walk blocks in pairs)
 //   e[16 + t] (t < 48): {query token, causal limit, partial slot (-1: final output), 0} of tile
@@ -82,6 +83,25 @@ struct MergeDesc {
     int32_t pad;
 };
 
+// What tkv_plan_update needs beyond the plan itself: the inputs the plan was made from (to check
+// that tables only grew, and to plan again when they did not grow in place) and, per row, its tail
+// chunk -- the last chunk of a decode row's private segment when the wave kernel runs it.
+struct PlanInputs {
+    std::vector<int32_t> q_indptr, kv_indptr, kv_blocks, block_len, mult;
+    tkv_plan_options opts{};
+    bool has_opts = false;
+    std::vector<int32_t> kv_len;     // [n_rows]
+    std::vector<int32_t> tail_run;   // [n_rows] wblks run (index / kWaveBlocks) of the tail chunk, or -1
+    std::vector<int32_t> spare;      // [n_rows] 1: the token's partial range ends in an unused slot
+    std::vector<int32_t> merge_of;   // [n_rows] the token's MergeDesc, or -1
+    // built on the first in-place update
+    bool indexed = false;
+    std::vector<int32_t> owner;      // [num_blocks] the one row whose table holds the block, -1 none, -2 several
+    std::vector<int32_t> run_items;  // [n_runs * hkv] wave items of each tail run, by KV head (-1: none)
+    std::vector<int32_t> rec_of;     // [n wave items] record index
+    std::vector<int32_t> free_waves; // idle waves (first records unused), taken from the back
+};
+
 }  // namespace tkv
 
 // ------------------------------------------------------------------ plan (host)
@@ -92,8 +112,12 @@ struct tkv_plan {
     std::vector<tkv::ItemDesc> items;       // workgroup-kernel items
     std::vector<tkv::ItemDesc> wave_items;  // wave-kernel items, longest first
     std::vector<tkv::ItemDesc> view_items;  // items then wave_items (tkv_plan_get_view)
-    std::vector<tkv::TokDesc> toks;
-    std::vector<tkv::BlkDesc> blks;
+    std::vector<tkv::TokDesc> view_toks;    // toks then wtoks
+    std::vector<tkv::BlkDesc> view_blks;    // blks then wblks
+    std::vector<tkv::TokDesc> toks;         // tile items' tokens (device image)
+    std::vector<tkv::BlkDesc> blks;         // tile items' key blocks (device image)
+    std::vector<tkv::TokDesc> wtoks;        // wave items' tokens (host: the records carry them)
+    std::vector<tkv::BlkDesc> wblks;        // wave chunks' key blocks, kWaveBlocks slots per chunk (host)
     std::vector<tkv::MergeDesc> merges;
     std::vector<int32_t> merge_slots;
     std::vector<int32_t> wave_rec;            // wave-kernel records, as the wave item each holds (-1: none):
@@ -110,6 +134,7 @@ struct tkv_plan {
     size_t image_cap = 0;              // bytes allocated for it (returned to the image pool on destroy)
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)
     tkv_plan_stats stats{};
+    std::unique_ptr<tkv::PlanInputs> in;  // for tkv_plan_update
     // instrumentation: 3 HIP events per recorded call (see tkv_plan_profile)
     mutable int32_t prof_max = 0;
     mutable int32_t prof_n = 0;

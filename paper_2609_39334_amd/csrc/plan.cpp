@@ -48,6 +48,47 @@ static_assert(kChunkBlocks <= tkv::kWaveBlocks, "a wave item holds its key block
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// The block slots of a wave item's record (see tkv::WaveDesc): {id, length, path position} of each
+// key block, {block 0's id, 0, 0} past the item's blocks (a length-0 block hides all its keys,
+// wherever it sits); the fourth words of slots 0-2 carry the KV head, the token count and the
+// walked block count.
+void write_record_blocks(const tkv_plan* p, const ItemDesc& it, int32_t* e) {
+    // widths 1 and 2 walk blocks in pairs: an odd key list gets an empty block
+    const int32_t nb_run = it.pad <= 2 ? (it.n_blk + 1) & ~1 : it.n_blk;
+    int32_t pos = it.pos0;
+    for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
+        const bool in = j < it.n_blk;
+        const BlkDesc& bd = p->wblks[it.blk_off + (in ? j : 0)];
+        e[4 * j] = bd.blk;
+        e[4 * j + 1] = in ? bd.len : 0;
+        e[4 * j + 2] = in ? pos : 0;
+        e[4 * j + 3] = 0;
+        if (in) pos += bd.len;
+    }
+    e[3] = it.kvh;
+    e[7] = it.n_tok;
+    e[11] = nb_run;
+}
+
+// A wave item's whole 1-KB record, written in place (zero for item < 0): its block slots, then 48
+// token slots {query token, causal limit, partial slot, 0}, token 0's past the tile.
+void write_record(const tkv_plan* p, int32_t item, uint8_t* dst) {
+    if (item < 0) {
+        std::memset(dst, 0, sizeof(tkv::WaveDesc));
+        return;
+    }
+    const ItemDesc& it = p->wave_items[item];
+    int32_t* e = reinterpret_cast<int32_t*>(dst);
+    write_record_blocks(p, it, e);
+    for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
+        const TokDesc& td = p->wtoks[it.tok_off + (t < it.n_tok ? t : 0)];
+        e[4 * (16 + t)] = td.qtok;
+        e[4 * (16 + t) + 1] = td.limit;
+        e[4 * (16 + t) + 2] = td.slot;
+        e[4 * (16 + t) + 3] = 0;
+    }
+}
+
 struct Node {
     int32_t parent, blk, len, pos0, count, seg;
 };
@@ -58,9 +99,14 @@ struct Segment {
 };
 
 struct Chunk {
-    int32_t blk_off, n_blk, pos0;
-    std::vector<TokDesc> toks;  // slot filled in later
+    int32_t blk_off, n_blk, pos0;  // blk_off: into the segments' block runs
+    bool wave;                     // run by the wave kernel
+    std::vector<TokDesc> toks;     // slot filled in later
 };
+
+// Idle waves a plan keeps for the chunks its decode tails open later (tkv_plan_update): one per
+// eight (row, KV head) tails, a multiple of kWaveWG, at most kMaxSpareWaves.
+constexpr int32_t kMaxSpareWaves = 512;
 
 // Dense ids for 64-bit keys in first-insertion order (open addressing, linear probing, grown at half
 // load).  Keys never equal ~0.
@@ -194,6 +240,28 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
     try {
         p->shape = s;
         p->group = G;
+        p->in.reset(new tkv::PlanInputs());
+        tkv::PlanInputs& in = *p->in;
+        if (n_rows > 0) {
+            in.q_indptr.assign(q_indptr, q_indptr + n_rows + 1);
+            in.kv_indptr.assign(kv_indptr, kv_indptr + n_rows + 1);
+            in.kv_blocks.assign(kv_blocks, kv_blocks + kv_indptr[n_rows]);
+            in.block_len.assign(block_len, block_len + s.num_blocks);
+            if (multiplicity) in.mult.assign(multiplicity, multiplicity + n_rows);
+        } else {
+            in.q_indptr.assign(1, 0);
+            in.kv_indptr.assign(1, 0);
+            in.block_len.assign(s.num_blocks, 0);
+            if (block_len) in.block_len.assign(block_len, block_len + s.num_blocks);
+        }
+        if (opts) {
+            in.opts = *opts;
+            in.has_opts = true;
+        }
+        in.kv_len = N;
+        in.tail_run.assign(n_rows, -1);
+        in.spare.assign(n_rows, 0);
+        in.merge_of.assign(n_rows, -1);
         tkv_plan_stats& st = p->stats;
         st.n_rows = n_rows;
         st.n_qtok = n_rows ? q_indptr[n_rows] : 0;
@@ -292,18 +360,20 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             if (wide_items < min_items) wave_max_rows = int64_t{1} << 40;
         }
         std::vector<Chunk> chunks;
+        std::vector<BlkDesc> seg_blks;                // each segment's key blocks, in path order
         std::vector<int32_t> cover(st.n_qtok, 0);
+        std::vector<int32_t> tail_chunk(n_rows, -1);  // a decode row's tail chunk (see tkv::PlanInputs)
         for (const Segment& sg : segs) {
             if (sg.rows.size() > 1) st.n_shared_segments += 1;
             const int32_t nb = static_cast<int32_t>(sg.nodes.size());
-            const int32_t seg_blk_off = static_cast<int32_t>(p->blks.size());
-            for (int32_t nd : sg.nodes) p->blks.push_back(BlkDesc{nodes[nd].blk, nodes[nd].len});
+            const int32_t seg_blk_off = static_cast<int32_t>(seg_blks.size());
+            for (int32_t nd : sg.nodes) seg_blks.push_back(BlkDesc{nodes[nd].blk, nodes[nd].len});
             // segments read by many query rows go to the 128-row tile kernel in long chunks; the
             // rest to the wave kernel in chunks that fit its records
             int64_t seg_rows = 0;
             for (int32_t r : sg.rows) seg_rows += static_cast<int64_t>(L[r]) * G;
             const bool wide = G > tkv::kWaveRows || seg_rows > wave_max_rows;
-            tile_evenly(nb, wide ? chunk_wide : kChunkBlocks, [&](int32_t a, int32_t e) {
+            auto cut = [&](int32_t a, int32_t e) {
                 Chunk c;
                 c.blk_off = seg_blk_off + a;
                 c.n_blk = e - a;
@@ -312,41 +382,72 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                     for (int32_t i = 0; i < L[r]; ++i) {
                         const int32_t lim = N[r] - L[r] + i;
                         if (lim < c.pos0) continue;  // the whole chunk is in this token's future
-                        c.toks.push_back(TokDesc{q_indptr[r] + i, lim, -1, 0});
+                        c.toks.push_back(TokDesc{q_indptr[r] + i, L[r] == 1 ? tkv::kNoLimit : lim, -1, 0});
                         cover[q_indptr[r] + i] += 1;
                     }
                 }
-                if (!c.toks.empty()) chunks.push_back(std::move(c));
-            });
+                if (c.toks.empty()) return;
+                // Chunks of groups with G <= 16 and at most kWaveMaxRows query rows go to the wave
+                // kernel: a wave contracts each K/V block against T column tiles of 16 rows (T = 1, 2
+                // as the chunk's rows need).  Wider chunks (and groups with G > 16) use the workgroup
+                // kernel's 128-row tiles, which stage each K/V block once for 128 rows.
+                const int64_t rows = static_cast<int64_t>(c.toks.size()) * G;
+                c.wave = G <= tkv::kWaveRows && rows <= wave_max_rows && c.n_blk <= kChunkBlocks;
+                if (sg.rows.size() == 1 && L[sg.rows[0]] == 1 && e == nb && c.wave)
+                    tail_chunk[sg.rows[0]] = static_cast<int32_t>(chunks.size());
+                chunks.push_back(std::move(c));
+            };
+            // A segment of one row is cut at fixed multiples of the chunk length from its start: as
+            // a decode row's path grows, its last chunk takes the new blocks or a new chunk follows
+            // it, and the chunks before stay as they are.  Shared segments are cut evenly.
+            if (sg.rows.size() == 1)
+                tile_full(nb, wide ? chunk_wide : kChunkBlocks, cut);
+            else
+                tile_evenly(nb, wide ? chunk_wide : kChunkBlocks, cut);
         }
         // partial slots for tokens covered by more than one chunk: each token's slots are
-        // contiguous (in chunk order), so the merge reads a token's partials as one range
+        // contiguous (in chunk order), so the merge reads a token's partials as one range.  A
+        // decode token with a tail chunk has one slot more, unused, for the chunk that its tail
+        // opens next (tkv_plan_update).
         std::vector<int32_t> slot_next(st.n_qtok, -1);
-        for (int32_t q = 0; q < st.n_qtok; ++q) {
+        for (int32_t r = 0; r < n_rows; ++r)
+            if (tail_chunk[r] >= 0 && cover[q_indptr[r]] >= 2) in.spare[r] = 1;
+        for (int32_t r = 0, q = 0; q < st.n_qtok; ++q) {
+            while (q_indptr[r + 1] <= q) ++r;
             if (cover[q] < 2) continue;
+            if (L[r] == 1) in.merge_of[r] = static_cast<int32_t>(p->merges.size());
             p->merges.push_back(MergeDesc{q, p->n_slots, cover[q], 0});
             slot_next[q] = p->n_slots;
-            p->n_slots += cover[q];
+            p->n_slots += cover[q] + (L[r] == 1 ? in.spare[r] : 0);
         }
         for (Chunk& c : chunks)
             for (TokDesc& t : c.toks)
                 if (cover[t.qtok] > 1) t.slot = slot_next[t.qtok]++;
         p->merge_slots.resize(p->n_slots);
         std::iota(p->merge_slots.begin(), p->merge_slots.end(), 0);
-        // Chunks of groups with G <= 16 and at most kWaveMaxRows query rows go to the wave kernel:
-        // a wave contracts each K/V block against T column tiles of 16 rows (T = 1, 2 as the
-        // chunk's rows need).  Wider chunks (and groups with G > 16) use the workgroup kernel's
-        // 128-row tiles, which stage each K/V block once for 128 rows.
-        for (const Chunk& c : chunks) {
+        // Items.  A wave chunk's blocks take a run of kWaveBlocks slots in wblks (room for a tail
+        // to grow into); its items' tokens go to wtoks.  Both stay on the host: the wave records
+        // carry them.  Tile items' blocks and tokens go to blks and toks, which the device reads.
+        std::vector<int32_t> chunk_run(chunks.size(), -1);
+        for (size_t ci = 0; ci < chunks.size(); ++ci) {
+            const Chunk& c = chunks[ci];
             const int64_t rows = static_cast<int64_t>(c.toks.size()) * G;
-            const bool wave = G <= tkv::kWaveRows && rows <= wave_max_rows && c.n_blk <= kChunkBlocks;
+            const bool wave = c.wave;
             const int32_t T = static_cast<int32_t>(std::min<int64_t>(tkv::kWaveMaxTiles, (rows + 15) / 16));
             const int32_t per_tile = wave ? tkv::kWaveRows * T / G : tpt;
+            std::vector<BlkDesc>& bv = wave ? p->wblks : p->blks;
+            std::vector<TokDesc>& tv = wave ? p->wtoks : p->toks;
+            const int32_t blk_off = static_cast<int32_t>(bv.size());
+            bv.insert(bv.end(), seg_blks.begin() + c.blk_off, seg_blks.begin() + c.blk_off + c.n_blk);
+            if (wave) {
+                bv.resize(blk_off + tkv::kWaveBlocks, BlkDesc{0, 0});
+                chunk_run[ci] = blk_off / tkv::kWaveBlocks;
+            }
             auto emit = [&](int32_t a, int32_t e) {
-                const int32_t tok_off = static_cast<int32_t>(p->toks.size());
-                p->toks.insert(p->toks.end(), c.toks.begin() + a, c.toks.begin() + e);
+                const int32_t tok_off = static_cast<int32_t>(tv.size());
+                tv.insert(tv.end(), c.toks.begin() + a, c.toks.begin() + e);
                 for (int32_t h = 0; h < s.hkv; ++h) {
-                    const ItemDesc d{h, tok_off, e - a, c.blk_off, c.n_blk, c.pos0,
+                    const ItemDesc d{h, tok_off, e - a, blk_off, c.n_blk, c.pos0,
                                      wave ? tkv::kItemWave : tkv::kItemShared, wave ? T : 0};
                     (wave ? p->wave_items : p->items).push_back(d);
                 }
@@ -358,6 +459,12 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                 tile_full(static_cast<int32_t>(c.toks.size()), per_tile, emit);
         }
         st.n_items_shared = static_cast<int32_t>(p->items.size() + p->wave_items.size());
+        int32_t n_tails = 0;
+        for (int32_t r = 0; r < n_rows; ++r)
+            if (tail_chunk[r] >= 0) {
+                in.tail_run[r] = chunk_run[tail_chunk[r]];
+                ++n_tails;
+            }
 
         // ------------------------------------------------------------ row items (large rows)
         {
@@ -389,7 +496,8 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                 const int32_t nb = static_cast<int32_t>(std::upper_bound(end_pos.begin(), end_pos.end(), max_lim) - end_pos.begin()) + 1;
                 const int32_t nbk = std::min<int32_t>(nb, static_cast<int32_t>(end_pos.size()));
                 const int32_t tok_off = static_cast<int32_t>(p->toks.size());
-                for (int32_t i = a; i < e; ++i) p->toks.push_back(TokDesc{q_indptr[r] + i, N[r] - L[r] + i, -1, 0});
+                for (int32_t i = a; i < e; ++i)
+                    p->toks.push_back(TokDesc{q_indptr[r] + i, L[r] == 1 ? tkv::kNoLimit : N[r] - L[r] + i, -1, 0});
                 for (int32_t h = 0; h < s.hkv; ++h)
                     p->items.push_back(ItemDesc{h, tok_off, e - a, row_blk_off, nbk, 0, tkv::kItemRow, 0});
             });
@@ -533,7 +641,10 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             // whose list has run out lends its slots to the longest remaining list
             size_t n_total = 0;
             for (auto& v : xcd_waves) n_total += v.size();
-            const size_t n_slots_w = (n_total + tkv::kWaveWG - 1) / tkv::kWaveWG * tkv::kWaveWG;
+            // idle waves follow the busy ones (kMaxSpareWaves)
+            const int64_t n_spare = std::min<int64_t>(kMaxSpareWaves,
+                ((static_cast<int64_t>(n_tails) * s.hkv + 7) / 8 + tkv::kWaveWG - 1) / tkv::kWaveWG * tkv::kWaveWG);
+            const size_t n_slots_w = (n_total + n_spare + tkv::kWaveWG - 1) / tkv::kWaveWG * tkv::kWaveWG;
             std::vector<size_t> next(kXcds, 0);
             std::vector<const Wave*> slots(n_slots_w, nullptr);
             for (size_t slot = 0; slot < n_slots_w; ++slot) {
@@ -566,6 +677,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         }
         st.n_items_wave = static_cast<int32_t>(p->wave_items.size());
         st.n_waves = static_cast<int32_t>(p->wave_tiles.size());
+        st.n_idle_waves = static_cast<int32_t>(std::count(p->wave_tiles.begin(), p->wave_tiles.end(), 0));
         // a plan of a few tile items and nothing else gives each tile a CU to itself: its 128 rows then
         // run as eight 16-row waves, which shortens the tile's walk
         const int64_t tile8_max = opt(&tkv_plan_options::tile8_max_items, tkv::kTile8MaxItems);
@@ -669,35 +781,6 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         p->off_plse = off;
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq, sizeof(float)));
         p->total_bytes = std::max<size_t>(off, 256);
-        // a wave item's 1-KB record, written in place: 16 block slots {id, length, position, -} (the
-        // fourth words of slots 0-2 carry the KV head, token count and walked block count) and 48 token
-        // slots {query token, causal limit, partial slot, -}
-        auto write_record = [&](int32_t item, uint8_t* dst) {
-            std::memset(dst, 0, sizeof(tkv::WaveDesc));
-            if (item < 0) return;
-            const ItemDesc& it = p->wave_items[item];
-            int32_t* e = reinterpret_cast<int32_t*>(dst);
-            // widths 1 and 2 walk blocks in pairs: an odd key list gets an empty block
-            const int32_t nb_run = it.pad <= 2 ? (it.n_blk + 1) & ~1 : it.n_blk;
-            int32_t pos = it.pos0;
-            for (int32_t j = 0; j < tkv::kWaveBlocks; ++j) {
-                const bool in = j < it.n_blk;
-                const BlkDesc& bd = p->blks[it.blk_off + (in ? j : 0)];
-                e[4 * j] = bd.blk;
-                e[4 * j + 1] = in ? bd.len : 0;
-                e[4 * j + 2] = pos;
-                if (in) pos += bd.len;
-            }
-            e[3] = it.kvh;
-            e[7] = it.n_tok;
-            e[11] = nb_run;
-            for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
-                const TokDesc& td = p->toks[it.tok_off + (t < it.n_tok ? t : 0)];
-                e[4 * (16 + t)] = td.qtok;
-                e[4 * (16 + t) + 1] = td.limit;
-                e[4 * (16 + t) + 2] = td.slot;
-            }
-        };
         // the image is written once: each section, its records in place, the padding zeroed
         p->image = tkv::take_image(p->desc_bytes, &p->image_cap);
         uint8_t* img = p->image.get();
@@ -714,7 +797,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         put(p->off_mslots, p->merge_slots.data(), bytes(p->merge_slots.size(), sizeof(int32_t)));
         put(p->off_wdesc, nullptr, 0);
         for (size_t r = 0; r < p->wave_rec.size(); ++r)
-            write_record(p->wave_rec[r], img + p->off_wdesc + r * sizeof(tkv::WaveDesc));
+            write_record(p, p->wave_rec[r], img + p->off_wdesc + r * sizeof(tkv::WaveDesc));
         filled = p->off_wdesc + p->wave_rec.size() * sizeof(tkv::WaveDesc);
         put(p->off_woff, p->wave_off.data(), bytes(p->wave_off.size(), sizeof(int32_t)));
         put(p->off_wtiles, p->wave_tiles.data(), bytes(p->wave_tiles.size(), sizeof(int32_t)));
@@ -788,19 +871,323 @@ TKV_EXPORT int tkv_plan_get_view(const tkv_plan* cp, tkv_plan_view* out) {
     tkv_plan* p = const_cast<tkv_plan*>(cp);
     tkv::clear_error();
     if (!p || !out) return set_error(TKV_EINVAL, "tkv_plan_get_view: NULL argument");
-    p->view_items.assign(p->items.begin(), p->items.end());
-    p->view_items.insert(p->view_items.end(), p->wave_items.begin(), p->wave_items.end());
+    // tile items, then wave items with their tokens and blocks placed after the tile items' ones
+    try {
+        p->view_items.assign(p->items.begin(), p->items.end());
+        const int32_t nt = static_cast<int32_t>(p->toks.size()), nbk = static_cast<int32_t>(p->blks.size());
+        for (ItemDesc it : p->wave_items) {
+            it.tok_off += nt;
+            it.blk_off += nbk;
+            p->view_items.push_back(it);
+        }
+        p->view_toks.assign(p->toks.begin(), p->toks.end());
+        p->view_toks.insert(p->view_toks.end(), p->wtoks.begin(), p->wtoks.end());
+        p->view_blks.assign(p->blks.begin(), p->blks.end());
+        p->view_blks.insert(p->view_blks.end(), p->wblks.begin(), p->wblks.end());
+    } catch (...) {
+        return set_error(TKV_ENOMEM, "tkv_plan_get_view: host allocation failed");
+    }
     out->items = reinterpret_cast<const int32_t*>(p->view_items.data());
-    out->toks = reinterpret_cast<const int32_t*>(p->toks.data());
-    out->blks = reinterpret_cast<const int32_t*>(p->blks.data());
+    out->toks = reinterpret_cast<const int32_t*>(p->view_toks.data());
+    out->blks = reinterpret_cast<const int32_t*>(p->view_blks.data());
     out->merges = reinterpret_cast<const int32_t*>(p->merges.data());
     out->merge_slots = p->merge_slots.data();
     out->n_items = static_cast<int32_t>(p->view_items.size());
-    out->n_toks = static_cast<int32_t>(p->toks.size());
-    out->n_blks = static_cast<int32_t>(p->blks.size());
+    out->n_toks = static_cast<int32_t>(p->view_toks.size());
+    out->n_blks = static_cast<int32_t>(p->view_blks.size());
     out->n_merge = static_cast<int32_t>(p->merges.size());
     out->n_merge_slots = static_cast<int32_t>(p->merge_slots.size());
     out->n_slots = p->n_slots;
+    return TKV_OK;
+}
+
+// ---------------------------------------------------------------------------- plan update
+namespace {
+
+// Every field of a plan's contents, exchanged (the instrumentation state stays with each object).
+void swap_contents(tkv_plan* a, tkv_plan* b) {
+    using std::swap;
+    swap(a->shape, b->shape);
+    swap(a->group, b->group);
+    swap(a->all_decode, b->all_decode);
+    swap(a->items, b->items);
+    swap(a->wave_items, b->wave_items);
+    swap(a->view_items, b->view_items);
+    swap(a->view_toks, b->view_toks);
+    swap(a->view_blks, b->view_blks);
+    swap(a->toks, b->toks);
+    swap(a->blks, b->blks);
+    swap(a->wtoks, b->wtoks);
+    swap(a->wblks, b->wblks);
+    swap(a->merges, b->merges);
+    swap(a->merge_slots, b->merge_slots);
+    swap(a->wave_rec, b->wave_rec);
+    swap(a->wave_off, b->wave_off);
+    swap(a->wave_tiles, b->wave_tiles);
+    swap(a->n_slots, b->n_slots);
+    swap(a->tile8, b->tile8);
+    swap(a->off_items, b->off_items);
+    swap(a->off_toks, b->off_toks);
+    swap(a->off_blks, b->off_blks);
+    swap(a->off_merges, b->off_merges);
+    swap(a->off_mslots, b->off_mslots);
+    swap(a->off_wdesc, b->off_wdesc);
+    swap(a->off_woff, b->off_woff);
+    swap(a->off_wtiles, b->off_wtiles);
+    swap(a->off_po, b->off_po);
+    swap(a->off_plse, b->off_plse);
+    swap(a->desc_bytes, b->desc_bytes);
+    swap(a->total_bytes, b->total_bytes);
+    swap(a->image, b->image);
+    swap(a->image_cap, b->image_cap);
+    swap(a->d_ws, b->d_ws);
+    swap(a->stats, b->stats);
+    swap(a->in, b->in);
+}
+
+// Room for `more` elements after the last, grown geometrically (an update appends a few each time).
+template <class V>
+void reserve_more(V& v, size_t more) {
+    if (v.size() + more > v.capacity()) v.reserve(std::max(v.size() + more, 2 * v.capacity()));
+}
+
+// The lookups an in-place update needs, built once per plan.
+void index_plan(tkv_plan* p) {
+    tkv::PlanInputs& in = *p->in;
+    const int32_t n_rows = p->stats.n_rows, hkv = p->shape.hkv;
+    in.owner.assign(p->shape.num_blocks, -1);
+    for (int32_t r = 0; r < n_rows; ++r)
+        for (int32_t j = in.kv_indptr[r]; j < in.kv_indptr[r + 1]; ++j) {
+            int32_t& o = in.owner[in.kv_blocks[j]];
+            o = o == -1 || o == r ? r : -2;
+        }
+    in.rec_of.assign(p->wave_items.size(), -1);
+    for (size_t w = 0; w < p->wave_rec.size(); ++w)
+        if (p->wave_rec[w] >= 0) in.rec_of[p->wave_rec[w]] = static_cast<int32_t>(w);
+    in.run_items.assign(p->wblks.size() / tkv::kWaveBlocks * hkv, -1);
+    std::vector<uint8_t> is_tail(p->wblks.size() / tkv::kWaveBlocks, 0);
+    for (int32_t r = 0; r < n_rows; ++r)
+        if (in.tail_run[r] >= 0) is_tail[in.tail_run[r]] = 1;
+    for (size_t i = 0; i < p->wave_items.size(); ++i) {
+        const ItemDesc& it = p->wave_items[i];
+        const int32_t run = it.blk_off / tkv::kWaveBlocks;
+        if (is_tail[run]) in.run_items[static_cast<size_t>(run) * hkv + it.kvh] = static_cast<int32_t>(i);
+    }
+    in.free_waves.clear();
+    const int32_t n_first = p->wave_off.empty() ? 0 : p->wave_off[0];
+    for (int32_t w = n_first - 1; w >= 0; --w)
+        if (p->wave_rec[w] < 0 && p->wave_tiles[w] == 0) in.free_waves.push_back(w);
+    in.indexed = true;
+}
+
+}  // namespace
+
+TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int32_t* kv_blocks,
+                               const int32_t* block_len, int32_t* in_place) {
+    tkv::clear_error();
+    if (in_place) *in_place = 0;
+    if (!p || !kv_indptr || !block_len) return set_error(TKV_EINVAL, "tkv_plan_update: NULL argument");
+    tkv::PlanInputs& in = *p->in;
+    const tkv_shape s = p->shape;
+    const int32_t n_rows = p->stats.n_rows, hkv = s.hkv;
+    if (kv_indptr[0] != 0) return set_error(TKV_EINVAL, "tkv_plan_update: kv_indptr[0] must be 0");
+    if (n_rows > 0 && kv_indptr[n_rows] > 0 && !kv_blocks) return set_error(TKV_EINVAL, "tkv_plan_update: kv_blocks is NULL");
+    auto is_decode = [&](int32_t r) { return in.q_indptr[r + 1] - in.q_indptr[r] == 1; };
+    auto tail_item = [&](int32_t run, int32_t h) { return in.run_items[static_cast<size_t>(run) * hkv + h]; };
+
+    // ------------------------------------------------ can the plan take the new tables in place?
+    // Every row keeps its blocks and may append new ones; a block changes length only as the last
+    // block of a decode row's path or as one of its new blocks.  Such a row must have a tail chunk;
+    // the new blocks fill it up to kWaveBlocks and may open one new chunk (its items on idle waves,
+    // its partial in the token's free slot).  Checked first, then applied: nothing changes unless
+    // all of it fits.  New blocks are marked in `owner` as taken by their row while checking.
+    std::vector<int32_t> grown, lengthened;  // rows with new blocks; rows whose last block grew
+    auto unmark = [&]() {
+        for (int32_t r : grown)
+            for (int32_t j = kv_indptr[r] + (in.kv_indptr[r + 1] - in.kv_indptr[r]); j < kv_indptr[r + 1]; ++j)
+                if (kv_blocks[j] >= 0 && kv_blocks[j] < s.num_blocks && in.owner[kv_blocks[j]] == -3 - r)
+                    in.owner[kv_blocks[j]] = -1;
+    };
+    bool fits = true;
+    size_t n_open = 0;  // new chunks
+    std::vector<uint8_t> dirty;
+    try {
+        if (!in.indexed) index_plan(p);
+        for (int32_t r = 0; r < n_rows && fits; ++r) {
+            const int32_t o0 = in.kv_indptr[r], n_old = in.kv_indptr[r + 1] - o0;
+            const int32_t n0 = kv_indptr[r], n_new = kv_indptr[r + 1] - n0;
+            if (n_new < n_old || (n_old > 0 && std::memcmp(in.kv_blocks.data() + o0, kv_blocks + n0, n_old * sizeof(int32_t)))) {
+                fits = false;
+                break;
+            }
+            if (n_new == n_old) continue;
+            if (!is_decode(r) || in.tail_run[r] < 0) {
+                fits = false;
+                break;
+            }
+            grown.push_back(r);
+            for (int32_t j = n0 + n_old; j < n0 + n_new && fits; ++j) {
+                const int32_t b = kv_blocks[j];
+                if (b < 0 || b >= s.num_blocks || block_len[b] < 1 || block_len[b] > s.block_size || in.owner[b] != -1)
+                    fits = false;
+                else
+                    in.owner[b] = -3 - r;
+            }
+            const int32_t room = tkv::kWaveBlocks - p->wave_items[tail_item(in.tail_run[r], 0)].n_blk;
+            const int32_t extra = n_new - n_old;
+            if (extra > room) {  // one new chunk at most, and only into the token's free slot
+                if (extra - room > tkv::kWaveBlocks || !in.spare[r] || in.merge_of[r] < 0) fits = false;
+                n_open += 1;
+            }
+        }
+        if (n_open * hkv > in.free_waves.size()) fits = false;
+        for (int32_t b = 0; b < s.num_blocks && fits; ++b) {
+            if (block_len[b] == in.block_len[b]) continue;
+            const int32_t o = in.owner[b];
+            if (o == -1 || o <= -3) continue;  // in no table, or one of this update's new blocks
+            if (o == -2 || !is_decode(o) || in.tail_run[o] < 0 || in.kv_blocks[in.kv_indptr[o + 1] - 1] != b ||
+                block_len[b] < in.block_len[b] || block_len[b] > s.block_size)
+                fits = false;
+            else
+                lengthened.push_back(o);
+        }
+        if (fits) {  // everything the patch appends to, so that it cannot fail half way
+            dirty.assign(n_rows, 0);
+            reserve_more(p->wtoks, n_open);
+            reserve_more(p->wblks, n_open * tkv::kWaveBlocks);
+            reserve_more(p->wave_items, n_open * hkv);
+            reserve_more(in.rec_of, n_open * hkv);
+            reserve_more(in.run_items, n_open * hkv);
+            reserve_more(in.kv_blocks, kv_indptr[n_rows] - in.kv_blocks.size());
+        }
+    } catch (...) {
+        unmark();
+        return set_error(TKV_ENOMEM, "tkv_plan_update: host allocation failed");
+    }
+    if (!fits) {
+        unmark();
+        // plan the new tables from scratch, with the plan's own query layout and options
+        tkv_plan* q = nullptr;
+        const int rc = tkv_plan_create_ex(&s, n_rows, in.q_indptr.data(), kv_indptr, kv_blocks, block_len,
+                                          in.mult.empty() ? nullptr : in.mult.data(), in.has_opts ? &in.opts : nullptr, &q);
+        if (rc != TKV_OK) return rc;  // create's error message; the plan is unchanged
+        swap_contents(p, q);
+        tkv_plan_destroy(q);
+        p->d_ws = nullptr;
+        return TKV_OK;
+    }
+
+    // ------------------------------------------------ in place
+    uint8_t* img = p->image.get();
+    auto record = [&](int32_t item) {
+        return reinterpret_cast<int32_t*>(img + p->off_wdesc + static_cast<size_t>(in.rec_of[item]) * sizeof(tkv::WaveDesc));
+    };
+    tkv_plan_stats& st = p->stats;
+    const int64_t flops_per_key = 4ll * s.d * s.hq;
+    for (int32_t r : lengthened) dirty[r] = 1;
+    for (int32_t r : grown) dirty[r] = 1;
+    for (int32_t r = 0; r < n_rows; ++r) {
+        if (!dirty[r]) continue;
+        const int32_t o0 = in.kv_indptr[r], n_old = in.kv_indptr[r + 1] - o0;
+        const int32_t n0 = kv_indptr[r], n_new = kv_indptr[r + 1] - n0;
+        int32_t run = in.tail_run[r];
+        BlkDesc* wb = &p->wblks[static_cast<size_t>(run) * tkv::kWaveBlocks];
+        int32_t n = p->wave_items[tail_item(run, 0)].n_blk;
+        int64_t added = 0;
+        // the path's last block (the tail chunk's last) took new tokens
+        const int32_t last = in.kv_blocks[o0 + n_old - 1];
+        const int32_t grew = block_len[last] - in.block_len[last];
+        if (grew) {
+            added += grew;
+            wb[n - 1].len = block_len[last];
+            in.block_len[last] = block_len[last];
+        }
+        if (n_new == n_old) {  // no new block: only the records' last block length changes
+            for (int32_t h = 0; h < hkv; ++h) record(tail_item(run, h))[4 * (n - 1) + 1] += grew;
+            in.kv_len[r] += grew;
+            st.path_kv_tokens += grew;
+            st.uniq_kv_tokens += grew;
+            st.flops += flops_per_key * grew;
+            continue;
+        }
+        int32_t end = p->wave_items[tail_item(run, 0)].pos0;
+        for (int32_t j = 0; j < n; ++j) end += wb[j].len;
+        bool opened = false;
+        for (int32_t j = n0 + n_old; j < n0 + n_new; ++j) {
+            const int32_t b = kv_blocks[j];
+            if (n == tkv::kWaveBlocks) {
+                // The tail chunk is full, its items final.  A new chunk of the row's token takes the
+                // following blocks; its partial goes to the token's free slot, after the others.
+                for (int32_t h = 0; h < hkv; ++h) {
+                    const int32_t i = tail_item(run, h);
+                    p->wave_items[i].n_blk = n;
+                    write_record_blocks(p, p->wave_items[i], record(i));
+                }
+                const int32_t T = p->wave_items[tail_item(run, 0)].pad;
+                MergeDesc& md = p->merges[in.merge_of[r]];
+                const int32_t slot = md.slot_off + md.n_slots;
+                md.n_slots += 1;
+                std::memcpy(img + p->off_merges + static_cast<size_t>(in.merge_of[r]) * sizeof(MergeDesc), &md, sizeof(MergeDesc));
+                in.spare[r] = 0;
+                const int32_t tok_off = static_cast<int32_t>(p->wtoks.size());
+                p->wtoks.push_back(TokDesc{in.q_indptr[r], tkv::kNoLimit, slot, 0});
+                run = static_cast<int32_t>(p->wblks.size() / tkv::kWaveBlocks);
+                p->wblks.resize(p->wblks.size() + tkv::kWaveBlocks, BlkDesc{0, 0});
+                wb = &p->wblks[static_cast<size_t>(run) * tkv::kWaveBlocks];
+                n = 0;
+                in.run_items.resize(in.run_items.size() + hkv, -1);
+                for (int32_t h = 0; h < hkv; ++h) {
+                    const int32_t i = static_cast<int32_t>(p->wave_items.size());
+                    p->wave_items.push_back(ItemDesc{h, tok_off, 1, run * tkv::kWaveBlocks, 0, end, tkv::kItemWave, T});
+                    const int32_t w = in.free_waves.back();
+                    in.free_waves.pop_back();
+                    p->wave_rec[w] = i;
+                    p->wave_tiles[w] = T;
+                    std::memcpy(img + p->off_wtiles + static_cast<size_t>(w) * sizeof(int32_t), &T, sizeof(int32_t));
+                    in.rec_of.push_back(w);
+                    in.run_items[static_cast<size_t>(run) * hkv + h] = i;
+                }
+                in.tail_run[r] = run;
+                st.n_items += hkv;
+                st.n_items_shared += hkv;
+                st.n_items_wave += hkv;
+                st.n_idle_waves -= hkv;
+                opened = true;
+            }
+            wb[n++] = BlkDesc{b, block_len[b]};
+            end += block_len[b];
+            added += block_len[b];
+            in.owner[b] = r;
+            in.block_len[b] = block_len[b];
+        }
+        for (int32_t h = 0; h < hkv; ++h) {
+            const int32_t i = tail_item(run, h);
+            p->wave_items[i].n_blk = n;
+            if (opened)
+                write_record(p, i, reinterpret_cast<uint8_t*>(record(i)));
+            else
+                write_record_blocks(p, p->wave_items[i], record(i));
+        }
+        in.kv_len[r] += static_cast<int32_t>(added);
+        st.path_kv_tokens += added;
+        st.uniq_kv_tokens += added;  // a tail's blocks are its row's alone
+        st.flops += flops_per_key * added;
+    }
+    // (in.block_len is kept for the blocks in the tables, above; a block in no table is skipped by
+    // the check whatever its length there)
+    std::memcpy(in.kv_indptr.data(), kv_indptr, (n_rows + 1) * sizeof(int32_t));
+    in.kv_blocks.assign(kv_blocks, kv_blocks + kv_indptr[n_rows]);  // within the reserved capacity
+    p->d_ws = nullptr;
+    if (in_place) *in_place = 1;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_plan_image(const tkv_plan* p, const void** data, tkv_plan_layout* layout) {
+    tkv::clear_error();
+    if (!p || !data || !layout) return set_error(TKV_EINVAL, "tkv_plan_image: NULL argument");
+    *data = p->image.get();
+    *layout = tkv_plan_layout{p->off_items, p->off_toks, p->off_blks, p->off_merges, p->off_mslots,
+                              p->off_wdesc, p->off_woff, p->off_wtiles, p->desc_bytes};
     return TKV_OK;
 }
 

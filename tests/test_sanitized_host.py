@@ -16,7 +16,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_39334_amd", "csrc")
 HOST_SOURCES = ["capi.cpp", "bm.cpp", "plan.cpp", "search.cpp"]
-SUITES = ["test_bm_parity.py", "test_bm_errors.py", "test_plan.py", "test_search_parity.py", "test_abi.py"]
+SUITES = ["test_bm_parity.py", "test_bm_errors.py", "test_plan.py", "test_plan_update.py", "test_search_parity.py",
+          "test_abi.py"]
 
 
 def _runtime(name):
