@@ -251,9 +251,9 @@ int tkv_plan_update(tkv_plan* plan, const int32_t* kv_indptr, const int32_t* kv_
 /* The plan's host descriptor image, what tkv_plan_upload copies (valid until the plan is updated
  * or destroyed; for tests and tools), and where its sections start, in bytes: tile items, their
  * tokens and blocks (the tkv_plan_get_view formats), merge entries, merge slot list, the wave
- * items' 1-KB records (one 16-byte word per lane: words 0-15 the key blocks {id, length,
- * position, header word}, header words KV head, token count, walked block count; words 16-63 the
- * tokens {query token, causal limit, slot, 0}), each wave's further records [off[w], off[w+1])
+ * items' 512-byte records (32 16-byte words: words 0-15 the key blocks {id, length, position,
+ * header word}, header words KV head, token count, walked block count; words 16-31 the tokens
+ * {query token, causal limit, slot, 0}), each wave's further records [off[w], off[w+1])
  * (int32, n_waves + 1), each wave's column tiles (int32, 0: no work); `end` = bytes uploaded.
  * Wave w runs record w, then its further records. */
 typedef struct {

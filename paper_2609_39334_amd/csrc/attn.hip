@@ -328,6 +328,11 @@ __device__ __forceinline__ void write_rows(const f32x4_t (&acc)[D / 16], float m
     }
 }
 
+// 16-byte words of a wave item's record (see tkv::WaveDesc): lane l loads word l % kRecWords, so
+// lanes 0-31 hold the record (the upper lanes repeat it and are never read).
+constexpr int kRecWords = static_cast<int>(sizeof(tkv::WaveDesc) / 16);
+static_assert(kRecWords == 32 && kRecWords == tkv::kWaveBlocks + tkv::kWaveToks, "record layout");
+
 // The item fields a wave needs, decoded from its descriptor (see tkv::WaveDesc): uniform values
 // by v_readlane, this lane's token of each tile by ds_bpermute from the token lanes.
 template <int T>
@@ -415,8 +420,8 @@ __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, co
     const uint8_t* vra = vs + (4 * kg + (col >> 2)) * VROW + (4 * (col & 3)) * 2;
     const uint8_t* vrb = vra + 16 * VROW;
 
-    int4 dc = wdesc[static_cast<size_t>(L.at(0)) * 64 + lane];
-    int4 dn = wdesc[static_cast<size_t>(L.at(1)) * 64 + lane];
+    int4 dc = wdesc[static_cast<size_t>(L.at(0)) * kRecWords + (lane & (kRecWords - 1))];
+    int4 dn = wdesc[static_cast<size_t>(L.at(1)) * kRecWords + (lane & (kRecWords - 1))];
     bf16x8_t qf[T][D / 32];
     int kvh_c, nb_c, limit[T];
     {
@@ -510,7 +515,7 @@ __device__ __forceinline__ void wave_run_pair(const int4* __restrict__ wdesc, co
         }
         if (!more) break;
         dc = dn;
-        dn = wdesc[static_cast<size_t>(L.at(e + 2)) * 64 + lane];
+        dn = wdesc[static_cast<size_t>(L.at(e + 2)) * kRecWords + (lane & (kRecWords - 1))];
         {
             int tok[T], grp[T];
             tile_rows<T>(col, G, tok, grp);

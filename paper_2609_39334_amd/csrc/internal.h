@@ -30,7 +30,8 @@ constexpr int kWaveMaxTiles = 2;  // column tiles a wave contracts against each 
 constexpr int kWaveMaxRows = 96;  // widest chunk (query rows) the wave kernel takes; wider ones use 128-row tiles
 constexpr int kTileMinItems = 0;  // wide chunks go to the tile kernel only if they make this many items
 constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
-constexpr int kWaveToks = 48;   // token slots of a wave-kernel record (>= 16 kWaveMaxTiles / G)
+constexpr int kWaveToks = 16;   // token slots of a wave-kernel record (a wave tile holds 16 T / G tokens,
+                                // so G = 1 takes T = 1)
 constexpr int kWaveWorkers = 2048;  // waves of the wave kernel: 2 workgroups of kWaveWG on each of 256 CUs
 constexpr int kWaveWG = 4;      // waves per workgroup of the wave kernel (independent; no barriers)
 constexpr int kTile8MaxItems = 256;  // tile items (and no wave grid) up to which 8-wave workgroups run them: one per CU
@@ -64,16 +65,16 @@ struct BlkDesc {
     int32_t len;  // tokens in the block (1..16)
 };
 
-// A wave-kernel item as one 1-KB record that a wave loads with one 16-byte load per lane (lane l
-// gets e[l]); block fields come out with v_readlane, token fields with ds_bpermute.
-//   e[j]      (j < 16): {pool block id, length, path position, header word j} of key block j
-//                       ({block 0's id, 0, 0} past the item's blocks); header words:
-//                       0 KV head, 1 tile tokens, 2 key blocks (rounded up to even for tile widths
-//                       1 and 2, whose waves walk blocks in pairs)
-//   e[16 + t] (t < 48): {query token, causal limit, partial slot (-1: final output), 0} of tile
-//                       token t (token 0's past the tile)
+// A wave-kernel item as one 512-byte record that a wave loads with one 16-byte load per lane (lane l
+// gets word l % 32); block fields come out with v_readlane, token fields with ds_bpermute.
+//   word j      (j < 16): {pool block id, length, path position, header word j} of key block j
+//                         ({block 0's id, 0, 0} past the item's blocks); header words:
+//                         0 KV head, 1 tile tokens, 2 key blocks (rounded up to even for tile widths
+//                         1 and 2, whose waves walk blocks in pairs)
+//   word 16 + t (t < 16): {query token, causal limit, partial slot (-1: final output), 0} of tile
+//                         token t (token 0's past the tile)
 struct WaveDesc {
-    int32_t e[256];
+    int32_t e[4 * (kWaveBlocks + kWaveToks)];
 };
 
 struct MergeDesc {

@@ -70,23 +70,21 @@ void write_record_blocks(const tkv_plan* p, const ItemDesc& it, int32_t* e) {
     e[11] = nb_run;
 }
 
-// A wave item's whole 1-KB record, written in place (zero for item < 0): its block slots, then 48
-// token slots {query token, causal limit, partial slot, 0}, token 0's past the tile.
+// A wave item's whole record, written in place (zero for item < 0): its block slots, then
+// kWaveToks token slots {query token, causal limit, partial slot, 0}, token 0's past the tile.
 void write_record(const tkv_plan* p, int32_t item, uint8_t* dst) {
     if (item < 0) {
         std::memset(dst, 0, sizeof(tkv::WaveDesc));
         return;
     }
+    static_assert(sizeof(TokDesc) == 16, "a token slot holds one TokDesc (its fourth word is 0)");
     const ItemDesc& it = p->wave_items[item];
     int32_t* e = reinterpret_cast<int32_t*>(dst);
     write_record_blocks(p, it, e);
-    for (int32_t t = 0; t < tkv::kWaveToks; ++t) {
-        const TokDesc& td = p->wtoks[it.tok_off + (t < it.n_tok ? t : 0)];
-        e[4 * (16 + t)] = td.qtok;
-        e[4 * (16 + t) + 1] = td.limit;
-        e[4 * (16 + t) + 2] = td.slot;
-        e[4 * (16 + t) + 3] = 0;
-    }
+    TokDesc* slots = reinterpret_cast<TokDesc*>(e + 4 * tkv::kWaveBlocks);
+    const TokDesc* src = p->wtoks.data() + it.tok_off;
+    std::memcpy(slots, src, static_cast<size_t>(it.n_tok) * sizeof(TokDesc));
+    for (int32_t t = it.n_tok; t < tkv::kWaveToks; ++t) slots[t] = src[0];
 }
 
 struct Node {
@@ -161,6 +159,17 @@ class IdMap {
     std::vector<int32_t> vals_;
     size_t mask_ = 0, n_ = 0;
 };
+
+// Stable sort of v by key(x) in [0, kmax], largest first (a counting sort).
+template <class T, class K>
+void sort_by_small_key_desc(std::vector<T>& v, int32_t kmax, K key) {
+    std::vector<size_t> start(kmax + 2, 0);
+    for (const T& x : v) ++start[kmax - key(x) + 1];
+    for (int32_t k = 1; k <= kmax + 1; ++k) start[k] += start[k - 1];
+    std::vector<T> out(v.size());
+    for (const T& x : v) out[start[kmax - key(x)]++] = x;
+    v.swap(out);
+}
 
 // Split n things into near-equal tiles of at most `cap`.
 template <class F>
@@ -289,12 +298,20 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         std::vector<Node> nodes;
         IdMap child(static_cast<size_t>(s.num_blocks));  // (parent node + 1, block) -> node
         std::vector<int32_t> path(n_rows ? kv_indptr[n_rows] : 0, -1);  // trie node of each table entry
-        int32_t prev = -1;  // the previous row walked: rows that share a prefix are usually adjacent
+        // the last row walked from each root block: the blocks a row shares with it lead to the
+        // same nodes, found without lookups
+        IdMap root_id(64);
+        std::vector<int32_t> root_last;
         for (int32_t r = 0; r < n_rows; ++r) {
             if (static_cast<int64_t>(L[r]) * G >= tkv::kTileRows) continue;
             int32_t cur = -1;
             int32_t j = kv_indptr[r];
-            if (prev >= 0) {  // the blocks this row shares with the previous one lead to the same nodes
+            bool fresh_root = false;
+            const int32_t rid = root_id.get(static_cast<uint32_t>(kv_blocks[j]), static_cast<int32_t>(root_last.size()), &fresh_root);
+            if (fresh_root) root_last.push_back(-1);
+            const int32_t prev = root_last[rid];
+            root_last[rid] = r;
+            if (prev >= 0) {
                 const int32_t len = std::min(kv_indptr[r + 1] - kv_indptr[r], kv_indptr[prev + 1] - kv_indptr[prev]);
                 for (int32_t k = 0; k < len && kv_blocks[j] == kv_blocks[kv_indptr[prev] + k]; ++k, ++j) {
                     cur = path[kv_indptr[prev] + k];
@@ -302,7 +319,6 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                     path[j] = cur;
                 }
             }
-            prev = r;
             for (; j < kv_indptr[r + 1]; ++j) {
                 const int32_t b = kv_blocks[j];
                 const uint64_t key = (static_cast<uint64_t>(static_cast<uint32_t>(cur + 1)) << 32) | static_cast<uint32_t>(b);
@@ -433,7 +449,9 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             const Chunk& c = chunks[ci];
             const int64_t rows = static_cast<int64_t>(c.toks.size()) * G;
             const bool wave = c.wave;
-            const int32_t T = static_cast<int32_t>(std::min<int64_t>(tkv::kWaveMaxTiles, (rows + 15) / 16));
+            // a wave tile holds 16 T / G tokens, at most the record's kWaveToks
+            const int32_t T = static_cast<int32_t>(std::min<int64_t>(
+                {tkv::kWaveMaxTiles, (rows + 15) / 16, static_cast<int64_t>(tkv::kWaveToks) * G / tkv::kWaveRows}));
             const int32_t per_tile = wave ? tkv::kWaveRows * T / G : tpt;
             std::vector<BlkDesc>& bv = wave ? p->wblks : p->blks;
             std::vector<TokDesc>& tv = wave ? p->wtoks : p->toks;
@@ -504,8 +522,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         }
         st.n_items = static_cast<int32_t>(p->items.size() + p->wave_items.size());
         st.n_items_row = st.n_items - st.n_items_shared;
-        std::stable_sort(p->wave_items.begin(), p->wave_items.end(),
-                         [](const ItemDesc& a, const ItemDesc& b) { return a.n_blk > b.n_blk; });
+        sort_by_small_key_desc(p->wave_items, tkv::kWaveBlocks, [](const ItemDesc& a) { return a.n_blk; });
         // Wave streams.  Every wave runs items of one tile width T (its code path is fixed); waves
         // are split over the widths in proportion to their work.  Workgroups of kWaveWG waves are
         // dispatched round-robin over the 8 XCDs (each with its own L2), so wave w runs on XCD
@@ -619,9 +636,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                 for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
                     auto& items_t = xcd_items_t[x][T];
                     if (items_t.empty()) continue;
-                    std::stable_sort(items_t.begin(), items_t.end(), [&](int32_t a2, int32_t b2) {
-                        return p->wave_items[a2].n_blk > p->wave_items[b2].n_blk;
-                    });
+                    sort_by_small_key_desc(items_t, tkv::kWaveBlocks, [&](int32_t i) { return p->wave_items[i].n_blk; });
                     using Load = std::pair<int64_t, int32_t>;
                     std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
                     for (size_t j = 0; j < ws.size(); ++j)
@@ -716,26 +731,18 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             using Load = std::pair<int64_t, int32_t>;
             std::priority_queue<Load, std::vector<Load>, std::greater<Load>> xheap;
             for (int32_t x = 0; x < kXcds; ++x) xheap.push({0, x});
+            // group-major: a group's items run together (so that the XCD's L2 holds the keys they
+            // share), groups in the order assigned, each group's items longest first
             std::vector<std::vector<int32_t>> xl(kXcds);
             for (int32_t g2 : gorder) {
                 Load l = xheap.top();
                 xheap.pop();
-                xl[l.second].insert(xl[l.second].end(), groups[g2].begin(), groups[g2].end());
+                std::vector<int32_t>& gi = groups[g2];
+                std::stable_sort(gi.begin(), gi.end(), [&](int32_t a2, int32_t b2) { return cost(p->items[a2]) > cost(p->items[b2]); });
+                xl[l.second].insert(xl[l.second].end(), gi.begin(), gi.end());
                 l.first += gcost[g2];
                 xheap.push(l);
             }
-            // group-major: a group's items run together (so that the XCD's L2 holds the keys they
-            // share), groups in the order assigned, each group's items longest first
-            std::vector<int32_t> group_of(p->items.size());
-            for (size_t g2 = 0; g2 < groups.size(); ++g2)
-                for (int32_t i : groups[g2]) group_of[i] = static_cast<int32_t>(g2);
-            std::vector<int32_t> rank(groups.size());
-            for (size_t k2 = 0; k2 < gorder.size(); ++k2) rank[gorder[k2]] = static_cast<int32_t>(k2);
-            for (auto& v : xl)
-                std::stable_sort(v.begin(), v.end(), [&](int32_t a2, int32_t b2) {
-                    if (group_of[a2] != group_of[b2]) return rank[group_of[a2]] < rank[group_of[b2]];
-                    return cost(p->items[a2]) > cost(p->items[b2]);
-                });
             std::vector<ItemDesc> ordered;
             ordered.reserve(p->items.size());
             std::vector<size_t> next(kXcds, 0);

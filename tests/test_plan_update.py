@@ -90,7 +90,7 @@ def decode_image(plan):
                    tuple(map(tuple, blks[bo:bo + nb].tolist())))
                   for kvh, to, nt, bo, nb, pos0, kind, _ in items)
     recs = sec("wave_records", "wave_off")
-    recs = recs[:len(recs) // 256 * 256].reshape(-1, 64, 4)
+    recs = recs[:len(recs) // 128 * 128].reshape(-1, 32, 4)
     n_w = st["n_waves"]
     woff = sec("wave_off", "wave_tiles")[:n_w + 1]
     wtiles = sec("wave_tiles", "end")[:n_w]
