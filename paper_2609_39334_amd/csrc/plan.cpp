@@ -110,7 +110,17 @@ constexpr int32_t kMaxSpareWaves = 512;
 // load).  Keys never equal ~0.
 class IdMap {
   public:
-    explicit IdMap(size_t expected) { rehash(std::max<size_t>(16, expected * 2)); }
+    explicit IdMap(size_t expected = 0) { reset(expected); }
+    // Empty, sized for `expected` keys (the storage is kept).
+    void reset(size_t expected) {
+        const size_t want = std::max<size_t>(16, expected * 2);
+        size_t cap = 16;
+        while (cap < want) cap <<= 1;
+        keys_.assign(cap, kEmpty);
+        vals_.resize(cap);
+        mask_ = cap - 1;
+        n_ = 0;
+    }
     // The key's id; a new key takes `next_id` (and *fresh is set).
     int32_t get(uint64_t key, int32_t next_id, bool* fresh) {
         if (2 * (n_ + 1) > keys_.size()) rehash(keys_.size() * 2);
@@ -188,6 +198,100 @@ void tile_full(int32_t n, int32_t cap, F f) {
     for (int32_t a = 0; a < n; a += cap) f(a, std::min(n, a + cap));
 }
 
+// The planner's working arrays, kept per thread from one plan to the next (a loop that plans every
+// step then fills memory it already holds).
+struct Scratch {
+    std::vector<int32_t> L, N, path, cover, tail_chunk, slot_next, chunk_run, end_pos, root_last;
+    std::vector<uint8_t> seen;
+    std::vector<Node> nodes;
+    std::vector<BlkDesc> seg_blks;
+    std::vector<ItemDesc> ordered;
+    IdMap child, root_id, gid;
+};
+
+// Plans destroyed without instrumentation are kept, emptied but with their arrays' capacity, for
+// the next tkv_plan_create (at most kPooledPlans; never destroyed: plans may be freed at exit).
+struct PlanPool {
+    std::mutex m;
+    std::vector<tkv_plan*> free;
+};
+PlanPool& plan_pool() {
+    static PlanPool* pool = new PlanPool();
+    return *pool;
+}
+constexpr size_t kPooledPlans = 2;
+
+// Every field back to a new plan's value; vectors keep their storage.  (The field list is
+// tkv_plan's; swap_contents below names the same fields.)
+void clear_plan(tkv_plan* p) {
+    p->shape = tkv_shape{};
+    p->group = 1;
+    p->all_decode = true;
+    p->items.clear();
+    p->wave_items.clear();
+    p->view_items.clear();
+    p->view_toks.clear();
+    p->view_blks.clear();
+    p->toks.clear();
+    p->blks.clear();
+    p->wtoks.clear();
+    p->wblks.clear();
+    p->merges.clear();
+    p->merge_slots.clear();
+    p->wave_rec.clear();
+    p->wave_off.clear();
+    p->wave_tiles.clear();
+    p->n_slots = 0;
+    p->tile8 = false;
+    p->off_items = p->off_toks = p->off_blks = p->off_merges = p->off_mslots = p->off_wdesc = p->off_woff = p->off_wtiles = 0;
+    p->off_po = p->off_plse = p->desc_bytes = p->total_bytes = 0;
+    tkv::give_image(std::move(p->image), p->image_cap);
+    p->image.reset();
+    p->image_cap = 0;
+    p->d_ws = nullptr;
+    p->stats = tkv_plan_stats{};
+    if (p->in) {
+        tkv::PlanInputs& in = *p->in;
+        for (auto* v : {&in.q_indptr, &in.kv_indptr, &in.kv_blocks, &in.block_len, &in.mult, &in.kv_len, &in.tail_run,
+                        &in.spare, &in.merge_of, &in.owner, &in.run_items, &in.rec_of, &in.free_waves})
+            v->clear();
+        in.opts = tkv_plan_options{};
+        in.has_opts = false;
+        in.indexed = false;
+    }
+}
+
+tkv_plan* take_plan() {
+    PlanPool& pool = plan_pool();
+    {
+        std::lock_guard<std::mutex> lock(pool.m);
+        if (!pool.free.empty()) {
+            tkv_plan* p = pool.free.back();
+            pool.free.pop_back();
+            return p;
+        }
+    }
+    return new (std::nothrow) tkv_plan();
+}
+
+void give_plan(tkv_plan* p) {
+    if (!p) return;
+    if (!p->prof_events.empty() || p->prof_max != 0) {  // instrumented: its events go with it
+        delete p;
+        return;
+    }
+    clear_plan(p);
+    PlanPool& pool = plan_pool();
+    {
+        std::lock_guard<std::mutex> lock(pool.m);
+        if (pool.free.size() < kPooledPlans) {
+            pool.free.push_back(p);
+            return;
+        }
+    }
+    delete p;
+}
+
 }  // namespace
 
 TKV_EXPORT int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_indptr,
@@ -224,7 +328,11 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
     if (n_rows > 0 && kv_indptr[n_rows] > 0 && !kv_blocks) return set_error(TKV_EINVAL, "tkv_plan_create: kv_blocks is NULL");
 
     // ---------------------------------------------------------------- validate rows
-    std::vector<int32_t> L(n_rows), N(n_rows);
+    thread_local Scratch sc;
+    std::vector<int32_t>& L = sc.L;
+    std::vector<int32_t>& N = sc.N;
+    L.assign(n_rows, 0);
+    N.assign(n_rows, 0);
     for (int32_t r = 0; r < n_rows; ++r) {
         L[r] = q_indptr[r + 1] - q_indptr[r];
         const int32_t nb = kv_indptr[r + 1] - kv_indptr[r];
@@ -244,12 +352,12 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         if (multiplicity && multiplicity[r] < 1) return set_error(TKV_EINVAL, "tkv_plan_create: multiplicity[%d] < 1", r);
     }
 
-    tkv_plan* p = new (std::nothrow) tkv_plan();
+    tkv_plan* p = take_plan();
     if (!p) return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
     try {
         p->shape = s;
         p->group = G;
-        p->in.reset(new tkv::PlanInputs());
+        if (!p->in) p->in.reset(new tkv::PlanInputs());
         tkv::PlanInputs& in = *p->in;
         if (n_rows > 0) {
             in.q_indptr.assign(q_indptr, q_indptr + n_rows + 1);
@@ -278,7 +386,8 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
 
         // ------------------------------------------------------------ accounting
         {
-            std::vector<uint8_t> seen(s.num_blocks, 0);
+            std::vector<uint8_t>& seen = sc.seen;
+            seen.assign(s.num_blocks, 0);
             for (int32_t r = 0; r < n_rows; ++r) {
                 p->all_decode = p->all_decode && L[r] == 1;
                 st.logical_qtok += static_cast<int64_t>(multiplicity ? multiplicity[r] : 1) * L[r];
@@ -295,13 +404,18 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         }
 
         // ------------------------------------------------------------ shared items (small rows)
-        std::vector<Node> nodes;
-        IdMap child(static_cast<size_t>(s.num_blocks));  // (parent node + 1, block) -> node
-        std::vector<int32_t> path(n_rows ? kv_indptr[n_rows] : 0, -1);  // trie node of each table entry
+        std::vector<Node>& nodes = sc.nodes;
+        nodes.clear();
+        IdMap& child = sc.child;  // (parent node + 1, block) -> node
+        child.reset(static_cast<size_t>(s.num_blocks));
+        std::vector<int32_t>& path = sc.path;  // trie node of each table entry
+        path.assign(n_rows ? kv_indptr[n_rows] : 0, -1);
         // the last row walked from each root block: the blocks a row shares with it lead to the
         // same nodes, found without lookups
-        IdMap root_id(64);
-        std::vector<int32_t> root_last;
+        IdMap& root_id = sc.root_id;
+        root_id.reset(64);
+        std::vector<int32_t>& root_last = sc.root_last;
+        root_last.clear();
         for (int32_t r = 0; r < n_rows; ++r) {
             if (static_cast<int64_t>(L[r]) * G >= tkv::kTileRows) continue;
             int32_t cur = -1;
@@ -376,9 +490,12 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             if (wide_items < min_items) wave_max_rows = int64_t{1} << 40;
         }
         std::vector<Chunk> chunks;
-        std::vector<BlkDesc> seg_blks;                // each segment's key blocks, in path order
-        std::vector<int32_t> cover(st.n_qtok, 0);
-        std::vector<int32_t> tail_chunk(n_rows, -1);  // a decode row's tail chunk (see tkv::PlanInputs)
+        std::vector<BlkDesc>& seg_blks = sc.seg_blks;  // each segment's key blocks, in path order
+        seg_blks.clear();
+        std::vector<int32_t>& cover = sc.cover;
+        cover.assign(st.n_qtok, 0);
+        std::vector<int32_t>& tail_chunk = sc.tail_chunk;  // a decode row's tail chunk (see tkv::PlanInputs)
+        tail_chunk.assign(n_rows, -1);
         for (const Segment& sg : segs) {
             if (sg.rows.size() > 1) st.n_shared_segments += 1;
             const int32_t nb = static_cast<int32_t>(sg.nodes.size());
@@ -425,7 +542,8 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         // contiguous (in chunk order), so the merge reads a token's partials as one range.  A
         // decode token with a tail chunk has one slot more, unused, for the chunk that its tail
         // opens next (tkv_plan_update).
-        std::vector<int32_t> slot_next(st.n_qtok, -1);
+        std::vector<int32_t>& slot_next = sc.slot_next;
+        slot_next.assign(st.n_qtok, -1);
         for (int32_t r = 0; r < n_rows; ++r)
             if (tail_chunk[r] >= 0 && cover[q_indptr[r]] >= 2) in.spare[r] = 1;
         for (int32_t r = 0, q = 0; q < st.n_qtok; ++q) {
@@ -444,7 +562,8 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         // Items.  A wave chunk's blocks take a run of kWaveBlocks slots in wblks (room for a tail
         // to grow into); its items' tokens go to wtoks.  Both stay on the host: the wave records
         // carry them.  Tile items' blocks and tokens go to blks and toks, which the device reads.
-        std::vector<int32_t> chunk_run(chunks.size(), -1);
+        std::vector<int32_t>& chunk_run = sc.chunk_run;
+        chunk_run.assign(chunks.size(), -1);
         for (size_t ci = 0; ci < chunks.size(); ++ci) {
             const Chunk& c = chunks[ci];
             const int64_t rows = static_cast<int64_t>(c.toks.size()) * G;
@@ -497,7 +616,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             p->toks.reserve(p->toks.size() + n_tok);
             p->items.reserve(p->items.size() + n_it);
         }
-        std::vector<int32_t> end_pos;  // end position of each block along a row's path
+        std::vector<int32_t>& end_pos = sc.end_pos;  // end position of each block along a row's path
         for (int32_t r = 0; r < n_rows; ++r) {
             if (static_cast<int64_t>(L[r]) * G < tkv::kTileRows) continue;
             const int32_t row_blk_off = static_cast<int32_t>(p->blks.size());
@@ -710,7 +829,8 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             auto cost = [&](const ItemDesc& it) {
                 return static_cast<int64_t>(it.n_blk) * ((static_cast<int64_t>(it.n_tok) * G + 31) / 32) + 1;
             };
-            IdMap gid(p->items.size());  // (first key block, KV head) -> group
+            IdMap& gid = sc.gid;  // (first key block, KV head) -> group
+            gid.reset(p->items.size());
             std::vector<std::vector<int32_t>> groups;
             std::vector<int64_t> gcost;
             for (int32_t i = 0; i < static_cast<int32_t>(p->items.size()); ++i) {
@@ -743,7 +863,8 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                 l.first += gcost[g2];
                 xheap.push(l);
             }
-            std::vector<ItemDesc> ordered;
+            std::vector<ItemDesc>& ordered = sc.ordered;
+            ordered.clear();
             ordered.reserve(p->items.size());
             std::vector<size_t> next(kXcds, 0);
             while (ordered.size() < p->items.size()) {
@@ -810,7 +931,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         put(p->off_wtiles, p->wave_tiles.data(), bytes(p->wave_tiles.size(), sizeof(int32_t)));
         if (p->desc_bytes > filled) std::memset(img + filled, 0, p->desc_bytes - filled);
     } catch (...) {
-        delete p;
+        give_plan(p);
         return set_error(TKV_ENOMEM, "tkv_plan_create: host allocation failed");
     }
     *out = p;
@@ -865,7 +986,7 @@ void give_image(std::unique_ptr<uint8_t[]> image, size_t cap) {
 
 TKV_EXPORT size_t tkv_plan_workspace_bytes(const tkv_plan* p) { return p ? p->total_bytes : 0; }
 
-TKV_EXPORT void tkv_plan_destroy(tkv_plan* p) { delete p; }
+TKV_EXPORT void tkv_plan_destroy(tkv_plan* p) { give_plan(p); }
 
 TKV_EXPORT int tkv_plan_get_stats(const tkv_plan* p, tkv_plan_stats* out) {
     tkv::clear_error();

@@ -191,3 +191,17 @@ def test_empty_plan():
     assert st["n_items"] == 0 and st["n_rows"] == 0
     assert tkv.tkv_plan_workspace_bytes(plan) >= 256
     tkv.tkv_plan_destroy(plan)
+
+
+def test_plans_do_not_depend_on_earlier_plans():
+    # destroyed plans are recycled with their arrays' storage: a plan must come out the same whatever
+    # plans were made and destroyed before it
+    cases = {"tiny": W.tiny_decode(0), "rt": W.random_tree(3, W.Shape(12, 2, 128), n_roots=3, depth=3),
+             "verify": W.step_verify(0, n_queries=2, n_cands=4)}
+    seen = {}
+    for order in (["tiny", "rt", "verify"], ["verify", "tiny", "rt"], ["rt", "verify", "tiny"]):
+        for name in order:
+            b, plan = _run(cases[name])
+            got = (plan.image(), plan.stats)
+            assert seen.setdefault(name, got) == got, name
+            del plan
