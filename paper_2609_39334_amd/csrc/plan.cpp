@@ -106,6 +106,9 @@ struct Chunk {
 // eight (row, KV head) tails, a multiple of kWaveWG, at most kMaxSpareWaves.
 constexpr int32_t kMaxSpareWaves = 512;
 
+// Key blocks per wave below which a wave grid beside a chip-filling set of tile items is made smaller.
+constexpr int64_t kWaveBlocksPerWave = 8;
+
 // Dense ids for 64-bit keys in first-insertion order (open addressing, linear probing, grown at half
 // load).  Keys never equal ~0.
 class IdMap {
@@ -658,6 +661,16 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             const int32_t n_tile = static_cast<int32_t>(p->items.size());
             int32_t target = tkv::kWaveWorkers;
             if (n_tile < wg_slots) target = std::max(wg_slots / 2, wg_slots - n_tile) / kXcds * kXcds * tkv::kWaveWG;
+            // A light wave grid (under kWaveBlocksPerWave key blocks per wave) beside many tile items
+            // shrinks, down to a quarter of the grid, so that its workgroups hold fewer of the slots
+            // the tile items need (the shared-prefix pass of a few long prompts with one-block tails).
+            int64_t wave_blocks = 0;
+            for (const ItemDesc& it : p->wave_items) wave_blocks += it.n_blk;
+            if (n_tile >= wg_slots) {
+                const int64_t light = (wave_blocks / kWaveBlocksPerWave + kXcds * tkv::kWaveWG - 1) / (kXcds * tkv::kWaveWG) *
+                                      (kXcds * tkv::kWaveWG);
+                target = static_cast<int32_t>(std::max<int64_t>(tkv::kWaveWorkers / 4, std::min<int64_t>(target, light)));
+            }
             if (opts && opts->waves > 0) target = std::max(kXcds, opts->waves);
             auto cost = [](const ItemDesc& it) { return static_cast<int64_t>(it.n_blk) * (3 + it.pad) + 4; };
             std::vector<std::vector<int32_t>> by_t(tkv::kWaveMaxTiles + 1);
