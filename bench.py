@@ -579,15 +579,19 @@ def shared_pass_flops(view, s):
     return total * g * 4 * s.d
 
 
-def time_plan_updates(wl, steps=48, seed=0):
-    """Host cost of a decode loop's planning: the workload's measured launch on a block manager with
-    room to grow, then `steps` decode steps (one token more for every candidate, a new block when
-    its last is full), each followed by tkv_plan_update of one plan.  A fresh tkv_plan_create of the
-    same tables is timed every eighth step for comparison.  Host only; no device memory."""
+def time_plan_updates(wl, steps=48, seed=0, device=None):
+    """Cost of a decode loop's planning: the workload's measured launch on a block manager with
+    room to grow, then decode steps (one token more for every candidate, a new block when its last
+    is full), each followed by tkv_plan_update of one plan.  `steps` steps time the update alone on
+    the host; a fresh tkv_plan_create of the same tables is timed every eighth step for comparison.
+    With a device, two more passes of `steps` // 2 steps run the loop as a decode loop would: update,
+    upload, decode on random K/V, wait; once uploading into the same workspace (after an in-place
+    update only the changed descriptor words go), once alternating two workspaces (the whole image
+    each time).  Their per-step wall times are reported."""
     import paper_2609_39334_amd as tkv
     import workloads as W
     s = wl.shape
-    nb = wl.num_blocks + 8192
+    nb = wl.num_blocks + 16384
     bm = tkv.BlockManager(nb, s.block_size, wl.max_seqs)
     cap = {}
     W.drive(wl, bm, on_launch=lambda i, l, c: cap.__setitem__(i, (l, c)))
@@ -598,20 +602,20 @@ def time_plan_updates(wl, steps=48, seed=0):
     rows = [seqs[c] for c in first]
     qi = np.concatenate([[0], np.cumsum([qls[c] for c in first])]).astype(np.int32)
     shape = (s.hq, s.hkv, s.d, s.block_size, nb)
+    rng = np.random.default_rng(seed)
 
-    def tables():
+    def grow():
+        for x in rows:
+            bm.append(x, rng.integers(0, 1 << 15, 1).astype(np.int32))
         t = [bm.table(x) for x in rows]
         return (np.concatenate([[0], np.cumsum([len(x) for x in t])]).astype(np.int32),
                 np.concatenate(t).astype(np.int32), bm.block_len())
 
-    h = tkv.tkv_plan_create(shape, qi, *tables(), mult)
-    rng = np.random.default_rng(seed)
+    h = tkv.tkv_plan_create(shape, qi, *grow(), mult)
     t_upd, in_place, t_create = [], 0, []
     try:
         for k in range(steps):
-            for x in rows:
-                bm.append(x, rng.integers(0, 1 << 15, 1).astype(np.int32))
-            ki, kb, bl = tables()
+            ki, kb, bl = grow()
             t0 = time.perf_counter()
             in_place += tkv.tkv_plan_update(h, ki, kb, bl)
             t_upd.append(time.perf_counter() - t0)
@@ -620,11 +624,50 @@ def time_plan_updates(wl, steps=48, seed=0):
                 h2 = tkv.tkv_plan_create(shape, qi, ki, kb, bl, mult)
                 t_create.append(time.perf_counter() - t0)
                 tkv.tkv_plan_destroy(h2)
+        res = {"decode_steps": steps, "plan_update_median": round(float(np.median(t_upd)) * 1e3, 4),
+               "plan_update_mean": round(float(np.mean(t_upd)) * 1e3, 4), "updates_in_place": in_place,
+               "plan_create_median_same_tables": round(float(np.median(t_create)) * 1e3, 3)}
+        if device is not None:
+            import torch
+            stream = torch.cuda.current_stream()
+            kd = torch.randn((nb, s.hkv, s.block_size, s.d), dtype=torch.bfloat16, device=device)
+            vd = torch.randn((nb, s.hkv, s.block_size, s.d), dtype=torch.bfloat16, device=device)
+            n_q = int(qi[-1])
+            qd = torch.randn((n_q, s.hq, s.d), dtype=torch.bfloat16, device=device)
+            od = torch.empty((n_q, s.hq, s.d), dtype=torch.bfloat16, device=device)
+            loop = {}
+            for mode in ("changed_words", "whole_image"):
+                wss = [torch.empty(2 * tkv.tkv_plan_workspace_bytes(h), dtype=torch.uint8, device=device)
+                       for _ in range(2)]
+                tkv.tkv_plan_upload(h, wss[0], stream)
+                t_u, t_l, t_w, n_ip = [], [], [], 0
+                for k in range(steps // 2):
+                    ki, kb, bl = grow()
+                    torch.cuda.synchronize()
+                    t0 = time.perf_counter()
+                    n_ip += tkv.tkv_plan_update(h, ki, kb, bl)
+                    t1 = time.perf_counter()
+                    ws = wss[0] if mode == "changed_words" else wss[k % 2]
+                    if tkv.tkv_plan_workspace_bytes(h) > ws.numel():
+                        break           # a plan made again grew past the workspaces: stop the pass
+                    tkv.tkv_plan_upload(h, ws, stream)
+                    t2 = time.perf_counter()
+                    tkv.tkv_decode(h, qd, kd, vd, od, None, stream)
+                    torch.cuda.synchronize()
+                    t3 = time.perf_counter()
+                    t_u.append(t1 - t0)
+                    t_l.append(t2 - t1)
+                    t_w.append(t3 - t0)
+                loop[mode] = {"steps": len(t_w), "in_place": n_ip, "update_us": round(float(np.median(t_u)) * 1e6, 1),
+                              "upload_call_us": round(float(np.median(t_l)) * 1e6, 1),
+                              "step_wall_us": round(float(np.median(t_w)) * 1e6, 1)}
+            img, _ = tkv.tkv_plan_image(h)
+            loop["image_bytes"] = len(img)
+            res["loop_update_upload_decode"] = loop
+            del kd, vd, qd, od
     finally:
         tkv.tkv_plan_destroy(h)
-    return {"decode_steps": steps, "plan_update_median": round(float(np.median(t_upd)) * 1e3, 4),
-            "plan_update_mean": round(float(np.mean(t_upd)) * 1e3, 4), "updates_in_place": in_place,
-            "plan_create_median_same_tables": round(float(np.median(t_create)) * 1e3, 3)}
+    return res
 
 
 def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
@@ -776,7 +819,7 @@ def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
         res["warm"] = {"ms_per_step": round(ms_step_warm, 5), "value": round(n_qtok / (ms_step_warm / 1e3), 1),
                        "kv_pool_fits_mall": pool_bytes <= MALL_BYTES}
     if L.decode:
-        res["host_ms"]["decode_loop"] = time_plan_updates(wl)
+        res["host_ms"]["decode_loop"] = time_plan_updates(wl, device=dev)
     if with_cpu:
         res["cpu_baseline"] = cpu_baseline(a, qbits, kbits, vbits, tables, bl, q_lens)
     return res

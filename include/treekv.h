@@ -220,9 +220,12 @@ size_t tkv_plan_workspace_bytes(const tkv_plan* plan);
 
 /* Copy the plan's descriptors into d_workspace (device memory of >= tkv_plan_workspace_bytes,
  * 256-byte aligned, caller-owned) on hip_stream; the plan keeps using that workspace until the
- * next upload.  The plan must outlive the copy: a destroyed plan's host image is recycled by later
- * plans.  (HIP stages a pageable host source before hipMemcpyAsync returns, which is what the
- * library's own callers rely on.)  EINVAL (size, alignment, NULL), EHIP. */
+ * next upload.  Into the workspace of the plan's last upload, after in-place tkv_plan_update calls,
+ * only the descriptor words those updates changed are sent (index/value pairs through a region of
+ * the workspace, written in by a small kernel on hip_stream); so the caller must not write into
+ * the descriptor region between uploads.  The plan must outlive the copy: a destroyed plan's host
+ * image is recycled by later plans.  (HIP stages a pageable host source before hipMemcpyAsync
+ * returns, which is what the library's own callers rely on.)  EINVAL (size, alignment, NULL), EHIP. */
 int tkv_plan_upload(tkv_plan* plan, void* d_workspace, size_t bytes, void* hip_stream);
 
 void tkv_plan_destroy(tkv_plan* plan);
@@ -247,6 +250,12 @@ void tkv_plan_destroy(tkv_plan* plan);
  * tkv_plan_create rejects in the new tables), ENOMEM. */
 int tkv_plan_update(tkv_plan* plan, const int32_t* kv_indptr, const int32_t* kv_blocks,
                     const int32_t* block_len, int32_t* in_place);
+
+/* The descriptor words (int32 indices into the image) that in-place updates changed since the
+ * plan's last upload (since its creation if never uploaded): *words, *n (repeats possible), and
+ * *complete = 0 if they overflowed the plan's patch capacity (the next upload then copies the
+ * whole image).  Valid until the next update or upload; for tests and tools. */
+int tkv_plan_dirty(const tkv_plan* plan, const int32_t** words, int32_t* n, int32_t* complete);
 
 /* The plan's host descriptor image, what tkv_plan_upload copies (valid until the plan is updated
  * or destroyed; for tests and tools), and where its sections start, in bytes: tile items, their

@@ -82,6 +82,8 @@ _SIG = {
     "tkv_plan_upload": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P]),
     "tkv_plan_update": (ctypes.c_int, [_P, _P, _P, _P, ctypes.POINTER(ctypes.c_int32)]),
     "tkv_plan_image": (ctypes.c_int, [_P, ctypes.POINTER(_P), ctypes.POINTER(tkv_plan_layout)]),
+    "tkv_plan_dirty": (ctypes.c_int, [_P, ctypes.POINTER(_PI32), ctypes.POINTER(ctypes.c_int32),
+                                      ctypes.POINTER(ctypes.c_int32)]),
     "tkv_plan_destroy": (None, [_P]),
     "tkv_plan_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_stats)]),
     "tkv_plan_get_view": (ctypes.c_int, [_P, ctypes.POINTER(tkv_plan_view)]),
@@ -330,6 +332,14 @@ def tkv_plan_update(plan: int, kv_indptr, kv_blocks, block_len) -> bool:
     flag = ctypes.c_int32(0)
     _check(lib().tkv_plan_update(plan, _ptr(ki), _ptr(kb) if len(kb) else None, _ptr(bl), ctypes.byref(flag)))
     return bool(flag.value)
+
+
+def tkv_plan_dirty(plan: int):
+    """(word indices the plan's in-place updates changed since its last upload, complete?)."""
+    words, n, complete = _PI32(), ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().tkv_plan_dirty(plan, ctypes.byref(words), ctypes.byref(n), ctypes.byref(complete)))
+    idx = np.ctypeslib.as_array(words, shape=(n.value,)).copy() if n.value else np.zeros(0, dtype=np.int32)
+    return idx, bool(complete.value)
 
 
 def tkv_plan_image(plan: int):

@@ -923,18 +923,60 @@ __global__ __launch_bounds__(1024) void merge_partials(const tkv::MergeDesc* __r
     }
 }
 
+// Writes image words into an uploaded workspace: pairs[i] = {word index, value}.  The host builds
+// every index from the plan's own image, below its size.
+__global__ __launch_bounds__(256) void patch_apply(const int2* __restrict__ pairs, int n, int32_t* __restrict__ ws) {
+    const int i = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x);
+    if (i < n) {
+        const int2 w = pairs[i];
+        ws[w.x] = w.y;
+    }
+}
+
 }  // namespace
 
 namespace tkv {
 
 int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream) {
     (void)bytes;
-    if (p->desc_bytes) {
-        const hipError_t e = hipMemcpyAsync(d_ws, p->image.get(), p->desc_bytes, hipMemcpyHostToDevice,
-                                            static_cast<hipStream_t>(stream));
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    // Into the workspace that holds the image of the last upload, only the words in-place updates
+    // changed since: (index, value) pairs copied to the patch region, then written in by patch_apply.
+    const size_t n_words = p->desc_bytes / sizeof(int32_t);
+    bool patch = d_ws == p->ws_image && !p->dirty_over && p->dirty.size() <= static_cast<size_t>(p->patch_cap);
+    if (patch && !p->dirty.empty()) {
+        const int32_t* img = reinterpret_cast<const int32_t*>(p->image.get());
+        std::vector<int32_t>& pairs = p->patch_pairs;
+        pairs.resize(2 * p->dirty.size());
+        for (size_t i = 0; i < p->dirty.size(); ++i) {
+            const int32_t w = p->dirty[i];
+            if (w < 0 || static_cast<size_t>(w) >= n_words) {  // cannot happen; never send an index out of the image
+                patch = false;
+                break;
+            }
+            pairs[2 * i] = w;
+            pairs[2 * i + 1] = img[w];
+        }
+        if (patch) {
+            uint8_t* ws = static_cast<uint8_t*>(d_ws);
+            const int n = static_cast<int>(p->dirty.size());
+            hipError_t e = hipMemcpyAsync(ws + p->off_patch, pairs.data(), pairs.size() * sizeof(int32_t),
+                                          hipMemcpyHostToDevice, st);
+            if (e != hipSuccess) return set_error(TKV_EHIP, "tkv_plan_upload: hipMemcpyAsync: %s", hipGetErrorString(e));
+            hipLaunchKernelGGL(patch_apply, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, st,
+                               reinterpret_cast<const int2*>(ws + p->off_patch), n, reinterpret_cast<int32_t*>(ws));
+            e = hipGetLastError();
+            if (e != hipSuccess) return set_error(TKV_EHIP, "tkv_plan_upload: patch_apply launch: %s", hipGetErrorString(e));
+        }
+    }
+    if (!patch && p->desc_bytes) {
+        const hipError_t e = hipMemcpyAsync(d_ws, p->image.get(), p->desc_bytes, hipMemcpyHostToDevice, st);
         if (e != hipSuccess) return set_error(TKV_EHIP, "tkv_plan_upload: hipMemcpyAsync: %s", hipGetErrorString(e));
     }
     p->d_ws = d_ws;
+    p->ws_image = d_ws;
+    p->dirty.clear();
+    p->dirty_over = false;
     return TKV_OK;
 }
 

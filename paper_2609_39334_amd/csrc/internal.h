@@ -106,6 +106,7 @@ struct PlanInputs {
 }  // namespace tkv
 
 // ------------------------------------------------------------------ plan (host)
+// Every field below is also named by clear_plan and swap_contents in plan.cpp.
 struct tkv_plan {
     tkv_shape shape{};
     int32_t group = 1;
@@ -134,6 +135,17 @@ struct tkv_plan {
     std::unique_ptr<uint8_t[]> image;  // host copy of the descriptor region (desc_bytes)
     size_t image_cap = 0;              // bytes allocated for it (returned to the image pool on destroy)
     void* d_ws = nullptr;        // uploaded workspace (caller-owned)
+    // Patch uploads: ws_image is the workspace that holds the image as of the last upload; `dirty`
+    // lists the image words in-place updates changed since (word indices, repeats allowed), complete
+    // unless dirty_over.  The next upload into ws_image sends only those words, as (index, value)
+    // pairs into the workspace's patch region (patch_cap pairs at off_patch; 0 for plans that cannot
+    // be updated in place), and a small kernel writes them in.
+    void* ws_image = nullptr;
+    std::vector<int32_t> dirty;
+    bool dirty_over = false;
+    std::vector<int32_t> patch_pairs;  // host staging of the pairs
+    size_t off_patch = 0;
+    int32_t patch_cap = 0;
     tkv_plan_stats stats{};
     std::unique_ptr<tkv::PlanInputs> in;  // for tkv_plan_update
     // instrumentation: 3 HIP events per recorded call (see tkv_plan_profile)

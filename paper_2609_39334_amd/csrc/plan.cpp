@@ -252,6 +252,12 @@ void clear_plan(tkv_plan* p) {
     p->image.reset();
     p->image_cap = 0;
     p->d_ws = nullptr;
+    p->ws_image = nullptr;
+    p->dirty.clear();
+    p->dirty_over = false;
+    p->patch_pairs.clear();
+    p->off_patch = 0;
+    p->patch_cap = 0;
     p->stats = tkv_plan_stats{};
     if (p->in) {
         tkv::PlanInputs& in = *p->in;
@@ -921,6 +927,11 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq * s.d, sizeof(uint16_t)));  // fp16 partial o
         p->off_plse = off;
         off = align256(off + bytes(static_cast<size_t>(p->n_slots) * s.hq, sizeof(float)));
+        // room for the (word, value) pairs of a patch upload after an in-place update: a lengthened
+        // tail changes one word per record; appended blocks and new chunks a few more
+        p->patch_cap = n_tails == 0 ? 0 : static_cast<int32_t>(std::min<int64_t>(int64_t{1} << 24, static_cast<int64_t>(n_tails) * s.hkv * 4 + 8192));
+        p->off_patch = off;
+        off = align256(off + bytes(static_cast<size_t>(p->patch_cap), 2 * sizeof(int32_t)));
         p->total_bytes = std::max<size_t>(off, 256);
         // the image is written once: each section, its records in place, the padding zeroed
         p->image = tkv::take_image(p->desc_bytes, &p->image_cap);
@@ -1082,6 +1093,12 @@ void swap_contents(tkv_plan* a, tkv_plan* b) {
     swap(a->image, b->image);
     swap(a->image_cap, b->image_cap);
     swap(a->d_ws, b->d_ws);
+    swap(a->ws_image, b->ws_image);
+    swap(a->dirty, b->dirty);
+    swap(a->dirty_over, b->dirty_over);
+    swap(a->patch_pairs, b->patch_pairs);
+    swap(a->off_patch, b->off_patch);
+    swap(a->patch_cap, b->patch_cap);
     swap(a->stats, b->stats);
     swap(a->in, b->in);
 }
@@ -1200,6 +1217,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
             reserve_more(in.rec_of, n_open * hkv);
             reserve_more(in.run_items, n_open * hkv);
             reserve_more(in.kv_blocks, kv_indptr[n_rows] - in.kv_blocks.size());
+            if (p->dirty.capacity() < static_cast<size_t>(p->patch_cap)) p->dirty.reserve(p->patch_cap);
         }
     } catch (...) {
         unmark();
@@ -1223,6 +1241,25 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     auto record = [&](int32_t item) {
         return reinterpret_cast<int32_t*>(img + p->off_wdesc + static_cast<size_t>(in.rec_of[item]) * sizeof(tkv::WaveDesc));
     };
+    // the image words changed, for the next upload (within the reserved capacity; past it the
+    // next upload copies the whole image)
+    auto note = [&](const int32_t* e, int32_t n_words) {
+        if (p->dirty_over || p->dirty.size() + n_words > static_cast<size_t>(p->patch_cap)) {
+            p->dirty_over = true;
+            return;
+        }
+        const int32_t base = static_cast<int32_t>(e - reinterpret_cast<const int32_t*>(img));
+        for (int32_t k = 0; k < n_words; ++k) p->dirty.push_back(base + k);
+    };
+    constexpr int32_t kBlockWords = 4 * tkv::kWaveBlocks;
+    auto rewrite_blocks = [&](int32_t item) {  // a record's block slots, noting the words that change
+        int32_t* e = record(item);
+        int32_t before[kBlockWords];
+        std::memcpy(before, e, sizeof(before));
+        write_record_blocks(p, p->wave_items[item], e);
+        for (int32_t k = 0; k < kBlockWords; ++k)
+            if (e[k] != before[k]) note(e + k, 1);
+    };
     tkv_plan_stats& st = p->stats;
     const int64_t flops_per_key = 4ll * s.d * s.hq;
     for (int32_t r : lengthened) dirty[r] = 1;
@@ -1244,7 +1281,11 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
             in.block_len[last] = block_len[last];
         }
         if (n_new == n_old) {  // no new block: only the records' last block length changes
-            for (int32_t h = 0; h < hkv; ++h) record(tail_item(run, h))[4 * (n - 1) + 1] += grew;
+            for (int32_t h = 0; h < hkv; ++h) {
+                int32_t* e = record(tail_item(run, h)) + 4 * (n - 1) + 1;
+                *e += grew;
+                note(e, 1);
+            }
             in.kv_len[r] += grew;
             st.path_kv_tokens += grew;
             st.uniq_kv_tokens += grew;
@@ -1262,13 +1303,14 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
                 for (int32_t h = 0; h < hkv; ++h) {
                     const int32_t i = tail_item(run, h);
                     p->wave_items[i].n_blk = n;
-                    write_record_blocks(p, p->wave_items[i], record(i));
+                    rewrite_blocks(i);
                 }
                 const int32_t T = p->wave_items[tail_item(run, 0)].pad;
                 MergeDesc& md = p->merges[in.merge_of[r]];
                 const int32_t slot = md.slot_off + md.n_slots;
                 md.n_slots += 1;
                 std::memcpy(img + p->off_merges + static_cast<size_t>(in.merge_of[r]) * sizeof(MergeDesc), &md, sizeof(MergeDesc));
+                note(reinterpret_cast<const int32_t*>(img + p->off_merges) + static_cast<size_t>(in.merge_of[r]) * 4, 4);
                 in.spare[r] = 0;
                 const int32_t tok_off = static_cast<int32_t>(p->wtoks.size());
                 p->wtoks.push_back(TokDesc{in.q_indptr[r], tkv::kNoLimit, slot, 0});
@@ -1285,6 +1327,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
                     p->wave_rec[w] = i;
                     p->wave_tiles[w] = T;
                     std::memcpy(img + p->off_wtiles + static_cast<size_t>(w) * sizeof(int32_t), &T, sizeof(int32_t));
+                    note(reinterpret_cast<const int32_t*>(img + p->off_wtiles) + w, 1);
                     in.rec_of.push_back(w);
                     in.run_items[static_cast<size_t>(run) * hkv + h] = i;
                 }
@@ -1304,10 +1347,12 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
         for (int32_t h = 0; h < hkv; ++h) {
             const int32_t i = tail_item(run, h);
             p->wave_items[i].n_blk = n;
-            if (opened)
+            if (opened) {
                 write_record(p, i, reinterpret_cast<uint8_t*>(record(i)));
-            else
-                write_record_blocks(p, p->wave_items[i], record(i));
+                note(record(i), static_cast<int32_t>(sizeof(tkv::WaveDesc) / sizeof(int32_t)));
+            } else {
+                rewrite_blocks(i);
+            }
         }
         in.kv_len[r] += static_cast<int32_t>(added);
         st.path_kv_tokens += added;
@@ -1320,6 +1365,15 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     in.kv_blocks.assign(kv_blocks, kv_blocks + kv_indptr[n_rows]);  // within the reserved capacity
     p->d_ws = nullptr;
     if (in_place) *in_place = 1;
+    return TKV_OK;
+}
+
+TKV_EXPORT int tkv_plan_dirty(const tkv_plan* p, const int32_t** words, int32_t* n, int32_t* complete) {
+    tkv::clear_error();
+    if (!p || !words || !n || !complete) return set_error(TKV_EINVAL, "tkv_plan_dirty: NULL argument");
+    *words = p->dirty.data();
+    *n = static_cast<int32_t>(p->dirty.size());
+    *complete = p->dirty_over ? 0 : 1;
     return TKV_OK;
 }
 

@@ -146,6 +146,25 @@ def test_update_through_decode_steps(G, d):
     assert n_in_place >= 15 and n_opened >= 2
 
 
+def test_dirty_words_carry_every_change():
+    # the words an in-place update lists are all that differ from the image of the last upload (here:
+    # the image at creation, since nothing is uploaded on the CPU): a patch upload is exact
+    tree = DecodeTree(13, W.Shape(12, 2, 128), [1, 15, 16, 255, 256, 40, 90])
+    plan = tree.plan()
+    img0 = np.frombuffer(plan.image()[0], dtype=np.int32).copy()
+    for _ in range(18):
+        tree.step()
+        _, ki, kb, bl = tree.tables()
+        assert plan.update(ki, kb, bl)
+        idx, complete = tkv.tkv_plan_dirty(plan.h)
+        assert complete and len(idx) > 0
+        now = np.frombuffer(plan.image()[0], dtype=np.int32)
+        patched = img0.copy()
+        patched[idx] = now[idx]
+        assert np.array_equal(patched, now)
+        assert set(np.flatnonzero(img0 != now)) <= set(idx.tolist())
+
+
 def test_update_lengths_only_is_byte_identical():
     tree = DecodeTree(3, W.Shape(12, 2, 128), [3, 40, 77, 130, 200, 9])
     plan = tree.plan()

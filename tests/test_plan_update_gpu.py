@@ -1,5 +1,6 @@
 """GPU: a plan carried through decode steps by tkv_plan_update gives, bit for bit, what a plan made
-from scratch gives, and matches the oracle.
+from scratch gives, and matches the oracle; after each in-place update the upload sends only the
+changed descriptor words, and the device copy of the descriptors equals the host image.
 
 Each step grows every decode candidate by one token (new blocks included, some candidates opening
 new chunks); the updated plan and a fresh one run the same attention call on the same pool.  The
@@ -43,14 +44,25 @@ def test_updated_plan_matches_fresh_plan_bitwise(shape, verify):
     kf, vf = W.bf16_bits_to_f32(kbits), W.bf16_bits_to_f32(vbits)
     n_qtok = int(sum(tree.q_lens))
     plan = None
-    n_in_place = 0
+    n_in_place = n_patched = 0
     for step in range(12):
         tree.step()
         t, ki, kb, bl = tree.tables()
         if plan is None:
             plan = tkv.Plan(tree.dims(), tree.q_indptr(), ki, kb, bl)
         else:
-            n_in_place += plan.update(ki, kb, bl)
+            # update, then upload: in place, only the changed descriptor words go to the device
+            in_place = tkv.tkv_plan_update(plan.h, ki, kb, bl)
+            n_in_place += in_place
+            _, complete = tkv.tkv_plan_dirty(plan.h)
+            n_patched += in_place and complete
+            nbytes = tkv.tkv_plan_workspace_bytes(plan.h)
+            if nbytes > plan.workspace.numel():
+                plan.workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+            tkv.tkv_plan_upload(plan.h, plan.workspace)
+            img, _ = plan.image()
+            torch.cuda.synchronize()
+            assert plan.workspace[:len(img)].cpu().numpy().tobytes() == img
         fresh = tkv.Plan(tree.dims(), tree.q_indptr(), ki, kb, bl)
         qbits = W.f32_to_bf16_bits(rng.standard_normal((n_qtok, shape.hq, shape.d)).astype(np.float32))
         qd = _dev(qbits)
@@ -70,4 +82,4 @@ def test_updated_plan_matches_fresh_plan_bitwise(shape, verify):
         assert same
         assert r["finite"] and r["max"] <= MAX_ABS and r["mean"] <= MEAN_ABS and r["lse_max"] <= LSE_ABS
         del fresh
-    assert n_in_place >= 8
+    assert n_in_place >= 8 and n_patched >= 8
