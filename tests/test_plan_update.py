@@ -244,3 +244,36 @@ def test_update_errors_leave_the_plan_unchanged():
     assert L.tkv_plan_update(plan.h, None, None, None, None) == tkv.TKV_EINVAL
     assert plan.update(ki, kb, bl)               # the good tables still go in place
     check_against_fresh(tree, plan, lengths_only=False)
+
+
+def test_update_of_plans_without_wave_tails_plans_again():
+    # G = 32 > 16: every chunk runs as 128-row tiles, no row has a tail the update could grow in place
+    tree = DecodeTree(17, W.Shape(64, 2, 64), [20, 40, 300], verify=False)
+    plan = tree.plan()
+    assert plan.stats["n_items_wave"] == 0 and plan.stats["n_idle_waves"] == 0
+    for _ in range(3):
+        tree.step()
+        _, ki, kb, bl = tree.tables()
+        assert not plan.update(ki, kb, bl)
+        assert plan.image() == tree.plan().image()
+
+
+def test_update_keeps_the_plan_options():
+    tree = DecodeTree(19, W.Shape(8, 2, 64), [5, 70, 250])
+    _, ki, kb, bl = tree.tables()
+    opts = {"wave_max_rows": 8, "tile_min_items": 0}
+    plan = tkv.Plan(tree.dims(), tree.q_indptr(), ki, kb, bl, upload=False, options=opts)
+    tkv.tkv_bm_seal(tree.bm.h, tree.decode[1])          # a table change beyond growth: planned again
+    child, _, _ = tree.bm.extend(tree.decode[1], np.arange(3, dtype=np.int32), True)
+    tree.rows[1] = tree.decode[1] = child
+    tree.step([tree.decode[0]])
+    t, ki, kb, bl = tree.tables()
+    plan.update(ki, kb, bl)
+    fresh = tkv.Plan(tree.dims(), tree.q_indptr(), ki, kb, bl, upload=False, options=opts)
+    assert decode_image(plan) == decode_image(fresh) and plan.stats["n_items"] == fresh.stats["n_items"]
+
+
+def test_update_of_an_empty_plan():
+    plan = tkv.Plan((8, 2, 64, 16, 4), [0], [0], [], [16, 3, 0, 0], upload=False)
+    assert plan.update([0], [], [16, 4, 0, 0])
+    assert plan.stats["n_items"] == 0
