@@ -72,6 +72,9 @@ def _args():
                     help="time only the headline workload (by default the mixed_serving headline is followed by "
                          "beam_decode, step_verify, spec_explosion and spec_prompts, reported under 'configs')")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU baseline sample")
+    ap.add_argument("--no-decode-loop", action="store_true",
+                    help="skip the decode-loop planning measurement (host_ms.decode_loop) of decode workloads, whose "
+                         "own attention launches would otherwise follow the measured ones (profiling runs)")
     ap.add_argument("--kv-copies", type=int, default=0,
                     help="device copies of the K/V pool rotated over the steps (0: enough to defeat the 256 MB MALL)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -818,7 +821,7 @@ def run_attention(a, name, steps, warmup, with_cpu=False, warm=True):
     if ms_step_warm is not None:
         res["warm"] = {"ms_per_step": round(ms_step_warm, 5), "value": round(n_qtok / (ms_step_warm / 1e3), 1),
                        "kv_pool_fits_mall": pool_bytes <= MALL_BYTES}
-    if L.decode:
+    if L.decode and not a.no_decode_loop:
         res["host_ms"]["decode_loop"] = time_plan_updates(wl, device=dev)
     if with_cpu:
         res["cpu_baseline"] = cpu_baseline(a, qbits, kbits, vbits, tables, bl, q_lens)
