@@ -1168,7 +1168,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     };
     bool fits = true;
     size_t n_open = 0;  // new chunks
-    std::vector<uint8_t> dirty;
+    std::vector<uint8_t> touched;  // rows the patch changes
     try {
         if (!in.indexed) index_plan(p);
         for (int32_t r = 0; r < n_rows && fits; ++r) {
@@ -1210,7 +1210,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
                 lengthened.push_back(o);
         }
         if (fits) {  // everything the patch appends to, so that it cannot fail half way
-            dirty.assign(n_rows, 0);
+            touched.assign(n_rows, 0);
             reserve_more(p->wtoks, n_open);
             reserve_more(p->wblks, n_open * tkv::kWaveBlocks);
             reserve_more(p->wave_items, n_open * hkv);
@@ -1262,10 +1262,10 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     };
     tkv_plan_stats& st = p->stats;
     const int64_t flops_per_key = 4ll * s.d * s.hq;
-    for (int32_t r : lengthened) dirty[r] = 1;
-    for (int32_t r : grown) dirty[r] = 1;
+    for (int32_t r : lengthened) touched[r] = 1;
+    for (int32_t r : grown) touched[r] = 1;
     for (int32_t r = 0; r < n_rows; ++r) {
-        if (!dirty[r]) continue;
+        if (!touched[r]) continue;
         const int32_t o0 = in.kv_indptr[r], n_old = in.kv_indptr[r + 1] - o0;
         const int32_t n0 = kv_indptr[r], n_new = kv_indptr[r + 1] - n0;
         int32_t run = in.tail_run[r];
