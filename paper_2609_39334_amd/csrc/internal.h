@@ -88,7 +88,11 @@ struct MergeDesc {
 // that tables only grew, and to plan again when they did not grow in place) and, per row, its tail
 // chunk -- the last chunk of a decode row's private segment when the wave kernel runs it.
 struct PlanInputs {
-    std::vector<int32_t> q_indptr, kv_indptr, kv_blocks, block_len, mult;
+    std::vector<int32_t> q_indptr, block_len, mult;
+    // each row's table: kv_blocks[row_start[r] .. + row_len[r]), with room up to row_cap[r] (a row
+    // that outgrows its room moves to the end of kv_blocks, with room for kRowSlack more)
+    std::vector<int32_t> kv_blocks, row_len, row_cap;
+    std::vector<int64_t> row_start;
     tkv_plan_options opts{};
     bool has_opts = false;
     std::vector<int32_t> kv_len;     // [n_rows]

@@ -106,6 +106,9 @@ struct Chunk {
 // eight (row, KV head) tails, a multiple of kWaveWG, at most kMaxSpareWaves.
 constexpr int32_t kMaxSpareWaves = 512;
 
+// Room a stored row table gets for more blocks when an update moves it (tkv::PlanInputs).
+constexpr int32_t kRowSlack = 16;
+
 // Key blocks per wave below which a wave grid beside a chip-filling set of tile items is made smaller.
 constexpr int64_t kWaveBlocksPerWave = 8;
 
@@ -261,9 +264,10 @@ void clear_plan(tkv_plan* p) {
     p->stats = tkv_plan_stats{};
     if (p->in) {
         tkv::PlanInputs& in = *p->in;
-        for (auto* v : {&in.q_indptr, &in.kv_indptr, &in.kv_blocks, &in.block_len, &in.mult, &in.kv_len, &in.tail_run,
-                        &in.spare, &in.merge_of, &in.owner, &in.run_items, &in.rec_of, &in.free_waves})
+        for (auto* v : {&in.q_indptr, &in.kv_blocks, &in.row_len, &in.row_cap, &in.block_len, &in.mult, &in.kv_len,
+                        &in.tail_run, &in.spare, &in.merge_of, &in.owner, &in.run_items, &in.rec_of, &in.free_waves})
             v->clear();
+        in.row_start.clear();
         in.opts = tkv_plan_options{};
         in.has_opts = false;
         in.indexed = false;
@@ -370,13 +374,18 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         tkv::PlanInputs& in = *p->in;
         if (n_rows > 0) {
             in.q_indptr.assign(q_indptr, q_indptr + n_rows + 1);
-            in.kv_indptr.assign(kv_indptr, kv_indptr + n_rows + 1);
             in.kv_blocks.assign(kv_blocks, kv_blocks + kv_indptr[n_rows]);
+            in.row_start.resize(n_rows);
+            in.row_len.resize(n_rows);
+            for (int32_t r = 0; r < n_rows; ++r) {
+                in.row_start[r] = kv_indptr[r];
+                in.row_len[r] = kv_indptr[r + 1] - kv_indptr[r];
+            }
+            in.row_cap = in.row_len;
             in.block_len.assign(block_len, block_len + s.num_blocks);
             if (multiplicity) in.mult.assign(multiplicity, multiplicity + n_rows);
         } else {
             in.q_indptr.assign(1, 0);
-            in.kv_indptr.assign(1, 0);
             in.block_len.assign(s.num_blocks, 0);
             if (block_len) in.block_len.assign(block_len, block_len + s.num_blocks);
         }
@@ -1115,7 +1124,7 @@ void index_plan(tkv_plan* p) {
     const int32_t n_rows = p->stats.n_rows, hkv = p->shape.hkv;
     in.owner.assign(p->shape.num_blocks, -1);
     for (int32_t r = 0; r < n_rows; ++r)
-        for (int32_t j = in.kv_indptr[r]; j < in.kv_indptr[r + 1]; ++j) {
+        for (int64_t j = in.row_start[r]; j < in.row_start[r] + in.row_len[r]; ++j) {
             int32_t& o = in.owner[in.kv_blocks[j]];
             o = o == -1 || o == r ? r : -2;
         }
@@ -1162,17 +1171,19 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     std::vector<int32_t> grown, lengthened;  // rows with new blocks; rows whose last block grew
     auto unmark = [&]() {
         for (int32_t r : grown)
-            for (int32_t j = kv_indptr[r] + (in.kv_indptr[r + 1] - in.kv_indptr[r]); j < kv_indptr[r + 1]; ++j)
+            for (int32_t j = kv_indptr[r] + in.row_len[r]; j < kv_indptr[r + 1]; ++j)
                 if (kv_blocks[j] >= 0 && kv_blocks[j] < s.num_blocks && in.owner[kv_blocks[j]] == -3 - r)
                     in.owner[kv_blocks[j]] = -1;
     };
     bool fits = true;
-    size_t n_open = 0;  // new chunks
+    size_t n_open = 0;      // new chunks
+    size_t n_moved = 0;     // table entries of rows that outgrow their room
     std::vector<uint8_t> touched;  // rows the patch changes
     try {
         if (!in.indexed) index_plan(p);
         for (int32_t r = 0; r < n_rows && fits; ++r) {
-            const int32_t o0 = in.kv_indptr[r], n_old = in.kv_indptr[r + 1] - o0;
+            const int64_t o0 = in.row_start[r];
+            const int32_t n_old = in.row_len[r];
             const int32_t n0 = kv_indptr[r], n_new = kv_indptr[r + 1] - n0;
             if (n_new < n_old || (n_old > 0 && std::memcmp(in.kv_blocks.data() + o0, kv_blocks + n0, n_old * sizeof(int32_t)))) {
                 fits = false;
@@ -1193,6 +1204,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
             }
             const int32_t room = tkv::kWaveBlocks - p->wave_items[tail_item(in.tail_run[r], 0)].n_blk;
             const int32_t extra = n_new - n_old;
+            if (n_new > in.row_cap[r]) n_moved += static_cast<size_t>(n_new) + kRowSlack;
             if (extra > room) {  // one new chunk at most, and only into the token's free slot
                 if (extra - room > tkv::kWaveBlocks || !in.spare[r] || in.merge_of[r] < 0) fits = false;
                 n_open += 1;
@@ -1203,7 +1215,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
             if (block_len[b] == in.block_len[b]) continue;
             const int32_t o = in.owner[b];
             if (o == -1 || o <= -3) continue;  // in no table, or one of this update's new blocks
-            if (o == -2 || !is_decode(o) || in.tail_run[o] < 0 || in.kv_blocks[in.kv_indptr[o + 1] - 1] != b ||
+            if (o == -2 || !is_decode(o) || in.tail_run[o] < 0 || in.kv_blocks[in.row_start[o] + in.row_len[o] - 1] != b ||
                 block_len[b] < in.block_len[b] || block_len[b] > s.block_size)
                 fits = false;
             else
@@ -1216,7 +1228,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
             reserve_more(p->wave_items, n_open * hkv);
             reserve_more(in.rec_of, n_open * hkv);
             reserve_more(in.run_items, n_open * hkv);
-            reserve_more(in.kv_blocks, kv_indptr[n_rows] - in.kv_blocks.size());
+            reserve_more(in.kv_blocks, n_moved);
             if (p->dirty.capacity() < static_cast<size_t>(p->patch_cap)) p->dirty.reserve(p->patch_cap);
         }
     } catch (...) {
@@ -1266,7 +1278,8 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     for (int32_t r : grown) touched[r] = 1;
     for (int32_t r = 0; r < n_rows; ++r) {
         if (!touched[r]) continue;
-        const int32_t o0 = in.kv_indptr[r], n_old = in.kv_indptr[r + 1] - o0;
+        const int64_t o0 = in.row_start[r];
+        const int32_t n_old = in.row_len[r];
         const int32_t n0 = kv_indptr[r], n_new = kv_indptr[r + 1] - n0;
         int32_t run = in.tail_run[r];
         BlkDesc* wb = &p->wblks[static_cast<size_t>(run) * tkv::kWaveBlocks];
@@ -1354,6 +1367,16 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
                 rewrite_blocks(i);
             }
         }
+        // the row's stored table takes the new blocks (moving to the end if it has no room)
+        if (n_new > in.row_cap[r]) {
+            const int64_t start = static_cast<int64_t>(in.kv_blocks.size());
+            in.kv_blocks.resize(in.kv_blocks.size() + n_new + kRowSlack);  // within the reserved capacity
+            std::memcpy(in.kv_blocks.data() + start, in.kv_blocks.data() + o0, n_old * sizeof(int32_t));
+            in.row_start[r] = start;
+            in.row_cap[r] = n_new + kRowSlack;
+        }
+        std::memcpy(in.kv_blocks.data() + in.row_start[r] + n_old, kv_blocks + n0 + n_old, (n_new - n_old) * sizeof(int32_t));
+        in.row_len[r] = n_new;
         in.kv_len[r] += static_cast<int32_t>(added);
         st.path_kv_tokens += added;
         st.uniq_kv_tokens += added;  // a tail's blocks are its row's alone
@@ -1361,8 +1384,6 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     }
     // (in.block_len is kept for the blocks in the tables, above; a block in no table is skipped by
     // the check whatever its length there)
-    std::memcpy(in.kv_indptr.data(), kv_indptr, (n_rows + 1) * sizeof(int32_t));
-    in.kv_blocks.assign(kv_blocks, kv_blocks + kv_indptr[n_rows]);  // within the reserved capacity
     p->d_ws = nullptr;
     if (in_place) *in_place = 1;
     return TKV_OK;
