@@ -207,7 +207,7 @@ void tile_full(int32_t n, int32_t cap, F f) {
 // The planner's working arrays, kept per thread from one plan to the next (a loop that plans every
 // step then fills memory it already holds).
 struct Scratch {
-    std::vector<int32_t> L, N, path, cover, tail_chunk, slot_next, chunk_run, end_pos, root_last;
+    std::vector<int32_t> L, N, path, cover, tail_chunk, slot_next, chunk_run, end_pos, root_last, grp;
     std::vector<uint8_t> seen;
     std::vector<Node> nodes;
     std::vector<BlkDesc> seg_blks;
@@ -698,8 +698,8 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             }
             struct Wave {
                 int32_t T;
-                int64_t cost;
-                std::vector<int32_t> items;
+                const int32_t* items;  // its items, in the XCD's flat list
+                int32_t n;
             };
             // waves per XCD of each width: shares of the target in proportion to the work (at
             // least one, at most one per item on the XCD), the remainder going to the widths
@@ -736,26 +736,42 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                 double key;
             };
             std::vector<std::vector<Wave>> xcd_waves(kXcds);
+            std::vector<std::vector<int32_t>> xcd_flat(kXcds);
             std::vector<std::vector<std::vector<int32_t>>> xcd_items_t(kXcds, std::vector<std::vector<int32_t>>(tkv::kWaveMaxTiles + 1));
             for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
                 const std::vector<int32_t>& its = by_t[T];
                 if (its.empty()) continue;
-                IdMap gid(its.size());  // (first key block, KV head) -> group
-                std::vector<std::vector<int32_t>> groups;
+                // groups (a chunk's tiles of one KV head) as lists in first-appearance order, built as
+                // offsets into one array; the previous item of a KV head usually shares its group
+                IdMap& gid = sc.gid;  // (first key block, KV head) -> group
+                gid.reset(its.size());
+                std::vector<int32_t>& grp = sc.grp;
+                grp.resize(its.size());
                 std::vector<int64_t> gcost;
-                for (int32_t i : its) {
-                    const ItemDesc& it = p->wave_items[i];
-                    bool fresh = false;
-                    const int32_t g2 = gid.get((static_cast<uint64_t>(it.blk_off) << 8) | static_cast<uint32_t>(it.kvh),
-                                               static_cast<int32_t>(groups.size()), &fresh);
-                    if (fresh) {
-                        groups.emplace_back();
-                        gcost.push_back(0);
+                std::vector<uint64_t> last_key(s.hkv, ~uint64_t{0});
+                std::vector<int32_t> last_group(s.hkv, -1);
+                for (size_t k2 = 0; k2 < its.size(); ++k2) {
+                    const ItemDesc& it = p->wave_items[its[k2]];
+                    const uint64_t key = (static_cast<uint64_t>(it.blk_off) << 8) | static_cast<uint32_t>(it.kvh);
+                    int32_t g2 = last_key[it.kvh] == key ? last_group[it.kvh] : -1;
+                    if (g2 < 0) {
+                        bool fresh = false;
+                        g2 = gid.get(key, static_cast<int32_t>(gcost.size()), &fresh);
+                        if (fresh) gcost.push_back(0);
+                        last_key[it.kvh] = key;
+                        last_group[it.kvh] = g2;
                     }
-                    groups[g2].push_back(i);
+                    grp[k2] = g2;
                     gcost[g2] += cost(it);
                 }
-                std::vector<int32_t> gorder(groups.size());
+                std::vector<int32_t> goff(gcost.size() + 1, 0), gitems(its.size());
+                for (size_t k2 = 0; k2 < its.size(); ++k2) ++goff[grp[k2] + 1];
+                for (size_t g2 = 0; g2 < gcost.size(); ++g2) goff[g2 + 1] += goff[g2];
+                {
+                    std::vector<int32_t> fill(goff.begin(), goff.end() - 1);
+                    for (size_t k2 = 0; k2 < its.size(); ++k2) gitems[fill[grp[k2]]++] = its[k2];
+                }
+                std::vector<int32_t> gorder(gcost.size());
                 std::iota(gorder.begin(), gorder.end(), 0);
                 std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a2, int32_t b2) { return gcost[a2] > gcost[b2]; });
                 using Load = std::pair<int64_t, int32_t>;
@@ -765,7 +781,7 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                     Load l = xheap.top();
                     xheap.pop();
                     auto& dst = xcd_items_t[l.second][T];
-                    dst.insert(dst.end(), groups[g2].begin(), groups[g2].end());
+                    dst.insert(dst.end(), gitems.begin() + goff[g2], gitems.begin() + goff[g2 + 1]);
                     l.first += gcost[g2];
                     xheap.push(l);
                 }
@@ -778,25 +794,36 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
                     for (int32_t k = 0; k < nw; ++k) slots_x.push_back(Slot{T, (k + 0.5) / nw});
                 }
                 std::stable_sort(slots_x.begin(), slots_x.end(), [](const Slot& a2, const Slot& b2) { return a2.key < b2.key; });
-                std::vector<Wave> ws(slots_x.size());
-                for (size_t j = 0; j < slots_x.size(); ++j) ws[j] = Wave{slots_x[j].T, 0, {}};
+                // items to waves longest processing time first, as (wave, item) in the order assigned;
+                // then each wave's items gathered into one flat list per XCD, in that order
+                std::vector<std::pair<int32_t, int32_t>> asg;
                 for (int32_t T = 1; T <= tkv::kWaveMaxTiles; ++T) {
                     auto& items_t = xcd_items_t[x][T];
                     if (items_t.empty()) continue;
                     sort_by_small_key_desc(items_t, tkv::kWaveBlocks, [&](int32_t i) { return p->wave_items[i].n_blk; });
                     using Load = std::pair<int64_t, int32_t>;
                     std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-                    for (size_t j = 0; j < ws.size(); ++j)
-                        if (ws[j].T == T) heap.push({0, static_cast<int32_t>(j)});
+                    for (size_t j = 0; j < slots_x.size(); ++j)
+                        if (slots_x[j].T == T) heap.push({0, static_cast<int32_t>(j)});
                     for (int32_t i : items_t) {
                         Load l = heap.top();
                         heap.pop();
-                        ws[l.second].items.push_back(i);
-                        ws[l.second].cost += cost(p->wave_items[i]);
+                        asg.emplace_back(l.second, i);
                         l.first += cost(p->wave_items[i]);
                         heap.push(l);
                     }
                 }
+                std::vector<int32_t> off(slots_x.size() + 1, 0);
+                for (const auto& a2 : asg) ++off[a2.first + 1];
+                for (size_t j = 0; j < slots_x.size(); ++j) off[j + 1] += off[j];
+                std::vector<int32_t>& flat = xcd_flat[x];
+                flat.resize(asg.size());
+                {
+                    std::vector<int32_t> fill(off.begin(), off.end() - 1);
+                    for (const auto& a2 : asg) flat[fill[a2.first]++] = a2.second;
+                }
+                std::vector<Wave> ws(slots_x.size());
+                for (size_t j = 0; j < slots_x.size(); ++j) ws[j] = Wave{slots_x[j].T, flat.data() + off[j], off[j + 1] - off[j]};
                 xcd_waves[x] = std::move(ws);
             }
             // launch order: workgroup k holds kWaveWG waves of XCD k % 8, in position order; an XCD
@@ -827,12 +854,12 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             // other items follow all first records, as the range [wave_off[w], wave_off[w + 1]).
             p->wave_rec.assign(n_slots_w, -1);
             for (size_t w = 0; w < n_slots_w; ++w)
-                if (slots[w] && !slots[w]->items.empty()) p->wave_rec[w] = slots[w]->items[0];
+                if (slots[w] && slots[w]->n > 0) p->wave_rec[w] = slots[w]->items[0];
             p->wave_off.assign(1, static_cast<int32_t>(n_slots_w));
             for (size_t w = 0; w < n_slots_w; ++w) {
-                const bool busy = slots[w] && !slots[w]->items.empty();
+                const bool busy = slots[w] && slots[w]->n > 0;
                 if (busy)
-                    for (size_t k = 1; k < slots[w]->items.size(); ++k) p->wave_rec.push_back(slots[w]->items[k]);
+                    for (int32_t k = 1; k < slots[w]->n; ++k) p->wave_rec.push_back(slots[w]->items[k]);
                 p->wave_off.push_back(static_cast<int32_t>(p->wave_rec.size()));
                 p->wave_tiles.push_back(busy ? slots[w]->T : 0);
             }
@@ -861,14 +888,23 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             gid.reset(p->items.size());
             std::vector<std::vector<int32_t>> groups;
             std::vector<int64_t> gcost;
+            // items come in runs of one tile per KV head: the previous item of the same KV head is
+            // usually in the same group, found without a lookup
+            std::vector<uint64_t> last_key(s.hkv, ~uint64_t{0});
+            std::vector<int32_t> last_group(s.hkv, -1);
             for (int32_t i = 0; i < static_cast<int32_t>(p->items.size()); ++i) {
                 const ItemDesc& it = p->items[i];
-                bool fresh = false;
-                const int32_t g2 = gid.get((static_cast<uint64_t>(p->blks[it.blk_off].blk) << 8) | static_cast<uint32_t>(it.kvh),
-                                           static_cast<int32_t>(groups.size()), &fresh);
-                if (fresh) {
-                    groups.emplace_back();
-                    gcost.push_back(0);
+                const uint64_t key = (static_cast<uint64_t>(p->blks[it.blk_off].blk) << 8) | static_cast<uint32_t>(it.kvh);
+                int32_t g2 = last_key[it.kvh] == key ? last_group[it.kvh] : -1;
+                if (g2 < 0) {
+                    bool fresh = false;
+                    g2 = gid.get(key, static_cast<int32_t>(groups.size()), &fresh);
+                    if (fresh) {
+                        groups.emplace_back();
+                        gcost.push_back(0);
+                    }
+                    last_key[it.kvh] = key;
+                    last_group[it.kvh] = g2;
                 }
                 groups[g2].push_back(i);
                 gcost[g2] += cost(it);
@@ -882,12 +918,16 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             // group-major: a group's items run together (so that the XCD's L2 holds the keys they
             // share), groups in the order assigned, each group's items longest first
             std::vector<std::vector<int32_t>> xl(kXcds);
+            std::vector<std::pair<int64_t, int32_t>> by_cost;  // (-cost, place in the group): longest first, stable
             for (int32_t g2 : gorder) {
                 Load l = xheap.top();
                 xheap.pop();
-                std::vector<int32_t>& gi = groups[g2];
-                std::stable_sort(gi.begin(), gi.end(), [&](int32_t a2, int32_t b2) { return cost(p->items[a2]) > cost(p->items[b2]); });
-                xl[l.second].insert(xl[l.second].end(), gi.begin(), gi.end());
+                const std::vector<int32_t>& gi = groups[g2];
+                by_cost.clear();
+                for (size_t k2 = 0; k2 < gi.size(); ++k2)
+                    by_cost.emplace_back(-cost(p->items[gi[k2]]), static_cast<int32_t>(k2));
+                std::sort(by_cost.begin(), by_cost.end());
+                for (const auto& bc : by_cost) xl[l.second].push_back(gi[bc.second]);
                 l.first += gcost[g2];
                 xheap.push(l);
             }
