@@ -223,9 +223,11 @@ size_t tkv_plan_workspace_bytes(const tkv_plan* plan);
  * next upload.  Into the workspace of the plan's last upload, after in-place tkv_plan_update calls,
  * only the descriptor words those updates changed are sent (index/value pairs through a region of
  * the workspace, written in by a small kernel on hip_stream); so the caller must not write into
- * the descriptor region between uploads.  The plan must outlive the copy: a destroyed plan's host
- * image is recycled by later plans.  (HIP stages a pageable host source before hipMemcpyAsync
- * returns, which is what the library's own callers rely on.)  EINVAL (size, alignment, NULL), EHIP. */
+ * the descriptor region between uploads.  The library records an event after the copy and waits
+ * for it before the plan's host memory changes or is recycled (tkv_plan_update, the next upload,
+ * tkv_plan_destroy), so a plan may be updated or destroyed right after an upload; those calls may
+ * then wait for the work enqueued on hip_stream before the copy.  EINVAL (size, alignment, NULL),
+ * EHIP. */
 int tkv_plan_upload(tkv_plan* plan, void* d_workspace, size_t bytes, void* hip_stream);
 
 void tkv_plan_destroy(tkv_plan* plan);
@@ -324,7 +326,11 @@ int tkv_verify(const tkv_plan* plan, const void* q, const void* k, const void* v
  *   - Every call on one GPU shares that array: calls that overlap on one GPU (two streams, or two
  *     threads) race and give undefined results.  Calls ordered on one stream are safe.  Nothing in
  *     the array needs to start at zero, and a call reads nothing that an earlier call left there.
- *   - The plan must outlive the copy, as for tkv_plan_upload.
+ *   - A plan that has been uploaded once has an event: the copy is recorded with it, and the plan
+ *     may be updated or destroyed right after the call, as after tkv_plan_upload.  A plan never
+ *     uploaded has none (creating it would allocate): it must then not be updated or destroyed
+ *     before hip_stream has passed the call (HIP stages a pageable source before hipMemcpyAsync
+ *     returns, which the library's own tests rely on).
  * EINVAL (NULL plan or tensors, plan too large), EHIP (symbol lookup, copy or launch failure). */
 #define TKV_NOALLOC_MAX_BYTES ((size_t)64 << 20)
 int tkv_verify_noalloc(const tkv_plan* plan, const void* q, const void* k, const void* v, void* o,

@@ -937,9 +937,31 @@ __global__ __launch_bounds__(256) void patch_apply(const int2* __restrict__ pair
 
 namespace tkv {
 
+void wait_copies(const tkv_plan* p) {
+    if (p->copy_pending) {
+        (void)hipEventSynchronize(static_cast<hipEvent_t>(p->copy_event));
+        p->copy_pending = false;
+    }
+}
+
+// Records the completion of the copies just enqueued from the plan's host memory.
+static int record_copy(const tkv_plan* p, hipStream_t st, const char* fn) {
+    if (!p->copy_event) {
+        hipEvent_t e;
+        const hipError_t rc = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+        if (rc != hipSuccess) return set_error(TKV_EHIP, "%s: hipEventCreateWithFlags: %s", fn, hipGetErrorString(rc));
+        p->copy_event = e;
+    }
+    const hipError_t rc = hipEventRecord(static_cast<hipEvent_t>(p->copy_event), st);
+    if (rc != hipSuccess) return set_error(TKV_EHIP, "%s: hipEventRecord: %s", fn, hipGetErrorString(rc));
+    p->copy_pending = true;
+    return TKV_OK;
+}
+
 int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream) {
     (void)bytes;
     const hipStream_t st = static_cast<hipStream_t>(stream);
+    wait_copies(p);  // the pair staging below may still be read by the last upload
     // Into the workspace that holds the image of the last upload, only the words in-place updates
     // changed since: (index, value) pairs copied to the patch region, then written in by patch_apply.
     const size_t n_words = p->desc_bytes / sizeof(int32_t);
@@ -973,6 +995,8 @@ int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream) {
         const hipError_t e = hipMemcpyAsync(d_ws, p->image.get(), p->desc_bytes, hipMemcpyHostToDevice, st);
         if (e != hipSuccess) return set_error(TKV_EHIP, "tkv_plan_upload: hipMemcpyAsync: %s", hipGetErrorString(e));
     }
+    const int rc = record_copy(p, st, "tkv_plan_upload");
+    if (rc != TKV_OK) return rc;
     p->d_ws = d_ws;
     p->ws_image = d_ws;
     p->dirty.clear();
@@ -1100,6 +1124,12 @@ TKV_EXPORT int tkv_verify_noalloc(const tkv_plan* p, const void* q, const void* 
     if (p->desc_bytes) {
         const hipError_t e = hipMemcpyAsync(ws, p->image.get(), p->desc_bytes, hipMemcpyHostToDevice, st);
         if (e != hipSuccess) return tkv::set_error(TKV_EHIP, "tkv_verify_noalloc: hipMemcpyAsync: %s", hipGetErrorString(e));
+        // the copy's completion is recorded with the plan's event if an upload made one (creating
+        // one here would allocate)
+        if (p->copy_event) {
+            rc = tkv::record_copy(p, st, "tkv_verify_noalloc");
+            if (rc != TKV_OK) return rc;
+        }
     }
     return tkv::launch_ws(p, ws, q, k, v, o, lse, st);
 }
@@ -1112,6 +1142,8 @@ static void free_events(const tkv_plan* p) {
 
 tkv_plan::~tkv_plan() {
     free_events(this);
+    tkv::wait_copies(this);
+    if (copy_event) (void)hipEventDestroy(static_cast<hipEvent_t>(copy_event));
     tkv::give_image(std::move(image), image_cap);
 }
 

@@ -152,6 +152,10 @@ struct tkv_plan {
     int32_t patch_cap = 0;
     tkv_plan_stats stats{};
     std::unique_ptr<tkv::PlanInputs> in;  // for tkv_plan_update
+    // The last copy from this plan's host memory (upload, no-allocation call): an event recorded on
+    // the stream after it, waited for before that memory is changed, reused or recycled.
+    mutable void* copy_event = nullptr;
+    mutable bool copy_pending = false;
     // instrumentation: 3 HIP events per recorded call (see tkv_plan_profile)
     mutable int32_t prof_max = 0;
     mutable int32_t prof_n = 0;
@@ -169,4 +173,6 @@ void give_image(std::unique_ptr<uint8_t[]> image, size_t cap);
 int launch_attention(const tkv_plan* p, const void* q, const void* k, const void* v, void* o,
                      float* lse, void* stream);
 int upload(tkv_plan* p, void* d_ws, size_t bytes, void* stream);
+// Waits until the last copy from the plan's host memory has completed (attn.hip).
+void wait_copies(const tkv_plan* p);
 }  // namespace tkv

@@ -230,6 +230,7 @@ constexpr size_t kPooledPlans = 2;
 // Every field back to a new plan's value; vectors keep their storage.  (The field list is
 // tkv_plan's; swap_contents below names the same fields.)
 void clear_plan(tkv_plan* p) {
+    tkv::wait_copies(p);  // its image and pair staging go back for reuse
     p->shape = tkv_shape{};
     p->group = 1;
     p->all_decode = true;
@@ -1201,6 +1202,7 @@ TKV_EXPORT int tkv_plan_update(tkv_plan* p, const int32_t* kv_indptr, const int3
     if (n_rows > 0 && kv_indptr[n_rows] > 0 && !kv_blocks) return set_error(TKV_EINVAL, "tkv_plan_update: kv_blocks is NULL");
     auto is_decode = [&](int32_t r) { return in.q_indptr[r + 1] - in.q_indptr[r] == 1; };
     auto tail_item = [&](int32_t run, int32_t h) { return in.run_items[static_cast<size_t>(run) * hkv + h]; };
+    tkv::wait_copies(p);  // the image is about to change (or move, when planned again)
 
     // ------------------------------------------------ can the plan take the new tables in place?
     // Every row keeps its blocks and may append new ones; a block changes length only as the last

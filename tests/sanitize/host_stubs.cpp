@@ -9,6 +9,7 @@ int launch_attention(const tkv_plan*, const void*, const void*, const void*, voi
     return set_error(TKV_EHIP, "attention: host-only build, no device");
 }
 int upload(tkv_plan*, void*, size_t, void*) { return set_error(TKV_EHIP, "tkv_plan_upload: host-only build, no device"); }
+void wait_copies(const tkv_plan*) {}  // no copies without a device
 }  // namespace tkv
 
 tkv_plan::~tkv_plan() { tkv::give_image(std::move(image), image_cap); }

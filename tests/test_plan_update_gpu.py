@@ -83,3 +83,28 @@ def test_updated_plan_matches_fresh_plan_bitwise(shape, verify):
         assert r["finite"] and r["max"] <= MAX_ABS and r["mean"] <= MEAN_ABS and r["lse_max"] <= LSE_ABS
         del fresh
     assert n_in_place >= 8 and n_patched >= 8
+
+
+def test_plan_destroyed_right_after_upload():
+    # the library waits for the copy before a destroyed plan's host image is recycled: the workspace
+    # holds the first plan's descriptors even though the next plan reuses its image at once
+    import paper_2609_39334_amd as tkv
+    tree = DecodeTree(23, W.Shape(12, 2, 128), [3, 70, 255, 256, 31], num_blocks=2048)
+    _, ki, kb, bl = tree.tables()
+    dims, qi = tree.dims(), tree.q_indptr()
+    h = tkv.tkv_plan_create(dims, qi, ki, kb, bl)
+    img, _ = tkv.tkv_plan_image(h)
+    ws = torch.empty(tkv.tkv_plan_workspace_bytes(h), dtype=torch.uint8, device="cuda")
+    busy = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    for _ in range(8):             # queue work ahead of the copy
+        busy.add_(1)
+    tkv.tkv_plan_upload(h, ws)
+    tkv.tkv_plan_destroy(h)
+    tree.step()
+    _, ki2, kb2, bl2 = tree.tables()
+    h2 = tkv.tkv_plan_create(dims, qi, ki2, kb2, bl2)   # takes the recycled image and rewrites it
+    img2, _ = tkv.tkv_plan_image(h2)
+    torch.cuda.synchronize()
+    assert img2 != img
+    assert ws[:len(img)].cpu().numpy().tobytes() == img
+    tkv.tkv_plan_destroy(h2)
