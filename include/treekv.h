@@ -197,7 +197,7 @@ int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_ind
 /* Work placement, for tests and tuning: which kernel path and grid the planner uses.  The results
  * do not depend on it (every placement computes the same attention up to fp32 summation order).
  * A negative field keeps the default.
- *   wave_max_rows    widest shared chunk, in query rows, kept on the wave kernel (default 96)
+ *   wave_max_rows    widest shared chunk, in query rows, kept on the wave kernel (default 32)
  *   tile_min_items   wider chunks go to 128-row tiles only if they make at least this many items
  *                    (default 0)
  *   waves            size of the wave grid (default 2048, less the 4 waves of each workgroup slot

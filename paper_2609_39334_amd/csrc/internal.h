@@ -27,7 +27,7 @@ constexpr int kItemRow = 1;     // tile of one row's tokens over its whole path 
 constexpr int kItemWave = 2;    // tile of <= 16 T rows over one segment chunk (wave kernel)
 constexpr int kWaveRows = 16;   // query rows of one MFMA column tile of the wave kernel
 constexpr int kWaveMaxTiles = 2;  // column tiles a wave contracts against each K/V block
-constexpr int kWaveMaxRows = 96;  // widest chunk (query rows) the wave kernel takes; wider ones use 128-row tiles
+constexpr int kWaveMaxRows = 32;  // widest chunk (query rows) the wave kernel takes; wider ones use 128-row tiles
 constexpr int kTileMinItems = 0;  // wide chunks go to the tile kernel only if they make this many items
 constexpr int kWaveBlocks = 16; // key blocks of a wave-kernel item
 constexpr int kWaveToks = 16;   // token slots of a wave-kernel record (a wave tile holds 16 T / G tokens,

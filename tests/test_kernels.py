@@ -151,7 +151,7 @@ def test_shared_chunks_on_tile_kernel(seed, hq, hkv, d):
 
 @pytest.mark.parametrize("seed,hq,hkv,d", [(17, 12, 2, 128), (20, 8, 1, 64)])
 def test_wide_chunks_on_wave_kernel(seed, hq, hkv, d):
-    # chunks read by more than 96 query rows stay on the wave kernel, split into many 32-row tiles
+    # chunks read by more than 32 query rows stay on the wave kernel, split into many 32-row tiles
     # over the same blocks (by default they go to 128-row tile items)
     wl = W.random_tree(seed, W.Shape(hq, hkv, d), n_roots=2, depth=3, max_branch=5, max_step=40)
     b, st = compare(wl, 0, options={"tile_min_items": 1000000})
@@ -162,8 +162,9 @@ def test_wide_chunks_on_wave_kernel(seed, hq, hkv, d):
 def test_small_wave_grids(waves):
     # a wave grid much smaller than the item count: long per-wave lists, items crossing into the
     # next item's first blocks many times per wave
+    # (chunks of up to 96 rows on the wave kernel, so that there are many wave items)
     wl = W.random_tree(20, W.Shape(12, 2, 128), n_roots=4, depth=3, max_branch=3, max_step=70)
-    b, st = compare(wl, 0, options={"waves": waves})
+    b, st = compare(wl, 0, options={"waves": waves, "wave_max_rows": 96})
     assert 0 < st["n_waves"] < st["n_items_wave"]            # waves walk lists of several items
 
 

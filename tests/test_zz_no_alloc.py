@@ -76,7 +76,9 @@ def test_noalloc_refuses_a_plan_larger_than_its_array():
     b = realize_native(wl)[1]
     s = wl.shape
     qi, ki, kb = b.arrays()
-    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, b.block_len, b.mult, upload=False)
+    # (chunks of up to 96 rows on the wave kernel: more partial slots, a workspace of about 71 MB)
+    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, b.block_len, b.mult, upload=False,
+                    options={"wave_max_rows": 96})
     assert tkv.tkv_plan_workspace_bytes(plan.h) > tkv.TKV_NOALLOC_MAX_BYTES
     t = torch.zeros((4, s.hq, s.d), dtype=torch.bfloat16, device="cuda")
     o = torch.full((4, s.hq, s.d), 3.0, dtype=torch.bfloat16, device="cuda")
