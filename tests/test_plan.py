@@ -154,6 +154,32 @@ def test_plan_covers_each_path_exactly_once(name):
         assert 0 < n_tile < 512 and 4 * n_tile + st["n_waves"] - st["n_idle_waves"] <= 2048
 
 
+@pytest.mark.parametrize("options,max_wave_rows", [(None, 32), ({"wave_max_rows": 96}, 96)])
+def test_chunks_route_by_their_query_rows(options, max_wave_rows):
+    # a chunk read by at most wave_max_rows query rows (32 by default) goes to the wave grid; a wider
+    # one to 128-row tile items, which together hold every one of its tokens
+    wl = W.spec_explosion(0)
+    b = realize_native(wl)[0]
+    s = wl.shape
+    G = s.hq // s.hkv
+    qi, ki, kb = b.arrays()
+    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, wl.num_blocks), qi, ki, kb, b.block_len, b.mult, upload=False,
+                    options=options)
+    v = plan.view()
+    chunk_toks, n_wave = {}, 0
+    for kvh, tok_off, n_tok, blk_off, n_blk, pos0, kind, _ in v["items"]:
+        if kind == 2:                                  # wave item: one tile of one chunk
+            assert n_tok * G <= max_wave_rows
+            n_wave += 1
+        else:
+            assert kind == 0 and n_tok * G <= 128
+            chunk_toks[(kvh, blk_off, n_blk)] = chunk_toks.get((kvh, blk_off, n_blk), 0) + n_tok
+    assert n_wave > 0 and chunk_toks
+    assert all(t * G > max_wave_rows for t in chunk_toks.values())
+    # spec_explosion's 16-candidate subtrees (96 query rows) change sides between the two thresholds
+    assert any(t * G == 96 for t in chunk_toks.values()) == (max_wave_rows < 96)
+
+
 def test_plan_rejects_bad_input():
     ok = dict(shape=(8, 2, 64, 16, 4), q_indptr=[0, 1], kv_indptr=[0, 2], kv_blocks=[0, 1], block_len=[16, 3, 0, 0])
     tkv.tkv_plan_destroy(tkv.tkv_plan_create(**ok))
