@@ -104,6 +104,25 @@ def measure_copy_gbs(torch, dev, stream, nbytes=1 << 30, reps=10):
     return 2 * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
 
 
+def measure_gemm_tflops(torch, dev, stream, n=8192, reps=20):
+    """Flop rate of a plain n x n x n bf16 matrix product in the vendor library (torch.matmul), timed in
+    the same process: the dense MFMA rate a tuned library reaches on this machine at the clock the chip
+    sustains under MFMA load, reported beside the nominal 2.5 PFLOP/s."""
+    a = torch.randn((n, n), dtype=torch.bfloat16, device=dev)
+    b = torch.randn((n, n), dtype=torch.bfloat16, device=dev)
+    c = torch.empty((n, n), dtype=torch.bfloat16, device=dev)
+    for _ in range(3):
+        torch.matmul(a, b, out=c)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        torch.matmul(a, b, out=c)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return 2.0 * n ** 3 * reps / (e0.elapsed_time(e1) / 1e3) / 1e12
+
+
 def calibration_copy(torch, dev):
     """One plain 256 MiB device-to-device copy: a kernel of known size for the PMC byte counters."""
     src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -855,6 +874,7 @@ def main():
     head = run_attention(a, a.workload, a.steps, a.warmup, with_cpu=not a.no_cpu)
     torch.cuda.synchronize()
     stream_gbs = measure_copy_gbs(torch, torch.device("cuda:0"), torch.cuda.current_stream())
+    gemm_tflops = measure_gemm_tflops(torch, torch.device("cuda:0"), torch.cuda.current_stream())
     out = {
         "metric": "candidate-tokens/s and % HBM roofline (unique KV bytes), tree decode + verify",
         "value": head["value"],
@@ -871,6 +891,9 @@ def main():
         "stream_copy_gbs": round(stream_gbs, 1),
         "unique_kv_frac_of_stream_copy": round(head["config"]["unique_kv_bytes"] / (head["kernel_us"]["attn_fwd"] / 1e6)
                                                / 1e9 / stream_gbs, 4),
+        "gemm_bf16_tflops": round(gemm_tflops, 1),
+        "mfma_achieved_frac_of_gemm": (round(head["roofline"]["achieved"] / gemm_tflops, 4)
+                                       if head["roofline"]["bound"] == "mfma" else None),
         "logical_candidate_tokens_per_s": head["logical_candidate_tokens_per_s"],
         "kernel_us": head["kernel_us"], "shared_pass": head["shared_pass"], "plan": head["plan"],
         "host_ms": head["host_ms"],
