@@ -205,9 +205,12 @@ int tkv_plan_create(const tkv_shape* shape, int32_t n_rows, const int32_t* q_ind
  *   tile8_max_items  a plan of at most this many tile items and no wave-grid work runs them as
  *                    8-wave workgroups (default 256)
  *   wide_chunk_blocks  longest key run, in blocks, of a shared chunk on the 128-row tiles
- *                    (default 64) */
+ *                    (default 64)
+ *   fold_blocks      a shared segment on the 128-row tiles of at most this many blocks, whose child
+ *                    segments all go to the 128-row tiles and hold all of its rows, is read as the
+ *                    head of each child's key run instead of on its own (default 16; 0: never) */
 typedef struct {
-    int32_t wave_max_rows, tile_min_items, waves, tile8_max_items, wide_chunk_blocks;
+    int32_t wave_max_rows, tile_min_items, waves, tile8_max_items, wide_chunk_blocks, fold_blocks;
 } tkv_plan_options;
 
 /* tkv_plan_create with placement options (opts may be NULL: all defaults). */

@@ -35,7 +35,7 @@ class tkv_shape(ctypes.Structure):
 
 class tkv_plan_options(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("wave_max_rows", "tile_min_items", "waves", "tile8_max_items",
-                                              "wide_chunk_blocks")]
+                                              "wide_chunk_blocks", "fold_blocks")]
 
 
 class tkv_plan_stats(ctypes.Structure):

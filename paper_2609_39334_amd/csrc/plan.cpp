@@ -44,6 +44,7 @@ namespace {
 
 constexpr int kChunkBlocks = 16;      // longest key run of a narrow shared item (256 tokens)
 constexpr int kChunkBlocksWide = 64;  // longest key run of a wide (128-row tile) shared item
+constexpr int kFoldBlocks = 16;       // longest shared segment folded into its children's key runs
 static_assert(kChunkBlocks <= tkv::kWaveBlocks, "a wave item holds its key blocks in one record");
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -208,7 +209,8 @@ void tile_full(int32_t n, int32_t cap, F f) {
 // step then fills memory it already holds).
 struct Scratch {
     std::vector<int32_t> L, N, path, cover, tail_chunk, slot_next, chunk_run, end_pos, root_last, grp;
-    std::vector<uint8_t> seen;
+    std::vector<uint8_t> seen, folded, absorbed;
+    std::vector<int32_t> kid_off, kids, kid_fill;
     std::vector<Node> nodes;
     std::vector<BlkDesc> seg_blks;
     std::vector<ItemDesc> ordered;
@@ -508,6 +510,58 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
             const int64_t min_items = opt(&tkv_plan_options::tile_min_items, tkv::kTileMinItems);
             if (wide_items < min_items) wave_max_rows = int64_t{1} << 40;
         }
+        // A short shared segment on the 128-row tiles whose children all go there too, and which
+        // holds no row beyond theirs, is read by each child as the head of the child's own key run:
+        // its blocks cost one more tile item's worth of reads per child, but its own tile items (short,
+        // so mostly start-up) and every token's partial from it go away.  One level only: a segment
+        // that takes its parent's blocks is not folded into its own children.
+        const int64_t fold_blocks = opt(&tkv_plan_options::fold_blocks, kFoldBlocks);
+        std::vector<uint8_t>& folded = sc.folded;
+        folded.assign(segs.size(), 0);
+        if (fold_blocks > 0 && G <= tkv::kWaveRows && !segs.empty()) {
+            auto rows_of = [&](const Segment& sg) {
+                int64_t n = 0;
+                for (int32_t r : sg.rows) n += static_cast<int64_t>(L[r]) * G;
+                return n;
+            };
+            // children of each segment (segments are numbered parents first)
+            std::vector<int32_t>& kid_off = sc.kid_off;
+            std::vector<int32_t>& kids = sc.kids;
+            kid_off.assign(segs.size() + 1, 0);
+            for (const Segment& sg : segs) {
+                const int32_t par = nodes[sg.nodes[0]].parent;
+                if (par >= 0) kid_off[nodes[par].seg + 1] += 1;
+            }
+            for (size_t i = 0; i < segs.size(); ++i) kid_off[i + 1] += kid_off[i];
+            kids.assign(kid_off[segs.size()], 0);
+            std::vector<int32_t>& fill = sc.kid_fill;
+            fill.assign(kid_off.begin(), kid_off.end() - 1);
+            for (int32_t c = 0; c < static_cast<int32_t>(segs.size()); ++c) {
+                const int32_t par = nodes[segs[c].nodes[0]].parent;
+                if (par >= 0) kids[fill[nodes[par].seg]++] = c;
+            }
+            std::vector<uint8_t>& absorbed = sc.absorbed;
+            absorbed.assign(segs.size(), 0);
+            for (int32_t p = 0; p < static_cast<int32_t>(segs.size()); ++p) {
+                Segment& sp = segs[p];
+                if (absorbed[p] || sp.rows.size() < 2 || static_cast<int64_t>(sp.nodes.size()) > fold_blocks ||
+                    kid_off[p] == kid_off[p + 1] || rows_of(sp) <= wave_max_rows)
+                    continue;
+                size_t kid_rows = 0;
+                bool wide_kids = true;
+                for (int32_t k = kid_off[p]; k < kid_off[p + 1]; ++k) {
+                    kid_rows += segs[kids[k]].rows.size();
+                    wide_kids = wide_kids && rows_of(segs[kids[k]]) > wave_max_rows;
+                }
+                if (!wide_kids || kid_rows != sp.rows.size()) continue;
+                for (int32_t k = kid_off[p]; k < kid_off[p + 1]; ++k) {
+                    std::vector<int32_t>& cn = segs[kids[k]].nodes;
+                    cn.insert(cn.begin(), sp.nodes.begin(), sp.nodes.end());
+                    absorbed[kids[k]] = 1;
+                }
+                folded[p] = 1;
+            }
+        }
         std::vector<Chunk> chunks;
         std::vector<BlkDesc>& seg_blks = sc.seg_blks;  // each segment's key blocks, in path order
         seg_blks.clear();
@@ -515,7 +569,9 @@ TKV_EXPORT int tkv_plan_create_ex(const tkv_shape* shape, int32_t n_rows, const 
         cover.assign(st.n_qtok, 0);
         std::vector<int32_t>& tail_chunk = sc.tail_chunk;  // a decode row's tail chunk (see tkv::PlanInputs)
         tail_chunk.assign(n_rows, -1);
-        for (const Segment& sg : segs) {
+        for (size_t si = 0; si < segs.size(); ++si) {
+            const Segment& sg = segs[si];
+            if (folded[si]) continue;
             if (sg.rows.size() > 1) st.n_shared_segments += 1;
             const int32_t nb = static_cast<int32_t>(sg.nodes.size());
             const int32_t seg_blk_off = static_cast<int32_t>(seg_blks.size());

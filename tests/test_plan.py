@@ -83,6 +83,31 @@ def test_plan_executes_to_oracle(seed, G, d):
     np.testing.assert_allclose(l, l_ref, atol=1e-11)
 
 
+@pytest.mark.parametrize("seed,G,d", [(40, 2, 64), (41, 4, 128), (42, 6, 128), (43, 1, 64)])
+def test_folded_segments_execute_to_oracle(seed, G, d):
+    # every shared chunk on the 128-row tiles (wave_max_rows 2) and short segments folded into their
+    # children's key runs: fewer partial slots, the same attention
+    shape = W.Shape(G * 2, 2, d)
+    wl = W.random_tree(seed, shape, n_roots=2, depth=4, max_branch=3, max_step=40, p_verify=0.3)
+    b = realize_native(wl)[0]
+    s = wl.shape
+    qi, ki, kb = b.arrays()
+    dims = (s.hq, s.hkv, s.d, s.block_size, wl.num_blocks)
+    base = dict(wave_max_rows=2, tile_min_items=0)
+    plain = tkv.Plan(dims, qi, ki, kb, b.block_len, b.mult, upload=False, options=dict(base, fold_blocks=0))
+    fold = tkv.Plan(dims, qi, ki, kb, b.block_len, b.mult, upload=False, options=dict(base, fold_blocks=1000))
+    assert fold.stats["n_slots"] < plain.stats["n_slots"]
+    assert fold.stats["n_shared_segments"] < plain.stats["n_shared_segments"]
+    ob = realize_oracle(wl)[0]
+    k, v = wl.kv_values()
+    q = wl.q_values(0, b.n_qtok)
+    kf, vf, qf = _f32(k), _f32(v), _f32(q)
+    o_ref, l_ref = oracle.attention(qf, kf, vf, ob.tables, ob.block_len, ob.q_lens)
+    o, l = execute_plan(fold.view(), (shape.hq, shape.hkv, shape.d), qf, kf, vf, b.n_qtok)
+    np.testing.assert_allclose(o, o_ref, atol=1e-11)
+    np.testing.assert_allclose(l, l_ref, atol=1e-11)
+
+
 def test_plan_tiny_decode_structure():
     b, plan = _run(W.tiny_decode(0))
     st = plan.stats
