@@ -149,6 +149,16 @@ def test_shared_chunks_on_tile_kernel(seed, hq, hkv, d):
     assert st["n_items_shared"] - st["n_items_wave"] > 0     # shared chunks did run on the tile kernel
 
 
+@pytest.mark.parametrize("seed,hq,hkv,d", [(40, 4, 2, 64), (42, 12, 2, 128)])
+def test_folded_segments_on_tile_kernel(seed, hq, hkv, d):
+    # every shared chunk on the 128-row tiles and every short segment folded into its children's key
+    # runs (a child's tiles read the parent's blocks, then its own)
+    wl = W.random_tree(seed, W.Shape(hq, hkv, d), n_roots=2, depth=4, max_branch=3, max_step=40, p_verify=0.3)
+    b, st = compare(wl, 0, options={"wave_max_rows": 2, "tile_min_items": 0, "fold_blocks": 1000})
+    b0, st0 = compare(wl, 0, options={"wave_max_rows": 2, "tile_min_items": 0, "fold_blocks": 0})
+    assert st["n_slots"] < st0["n_slots"]
+
+
 @pytest.mark.parametrize("seed,hq,hkv,d", [(17, 12, 2, 128), (20, 8, 1, 64)])
 def test_wide_chunks_on_wave_kernel(seed, hq, hkv, d):
     # chunks read by more than 32 query rows stay on the wave kernel, split into many 32-row tiles
