@@ -178,6 +178,44 @@ def test_small_wave_grids(waves):
     assert 0 < st["n_waves"] < st["n_items_wave"]            # waves walk lists of several items
 
 
+@pytest.mark.parametrize("options", [None, {"wave_max_rows": 8, "tile_min_items": 0}])
+def test_blocks_past_4gib_of_pool(options):
+    # block ids whose K/V start more than 4 GiB into each pool (64-bit offsets in every path): a
+    # random tree's blocks moved to the top of pools of 4.6 GiB each, the blocks below NaN
+    import paper_2609_39334_amd as tkv
+    wl = W.random_tree(70, W.Shape(12, 2, 128), n_roots=2, depth=3, max_branch=3, max_step=60)
+    b = realize_native(wl)[0]
+    ob = realize_oracle(wl)[0]
+    s = wl.shape
+    k, v = wl.kv_values()
+    blk_bytes = s.hkv * s.block_size * s.d * 2
+    base = (4 << 30) // blk_bytes + 4096                        # first moved block: past 4 GiB
+    nb_big = base + wl.num_blocks
+    assert nb_big * blk_bytes > (4 << 30) + wl.num_blocks * blk_bytes
+    kd = torch.full((nb_big, s.hkv, s.block_size, s.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    vd = torch.full_like(kd, float("nan"))
+    kd[base:] = _dev(k)
+    vd[base:] = _dev(v)
+    bl = np.zeros(nb_big, dtype=np.int32)
+    bl[base:] = b.block_len
+    qi, ki, kb = b.arrays()
+    q = wl.q_values(0, b.n_qtok)
+    plan = tkv.Plan((s.hq, s.hkv, s.d, s.block_size, nb_big), qi, ki, np.asarray(kb, dtype=np.int32) + base, bl,
+                    b.mult, options=options)
+    o = torch.full((b.n_qtok, s.hq, s.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((b.n_qtok, s.hq), float("nan"), dtype=torch.float32, device="cuda")
+    (plan.decode if b.decode else plan.verify)(_dev(q), kd, vd, o, lse)
+    torch.cuda.synchronize()
+    st = plan.stats
+    del plan, kd, vd
+    r = oracle_check(q, W.bf16_bits_to_f32(k), W.bf16_bits_to_f32(v), ob.tables, ob.block_len, ob.q_lens,
+                     o.float().cpu().numpy(), lse.cpu().numpy())
+    _log(f"    pool of {nb_big} blocks; max {r['max']:.2e} mean {r['mean']:.2e} lse {r['lse_max']:.2e}; items {st['n_items']}")
+    assert r["finite"] and r["max"] <= MAX_ABS and r["mean"] <= MEAN_ABS and r["lse_max"] <= LSE_ABS
+    if options:
+        assert st["n_items_shared"] - st["n_items_wave"] > 0    # shared chunks on the tile kernel too
+
+
 def test_empty_plan_on_gpu():
     import paper_2609_39334_amd as tkv
     plan = tkv.Plan((8, 2, 64, 16, 4), [0], [0], [], [16, 3, 0, 0])
