@@ -115,6 +115,26 @@ def test_verify_long_steps_and_single_token_rows():
     compare(wl, 0)
 
 
+@pytest.mark.parametrize("options", [None, {"wave_max_rows": 8, "tile_min_items": 0}])
+def test_long_context(options):
+    # a 40,000-token shared context (2,500 blocks: 157 wave chunks, or 40 wide chunks on the tiles, so
+    # every decode token merges that many partials), under it decode candidates with private steps and
+    # verify candidates whose steps of 54-76 tokens walk the whole context as row items
+    wl = W.Workload("long", W.Shape(16, 2, 128), 13)
+    rt = np.random.default_rng(9)
+    root = wl.extend(-1, rt.integers(0, 1000, 40000), True)
+    cands = []
+    for i in range(6):
+        h = wl.extend(root, rt.integers(0, 1000, int(rt.integers(1, 200))), i % 2 == 1)
+        cands.append((h, int(rt.integers(100, 301)) if i % 2 == 1 else 1))
+    # the verify candidates' q_len is their own step's length
+    cands = [(h, q if q == 1 else len(wl.events[h].tokens)) for h, q in cands]
+    wl.launch("long", cands)
+    wl.finalize()
+    b, st = compare(wl, 0, options=options)
+    assert st["n_merge"] > 0 and st["n_items_row"] > 0
+
+
 @pytest.mark.parametrize("name", ["beam_decode", "step_verify", "spec_prompts"])
 def test_full_size_every_row(name):
     compare(W.CONFIGS[name](0), 0)
