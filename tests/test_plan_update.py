@@ -258,6 +258,26 @@ def test_update_of_plans_without_wave_tails_plans_again():
         assert plan.image() == tree.plan().image()
 
 
+def test_update_with_folded_segments():
+    # G = 1 and wave_max_rows 2: each root (6 rows) and its sealed steps (3 rows each) go to the tiles,
+    # the root folded into its steps' key runs; the one-row tails stay on the wave grid and grow in place
+    tails = [1, 15, 16, 17, 250, 251, 255, 256, 240, 31, 32, 33]
+    tree = DecodeTree(31, W.Shape(2, 2, 64), tails, verify=False)
+    opts = {"wave_max_rows": 2, "tile_min_items": 0, "fold_blocks": 16}
+    _, ki, kb, bl = tree.tables()
+    plan = tkv.Plan(tree.dims(), tree.q_indptr(), ki, kb, bl, upload=False, options=opts)
+    unfolded = tkv.Plan(tree.dims(), tree.q_indptr(), ki, kb, bl, upload=False, options=dict(opts, fold_blocks=0))
+    assert plan.stats["n_shared_segments"] < unfolded.stats["n_shared_segments"]
+    n_in_place = 0
+    for step in range(12):
+        tree.step()
+        _, ki, kb, bl = tree.tables()
+        n_in_place += plan.update(ki, kb, bl)
+        fresh = tkv.Plan(tree.dims(), tree.q_indptr(), ki, kb, bl, upload=False, options=opts)
+        assert decode_image(plan) == decode_image(fresh)
+    assert n_in_place >= 8
+
+
 def test_update_keeps_the_plan_options():
     tree = DecodeTree(19, W.Shape(8, 2, 64), [5, 70, 250])
     _, ki, kb, bl = tree.tables()
