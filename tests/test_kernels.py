@@ -94,7 +94,8 @@ def test_tiny_decode_full():
 
 
 @pytest.mark.parametrize("seed,hq,hkv,d", [(0, 8, 2, 64), (1, 12, 2, 128), (2, 28, 4, 128), (3, 32, 8, 128),
-                                           (4, 4, 4, 64), (5, 14, 2, 64), (6, 64, 1, 128), (7, 16, 1, 64)])
+                                           (4, 4, 4, 64), (5, 14, 2, 64), (6, 64, 1, 128), (7, 16, 1, 64),
+                                           (8, 15, 5, 128), (9, 10, 2, 64), (14, 40, 8, 128)])
 def test_random_trees_full(seed, hq, hkv, d):
     wl = W.random_tree(seed, W.Shape(hq, hkv, d), n_roots=3, depth=3, max_branch=3, max_step=70)
     compare(wl, 0)
