@@ -183,8 +183,11 @@ typedef struct tkv_plan tkv_plan;
  *   candidates per row (nullable: all 1; used for accounting only).
  * The planner finds the blocks that several rows share (a trie over the tables).  Rows whose own
  * query tile is small (q_len * G < 64: decode rows and short verify rows) go through the shared
- * segments, so that each shared K/V block is contracted once against all of those rows' query
- * tokens.  A longer verify row fills 128-row tiles of its own tokens, each walking the row's whole
+ * segments: the rows that share a segment contract its K/V blocks together, in tiles of up to 128
+ * query rows (workgroup kernel) or 16-32 (wave kernel), so that a block is read once per tile rather
+ * than once per row (a short segment whose child segments all take 128-row tiles is read as the head
+ * of each child's key run instead; option fold_blocks).  A longer verify row fills 128-row tiles of
+ * its own tokens, each walking the row's whole
  * path: its shared context is then read once per tile (mostly from L2: tiles of one context are
  * launched together on one XCD), which costs no extra arithmetic, since every query token needs
  * its own dot products with every context key either way.  Long runs are split, and descriptors
